@@ -1,0 +1,196 @@
+"""LightBeam CPU oracle -- TEST INFRASTRUCTURE ONLY.
+
+Python wrapper (ctypes) around ``oracle.cpp``, a plain single-threaded fp64
+implementation of the decoding method of LightBeam (arXiv 2603.14002, Alg. 1,
+Eq. (1), Eq. (2), App. E).  Only the test suite, the smoke check and the
+benchmark's CPU-baseline leg may import this package; the HIP decoder never
+does.  ``build()`` compiles ``liboracle.so`` with g++.
+
+Every function of the oracle is pinned by tests that do not re-type it:
+brute-force enumeration of CTC alignments, the CTC forward algorithm of
+``torch.nn.functional.ctc_loss``, probability conservation, hand-computed
+backoff values, a published SplitMix64 output and special cases (fusion
+identity, greedy homophones).
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from dataclasses import dataclass
+from typing import List, Optional
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "oracle.cpp")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+MARGIN_NAMES = ("topk", "theta", "homophone", "lambda", "fusion", "ranking")
+
+
+def build(force: bool = True) -> str:
+    """Compile liboracle.so (g++, -O2, no FP contraction)."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + ".tmp"
+        subprocess.check_call(["g++", "-O2", "-std=c++17", "-fPIC", "-shared", "-ffp-contract=off",
+                               "-fno-fast-math", "-o", tmp, _SRC])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+class _Params(ctypes.Structure):
+    _fields_ = [("beam", ctypes.c_int32), ("subbeams", ctypes.c_int32),
+                ("alpha", ctypes.c_double), ("beta", ctypes.c_double), ("gamma", ctypes.c_double),
+                ("omega", ctypes.c_double), ("phi", ctypes.c_double), ("theta", ctypes.c_double),
+                ("lam", ctypes.c_double),
+                ("fusion_interval", ctypes.c_int32), ("fusion_top_f", ctypes.c_int32),
+                ("fusion_mode", ctypes.c_int32), ("pad_", ctypes.c_int32),
+                ("fusion_seed", ctypes.c_uint64),
+                ("fusion_lo", ctypes.c_double), ("fusion_hi", ctypes.c_double)]
+
+
+_lib = None
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+            build(force=True)
+        lib = ctypes.CDLL(_LIB)
+        P = ctypes.c_void_p
+        lib.orc_create.restype = P
+        lib.orc_create.argtypes = [ctypes.c_int32, P, P, ctypes.c_int32, ctypes.c_int32,
+                                   ctypes.c_int32, P] + [P] * 11
+        lib.orc_destroy.argtypes = [P]
+        lib.orc_last_error.restype = ctypes.c_char_p
+        lib.orc_decode.restype = ctypes.c_int32
+        lib.orc_decode.argtypes = [P, ctypes.POINTER(_Params), P, ctypes.c_int32, ctypes.c_int32,
+                                   ctypes.c_int32, ctypes.c_int32] + [P] * 10
+        lib.orc_log10p.restype = ctypes.c_double
+        lib.orc_log10p.argtypes = [P, P, ctypes.c_int32, ctypes.c_int32]
+        lib.orc_fusion_score.restype = ctypes.c_double
+        lib.orc_fusion_score.argtypes = [P, ctypes.POINTER(_Params), P, ctypes.c_int32]
+        lib.orc_splitmix64.restype = ctypes.c_uint64
+        lib.orc_splitmix64.argtypes = [ctypes.c_uint64]
+        lib.orc_prefix_key.restype = ctypes.c_uint64
+        lib.orc_prefix_key.argtypes = [P, ctypes.c_int32]
+        _lib = lib
+    return _lib
+
+
+def _ptr(a: Optional[np.ndarray]):
+    return None if a is None else ctypes.c_void_p(a.ctypes.data)
+
+
+@dataclass
+class OracleResult:
+    words: List[List[int]]      # best sub-beam word ids, per ranked hypothesis
+    total: np.ndarray           # float64 [n]
+    acoustic: np.ndarray        # float64 [n]
+    labels: List[List[int]]     # collapsed symbol sequences
+    keys: np.ndarray            # uint64 [n]
+    margins: dict               # min decision margins
+    frame_lse: Optional[np.ndarray]
+    stats: dict
+
+    @property
+    def min_margin(self) -> float:
+        return float(min(self.margins.values()))
+
+
+def params_from(p, fusion_seed: int = 0, fusion_mode: int = 0, **overrides) -> _Params:
+    """orc params from a ``workloads.DecodeParams`` (plus overrides)."""
+    d = dict(beam=p.beam, subbeams=p.subbeams, alpha=p.alpha, beta=p.beta, gamma=p.gamma,
+             omega=p.omega, phi=p.phi, theta=p.theta, lam=p.lam,
+             fusion_interval=p.fusion_interval, fusion_top_f=p.fusion_top_f,
+             fusion_mode=fusion_mode, pad_=0, fusion_seed=fusion_seed,
+             fusion_lo=p.fusion_lo, fusion_hi=p.fusion_hi)
+    d.update(overrides)
+    return _Params(**d)
+
+
+class Oracle:
+    """Holds a lexicon + LM copy inside the C++ oracle.  Thread-safe decode."""
+
+    def __init__(self, lexicon, lm):
+        lib = _load()
+        self._keep = []
+        offs = np.ascontiguousarray(lexicon.offsets, dtype=np.int32)
+        phs = np.ascontiguousarray(lexicon.phonemes, dtype=np.int32)
+        counts = np.array(lm.counts, dtype=np.int64)
+        ids = [np.ascontiguousarray(a, dtype=np.int32) for a in lm.ids]
+        lp = [np.ascontiguousarray(a, dtype=np.float32) for a in lm.logp]
+        bo = [np.ascontiguousarray(a, dtype=np.float32) for a in lm.bo[:3]]
+        self._h = lib.orc_create(int(lexicon.n_words), _ptr(offs), _ptr(phs), int(lm.vocab_size),
+                                 int(lm.bos), int(lm.unk), _ptr(counts),
+                                 _ptr(ids[0]), _ptr(lp[0]), _ptr(bo[0]),
+                                 _ptr(ids[1]), _ptr(lp[1]), _ptr(bo[1]),
+                                 _ptr(ids[2]), _ptr(lp[2]), _ptr(bo[2]),
+                                 _ptr(ids[3]), _ptr(lp[3]))
+        if not self._h:
+            raise RuntimeError("oracle create failed: " + lib.orc_last_error().decode())
+        self.lib = lib
+
+    def close(self):
+        if getattr(self, "_h", None):
+            self.lib.orc_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def decode(self, logits: np.ndarray, params: _Params, max_hyps: int = 4096,
+               max_words: int = 512, max_labels: int = 2048,
+               frame_lse: bool = False) -> OracleResult:
+        lg = np.ascontiguousarray(logits, dtype=np.float32)
+        T = int(lg.shape[0])
+        assert lg.ndim == 2 and lg.shape[1] == 41
+        words = np.empty((max_hyps, max_words), np.int32)
+        nwords = np.empty(max_hyps, np.int32)
+        tot = np.empty(max_hyps, np.float64)
+        ac = np.empty(max_hyps, np.float64)
+        labels = np.empty((max_hyps, max_labels), np.int32)
+        nlabels = np.empty(max_hyps, np.int32)
+        keys = np.empty(max_hyps, np.uint64)
+        margins = np.empty(6, np.float64)
+        flse = np.empty(max(T, 1), np.float64) if frame_lse else None
+        stats = np.empty(4, np.int64)
+        n = self.lib.orc_decode(self._h, ctypes.byref(params), _ptr(lg), T, max_hyps, max_words,
+                                max_labels, _ptr(words), _ptr(nwords), _ptr(tot), _ptr(ac),
+                                _ptr(labels), _ptr(nlabels), _ptr(keys), _ptr(margins),
+                                _ptr(flse), _ptr(stats))
+        if n < 0:
+            raise RuntimeError("oracle decode failed: " + self.lib.orc_last_error().decode())
+        m = min(n, max_hyps)
+        return OracleResult(
+            words=[list(words[i, :min(nwords[i], max_words)]) for i in range(m)],
+            total=tot[:m].copy(), acoustic=ac[:m].copy(),
+            labels=[list(labels[i, :min(nlabels[i], max_labels)]) for i in range(m)],
+            keys=keys[:m].copy(),
+            margins=dict(zip(MARGIN_NAMES, margins.tolist())),
+            frame_lse=None if flse is None else flse[:T].copy(),
+            stats=dict(expansions=int(stats[0]), word_events=int(stats[1]),
+                       lm_queries=int(stats[2]), fused=int(stats[3])))
+
+    def log10p(self, ctx, w: int) -> float:
+        c = np.ascontiguousarray(list(ctx) or [0], dtype=np.int32)
+        return float(self.lib.orc_log10p(self._h, _ptr(c), len(ctx), int(w)))
+
+    def fusion_score(self, params: _Params, words) -> float:
+        a = np.ascontiguousarray(list(words) or [0], dtype=np.int32)
+        return float(self.lib.orc_fusion_score(self._h, ctypes.byref(params), _ptr(a), len(words)))
+
+
+def splitmix64(x: int) -> int:
+    return int(_load().orc_splitmix64(ctypes.c_uint64(x & (2**64 - 1))))
+
+
+def prefix_key(y) -> int:
+    a = np.ascontiguousarray(list(y) or [0], dtype=np.int32)
+    return int(_load().orc_prefix_key(_ptr(a), len(y)))
