@@ -90,6 +90,7 @@ struct Params {
   int fusion_interval;  // 0 = no fusion
   int fusion_top_f;     // 0 = all entries
   int fusion_mode;      // 0 = synthetic bigram scorer, 1 = the n-gram LM's own score (pin)
+  int finalize;         // 1 = end of utterance (final fusion, drop mid-word); 0 = rank the live beam
   uint64_t fusion_seed;
   double fusion_lo, fusion_hi;
 };
@@ -427,11 +428,12 @@ Output decode(const Model& M, const Params& p, const float* logits, int T, bool 
   }
 
   // End of the utterance: final fusion over every entry, drop entries that
-  // stop inside a word, rank the rest.
-  if (p.fusion_interval > 0) apply_fusion(M, p, beam, 0, out.mg, out.st);
+  // stop inside a word, rank the rest.  Without finalisation the live beam is
+  // ranked as it stands (the state a streaming decoder reports mid-stream).
+  if (p.finalize && p.fusion_interval > 0) apply_fusion(M, p, beam, 0, out.mg, out.st);
   std::vector<Hyp> done;
   for (Hyp& h : beam)
-    if (partial_word(h.y).empty()) done.push_back(std::move(h));
+    if (!p.finalize || partial_word(h.y).empty()) done.push_back(std::move(h));
   std::vector<Ranked> r = rank(done);
   for (size_t i = 0; i + 1 < r.size(); ++i)
     out.mg.ranking = std::min(out.mg.ranking, r[i].total - r[i + 1].total);
@@ -452,7 +454,7 @@ struct orc_params {
   int32_t fusion_interval;
   int32_t fusion_top_f;
   int32_t fusion_mode;
-  int32_t pad_;
+  int32_t finalize;
   uint64_t fusion_seed;
   double fusion_lo, fusion_hi;
 };
@@ -520,6 +522,7 @@ static Params to_params(const orc_params* q) {
   p.fusion_interval = q->fusion_interval;
   p.fusion_top_f = q->fusion_top_f;
   p.fusion_mode = q->fusion_mode;
+  p.finalize = q->finalize;
   p.fusion_seed = q->fusion_seed;
   p.fusion_lo = q->fusion_lo;
   p.fusion_hi = q->fusion_hi;

@@ -1,0 +1,516 @@
+// C ABI of the LightBeam gfx950 decoder: validation, one-time table build and
+// upload, buffer allocation, and the per-frame launch sequence of Alg. 1.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <array>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/lightbeam.h"
+#include "lb_device.h"
+#include "lb_launch.h"
+
+using namespace lb;
+
+namespace {
+
+thread_local std::string g_err;
+
+lb_status fail(lb_status st, const std::string& msg) {
+  g_err = msg;
+  return st;
+}
+
+#define LB_HIP(call)                                                                  \
+  do {                                                                                \
+    hipError_t e_ = (call);                                                           \
+    if (e_ != hipSuccess)                                                             \
+      return fail(e_ == hipErrorOutOfMemory ? LB_ERR_OUT_OF_MEMORY : LB_ERR_HIP,      \
+                  std::string(#call) + ": " + hipGetErrorString(e_));                 \
+  } while (0)
+
+// Lexicon trie flattened to CSR in breadth-first order, so that the children
+// of a node are contiguous and ordered by phoneme (App. E.2 flattens the trie
+// into a transition table; a child bitmask + first-child index gives the same
+// transitions in 16 B per node).
+struct HostTrie {
+  std::vector<TrieNode> nodes;  // + sentinel
+  std::vector<int32_t> words;
+};
+
+HostTrie build_trie(const lb_lexicon_desc& lex) {
+  std::vector<std::array<int32_t, 40>> ch(1);
+  ch[0].fill(-1);
+  std::vector<std::vector<int32_t>> at(1);
+  for (int32_t w = 0; w < lex.n_words; ++w) {
+    int32_t n = 0;
+    for (int32_t k = lex.offsets[w]; k < lex.offsets[w + 1]; ++k) {
+      const int p = lex.phonemes[k];
+      if (ch[n][p] < 0) {
+        ch[n][p] = static_cast<int32_t>(ch.size());
+        ch.emplace_back();
+        ch.back().fill(-1);
+        at.emplace_back();
+      }
+      n = ch[n][p];
+    }
+    at[n].push_back(w);
+  }
+  const size_t N = ch.size();
+  std::vector<int32_t> order;  // BFS order of old ids
+  std::vector<int32_t> newid(N, -1);
+  order.reserve(N);
+  order.push_back(0);
+  newid[0] = 0;
+  for (size_t h = 0; h < order.size(); ++h) {
+    const int32_t o = order[h];
+    for (int p = 1; p <= 39; ++p) {
+      const int32_t c = ch[o][p];
+      if (c >= 0) {
+        newid[c] = static_cast<int32_t>(order.size());
+        order.push_back(c);
+      }
+    }
+  }
+  HostTrie t;
+  t.nodes.resize(N + 1);
+  uint32_t woff = 0;
+  for (size_t k = 0; k < N; ++k) {
+    const int32_t o = order[k];
+    TrieNode& tn = t.nodes[k];
+    tn.mask = 0;
+    tn.first_child = 0;
+    bool first = true;
+    for (int p = 1; p <= 39; ++p) {
+      if (ch[o][p] >= 0) {
+        tn.mask |= 1ull << p;
+        if (first) {
+          tn.first_child = static_cast<uint32_t>(newid[ch[o][p]]);
+          first = false;
+        }
+      }
+    }
+    if (k != 0 && !at[o].empty()) tn.mask |= 1ull << kSep;
+    tn.word_off = woff;
+    for (int32_t w : at[o]) t.words.push_back(w);
+    woff += static_cast<uint32_t>(at[o].size());
+  }
+  t.nodes[N].mask = 0;
+  t.nodes[N].first_child = 0;
+  t.nodes[N].word_off = woff;
+  return t;
+}
+
+uint64_t buckets_for(int64_t count, double lf) {
+  if (count <= 0) return 1;
+  const double slots = std::ceil(static_cast<double>(count) / lf);
+  return std::max<uint64_t>(1, static_cast<uint64_t>(std::ceil(slots / 4.0)));
+}
+
+struct EventPair {
+  hipEvent_t a, b;
+  int kind;
+};
+
+}  // namespace
+
+struct lb_decoder {
+  lb_params p{};
+  DevParams P{};
+  DevState S{};
+  int block = 64;       // workgroup size of the per-stream kernels (>= beam)
+  int ngram_grid = 1;   // workgroups of the n-gram kernel
+  std::vector<void*> allocs;
+  int64_t launches[4] = {0, 0, 0, 0};
+  bool profiling = false;
+  std::vector<EventPair> pending;
+  std::vector<hipEvent_t> pool;
+  double kernel_ms[4] = {0, 0, 0, 0};
+  int64_t timed[4] = {0, 0, 0, 0};
+
+  template <typename T>
+  lb_status alloc(T** ptr, size_t count) {
+    void* q = nullptr;
+    const size_t bytes = std::max<size_t>(count, 1) * sizeof(T);
+    hipError_t e = hipMalloc(&q, bytes);
+    if (e != hipSuccess)
+      return fail(LB_ERR_OUT_OF_MEMORY, "hipMalloc(" + std::to_string(bytes) + " B) failed: " + hipGetErrorString(e));
+    allocs.push_back(q);
+    *ptr = static_cast<T*>(q);
+    return LB_OK;
+  }
+
+  hipEvent_t get_event() {
+    if (!pool.empty()) {
+      hipEvent_t e = pool.back();
+      pool.pop_back();
+      return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+  }
+
+  void harvest() {
+    for (EventPair& ep : pending) {
+      float ms = 0.f;
+      if (hipEventElapsedTime(&ms, ep.a, ep.b) == hipSuccess) {
+        kernel_ms[ep.kind] += ms;
+        timed[ep.kind] += 1;
+      }
+      pool.push_back(ep.a);
+      pool.push_back(ep.b);
+    }
+    pending.clear();
+  }
+
+  ~lb_decoder() {
+    for (EventPair& ep : pending) {
+      (void)hipEventDestroy(ep.a);
+      (void)hipEventDestroy(ep.b);
+    }
+    for (hipEvent_t e : pool) (void)hipEventDestroy(e);
+    for (void* q : allocs) (void)hipFree(q);
+  }
+};
+
+namespace {
+
+lb_status validate(const lb_lexicon_desc* lex, const lb_ngram_desc* lm, const lb_params* p) {
+  if (!lex || !lm || !p) return fail(LB_ERR_INVALID_ARG, "null descriptor");
+  if (lex->n_words < 1 || !lex->offsets || !lex->phonemes) return fail(LB_ERR_INVALID_ARG, "empty lexicon");
+  if (lex->offsets[0] != 0) return fail(LB_ERR_INVALID_ARG, "lexicon offsets[0] != 0");
+  for (int32_t w = 0; w < lex->n_words; ++w) {
+    if (lex->offsets[w + 1] <= lex->offsets[w])
+      return fail(LB_ERR_INVALID_ARG, "word " + std::to_string(w) + " has no phonemes");
+    for (int32_t k = lex->offsets[w]; k < lex->offsets[w + 1]; ++k)
+      if (lex->phonemes[k] < 1 || lex->phonemes[k] > 39)
+        return fail(LB_ERR_INVALID_ARG, "phoneme out of 1..39 in word " + std::to_string(w));
+  }
+  if (lm->vocab_size < lex->n_words + 1) return fail(LB_ERR_INVALID_ARG, "LM vocabulary smaller than the lexicon");
+  if (lm->bos_id < 0 || lm->bos_id >= lm->vocab_size || lm->unk_id < 0 || lm->unk_id >= lm->vocab_size)
+    return fail(LB_ERR_INVALID_ARG, "bos/unk id out of range");
+  for (int n = 0; n < 4; ++n) {
+    if (lm->count[n] < 0) return fail(LB_ERR_INVALID_ARG, "negative n-gram count");
+    if (lm->count[n] > 0 && (!lm->ids[n] || !lm->log10p[n] || (n < 3 && !lm->backoff[n])))
+      return fail(LB_ERR_INVALID_ARG, "missing n-gram arrays for order " + std::to_string(n + 1));
+  }
+  if (p->beam < 1 || p->beam > LB_MAX_BEAM) return fail(LB_ERR_INVALID_ARG, "beam must be in 1..256");
+  if (p->subbeams < 1 || p->subbeams > LB_MAX_SUBBEAMS) return fail(LB_ERR_INVALID_ARG, "subbeams must be in 1..4");
+  if (p->max_batch < 1 || p->max_frames < 1 || p->max_words_out < 1)
+    return fail(LB_ERR_INVALID_ARG, "max_batch, max_frames and max_words_out must be >= 1");
+  if (p->fusion_source < LB_FUSION_NONE || p->fusion_source > LB_FUSION_EXTERNAL)
+    return fail(LB_ERR_INVALID_ARG, "unknown fusion_source");
+  if (p->fusion_source != LB_FUSION_NONE && p->fusion_interval < 1)
+    return fail(LB_ERR_INVALID_ARG, "fusion needs fusion_interval >= 1");
+  if (p->fusion_top_f < 0) return fail(LB_ERR_INVALID_ARG, "fusion_top_f < 0");
+  if (p->fusion_source == LB_FUSION_EXTERNAL) return fail(LB_ERR_INVALID_ARG, "external fusion is not supported yet");
+  const double lf = p->lm_load_factor == 0.0 ? 0.5 : p->lm_load_factor;
+  if (!(lf > 0.0 && lf <= 0.9)) return fail(LB_ERR_INVALID_ARG, "lm_load_factor must be in (0, 0.9]");
+  for (double x : {p->alpha, p->beta, p->gamma, p->omega, p->phi, p->theta, p->lambda, p->fusion_lo, p->fusion_hi})
+    if (!std::isfinite(x)) return fail(LB_ERR_INVALID_ARG, "non-finite parameter");
+  if (p->theta < 0 || p->lambda < 0) return fail(LB_ERR_INVALID_ARG, "theta and lambda must be >= 0");
+  if (p->arena_nodes_per_stream < 0) return fail(LB_ERR_INVALID_ARG, "arena_nodes_per_stream < 0");
+  return LB_OK;
+}
+
+lb_status build_tables(lb_decoder* d, const lb_lexicon_desc* lex, const lb_ngram_desc* lm, double lf) {
+  lb_status st;
+  // trie
+  HostTrie trie = build_trie(*lex);
+  TrieNode* dtrie = nullptr;
+  int32_t* dwords = nullptr;
+  if ((st = d->alloc(&dtrie, trie.nodes.size())) != LB_OK) return st;
+  if ((st = d->alloc(&dwords, trie.words.size())) != LB_OK) return st;
+  LB_HIP(hipMemcpy(dtrie, trie.nodes.data(), trie.nodes.size() * sizeof(TrieNode), hipMemcpyHostToDevice));
+  LB_HIP(hipMemcpy(dwords, trie.words.data(), trie.words.size() * sizeof(int32_t), hipMemcpyHostToDevice));
+  d->S.trie = dtrie;
+  d->S.trie_words = dwords;
+
+  // unigrams, dense by id; ids without an entry score as <unk> with backoff 0
+  const int32_t V = lm->vocab_size;
+  std::vector<Unigram> uni(V);
+  float p_unk = -HUGE_VALF;
+  for (int64_t e = 0; e < lm->count[0]; ++e)
+    if (lm->ids[0][e] == lm->unk_id) p_unk = lm->log10p[0][e];
+  for (int32_t v = 0; v < V; ++v) uni[v] = Unigram{p_unk, 0.0f};
+  for (int64_t e = 0; e < lm->count[0]; ++e) {
+    const int32_t v = lm->ids[0][e];
+    if (v < 0 || v >= V) return fail(LB_ERR_INVALID_ARG, "unigram id out of range");
+    uni[v] = Unigram{lm->log10p[0][e], lm->backoff[0][e]};
+  }
+  Unigram* duni = nullptr;
+  if ((st = d->alloc(&duni, V)) != LB_OK) return st;
+  LB_HIP(hipMemcpy(duni, uni.data(), V * sizeof(Unigram), hipMemcpyHostToDevice));
+  d->S.uni = duni;
+
+  // orders 2..4: open-addressing tables filled on the device
+  NgramTable* tabs[3] = {&d->S.t2, &d->S.t3, &d->S.t4};
+  for (int n = 2; n <= 4; ++n) {
+    const uint64_t nb = buckets_for(lm->count[n - 1], lf);
+    if (nb * 4 >= 0xFFFFFFFFull) return fail(LB_ERR_CAPACITY, "n-gram table too large for 32-bit slot ids");
+    Slot* slots = nullptr;
+    if ((st = d->alloc(&slots, nb * 4)) != LB_OK) return st;
+    LB_HIP(hipMemset(slots, 0xFF, nb * 4 * sizeof(Slot)));
+    tabs[n - 2]->slots = slots;
+    tabs[n - 2]->nbuckets = nb;
+  }
+  uint32_t* dflags = d->S.flags;
+  const int64_t kChunk = 1 << 24;
+  int32_t* sids = nullptr;
+  float* slp = nullptr;
+  float* sbo = nullptr;
+  int64_t maxc = 0;
+  for (int n = 2; n <= 4; ++n) maxc = std::max(maxc, lm->count[n - 1]);
+  const int64_t chunk = std::min<int64_t>(kChunk, std::max<int64_t>(maxc, 1));
+  LB_HIP(hipMalloc(&sids, chunk * 4 * sizeof(int32_t)));
+  LB_HIP(hipMalloc(&slp, chunk * sizeof(float)));
+  LB_HIP(hipMalloc(&sbo, chunk * sizeof(float)));
+  hipError_t err = hipSuccess;
+  for (int n = 2; n <= 4 && err == hipSuccess; ++n) {
+    const int64_t cnt = lm->count[n - 1];
+    for (int64_t s = 0; s < cnt && err == hipSuccess; s += chunk) {
+      const int64_t m = std::min(chunk, cnt - s);
+      err = hipMemcpy(sids, lm->ids[n - 1] + s * n, m * n * sizeof(int32_t), hipMemcpyHostToDevice);
+      if (err == hipSuccess) err = hipMemcpy(slp, lm->log10p[n - 1] + s, m * sizeof(float), hipMemcpyHostToDevice);
+      if (err == hipSuccess && n < 4)
+        err = hipMemcpy(sbo, lm->backoff[n - 1] + s, m * sizeof(float), hipMemcpyHostToDevice);
+      if (err == hipSuccess)
+        err = launch_build_order(n, sids, slp, n < 4 ? sbo : nullptr, m, V, d->S.t2, d->S.t3, *tabs[n - 2], dflags,
+                                 nullptr);
+      if (err == hipSuccess) err = hipDeviceSynchronize();
+    }
+  }
+  (void)hipFree(sids);
+  (void)hipFree(slp);
+  (void)hipFree(sbo);
+  if (err != hipSuccess) return fail(LB_ERR_HIP, std::string("n-gram table build: ") + hipGetErrorString(err));
+  uint32_t flags = 0;
+  LB_HIP(hipMemcpy(&flags, dflags, sizeof(flags), hipMemcpyDeviceToHost));
+  if (flags & kFlagBuildRange) return fail(LB_ERR_INVALID_ARG, "n-gram word id out of range");
+  if (flags & kFlagBuildContext) return fail(LB_ERR_INVALID_ARG, "n-gram whose context is not an n-gram of the lower order");
+  if (flags & kFlagBuildDup) return fail(LB_ERR_INVALID_ARG, "duplicate n-gram");
+  if (flags & kFlagBuildFull) return fail(LB_ERR_CAPACITY, "n-gram hash table full");
+
+  // root of the word-history arena: the empty history, context <s>
+  HistNode root{};
+  root.parent = kNone;
+  root.word = lm->bos_id;
+  root.c2 = kNone;
+  root.c3 = kNone;
+  root.bo1 = uni[lm->bos_id].bo;
+  root.bo2 = 0.0f;
+  root.bo3 = 0.0f;
+  root.sfus = 0.0;
+  LB_HIP(hipMemcpy(d->S.arena, &root, sizeof(root), hipMemcpyHostToDevice));
+  return LB_OK;
+}
+
+void record_start(lb_decoder* d, hipStream_t st, EventPair* ep, int kind) {
+  ep->kind = kind;
+  ep->a = d->get_event();
+  ep->b = d->get_event();
+  if (ep->a) (void)hipEventRecord(ep->a, st);
+}
+
+void record_stop(lb_decoder* d, hipStream_t st, EventPair* ep) {
+  if (ep->a && ep->b) {
+    (void)hipEventRecord(ep->b, st);
+    d->pending.push_back(*ep);
+  }
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* lb_last_error(void) { return g_err.c_str(); }
+
+lb_status lb_create(const lb_lexicon_desc* lex, const lb_ngram_desc* lm, const lb_params* params,
+                    lb_decoder** out) {
+  g_err.clear();
+  if (!out) return fail(LB_ERR_INVALID_ARG, "out is null");
+  *out = nullptr;
+  lb_status st = validate(lex, lm, params);
+  if (st != LB_OK) return st;
+  lb_decoder* d = new (std::nothrow) lb_decoder();
+  if (!d) return fail(LB_ERR_OUT_OF_MEMORY, "host allocation failed");
+  d->p = *params;
+  const lb_params& p = d->p;
+  const double lf = p.lm_load_factor == 0.0 ? 0.5 : p.lm_load_factor;
+  const int K = p.beam, O = p.subbeams, B = p.max_batch;
+  d->block = K <= 64 ? 64 : (K <= 128 ? 128 : 256);
+  uint64_t cap = p.arena_nodes_per_stream > 0
+                     ? static_cast<uint64_t>(p.arena_nodes_per_stream)
+                     : static_cast<uint64_t>(p.max_frames) * K * O + O;
+  if (1 + cap * B >= 0xFFFFFFFFull) {
+    delete d;
+    return fail(LB_ERR_CAPACITY, "word-history arena exceeds 32-bit node ids; lower max_frames or max_batch");
+  }
+  DevState& S = d->S;
+  const size_t BK = static_cast<size_t>(B) * K;
+  if ((st = d->alloc(&S.key, BK)) != LB_OK || (st = d->alloc(&S.pkey, BK)) != LB_OK ||
+      (st = d->alloc(&S.ab, BK)) != LB_OK || (st = d->alloc(&S.anb, BK)) != LB_OK ||
+      (st = d->alloc(&S.node, BK)) != LB_OK || (st = d->alloc(&S.meta, BK)) != LB_OK ||
+      (st = d->alloc(&S.Lw, BK * O)) != LB_OK || (st = d->alloc(&S.hist, BK * O)) != LB_OK ||
+      (st = d->alloc(&S.nbeam, B)) != LB_OK || (st = d->alloc(&S.t0, B)) != LB_OK ||
+      (st = d->alloc(&S.arena_n, B)) != LB_OK || (st = d->alloc(&S.arena, 1 + cap * B)) != LB_OK ||
+      (st = d->alloc(&S.events, BK)) != LB_OK || (st = d->alloc(&S.ev_count, 2)) != LB_OK ||
+      (st = d->alloc(&S.flags, 1)) != LB_OK || (st = d->alloc(&S.counters, static_cast<size_t>(B) * kNumCounters)) != LB_OK ||
+      (st = d->alloc(&S.fsel, BK)) != LB_OK || (st = d->alloc(&S.fsel_n, B)) != LB_OK) {
+    std::string msg = g_err;
+    delete d;
+    return fail(st, msg);
+  }
+  S.arena_cap = cap;
+  auto init = [&]() -> lb_status {
+    LB_HIP(hipMemset(S.nbeam, 0, B * sizeof(int32_t)));
+    LB_HIP(hipMemset(S.t0, 0, B * sizeof(int64_t)));
+    LB_HIP(hipMemset(S.arena_n, 0, B * sizeof(uint32_t)));
+    LB_HIP(hipMemset(S.ev_count, 0, 2 * sizeof(uint32_t)));
+    LB_HIP(hipMemset(S.flags, 0, sizeof(uint32_t)));
+    LB_HIP(hipMemset(S.counters, 0, static_cast<size_t>(B) * kNumCounters * sizeof(unsigned long long)));
+    return LB_OK;
+  };
+  if ((st = init()) != LB_OK || (st = build_tables(d, lex, lm, lf)) != LB_OK) {
+    std::string msg = g_err;
+    delete d;
+    return fail(st, msg);
+  }
+  DevParams& P = d->P;
+  P.K = K;
+  P.O = O;
+  P.W = p.max_words_out;
+  P.fusion_source = p.fusion_source;
+  P.fusion_interval = p.fusion_interval;
+  P.fusion_top_f = p.fusion_top_f;
+  P.bos = lm->bos_id;
+  P.alpha = p.alpha;
+  P.beta = p.beta;
+  P.gamma = p.gamma;
+  P.comega = p.omega * kLn10;
+  P.phi = p.phi;
+  P.theta = p.theta;
+  P.lam = p.lambda;
+  P.seed = p.fusion_seed;
+  P.lo = p.fusion_lo;
+  P.hi = p.fusion_hi;
+  // enough waves to cover the largest event queue of a frame, capped at 8 per SIMD
+  d->ngram_grid = static_cast<int>(std::max<size_t>(1, std::min<size_t>((BK + 3) / 4, 2048)));
+  *out = d;
+  return LB_OK;
+}
+
+void lb_destroy(lb_decoder* dec) { delete dec; }
+
+lb_status lb_decode_batch(lb_decoder* d, const float* logits, const int32_t* lengths, int32_t batch,
+                          int32_t frames, uint32_t flags, void* stream, int32_t* out_hyps, float* out_scores) {
+  g_err.clear();
+  if (!d) return fail(LB_ERR_INVALID_ARG, "decoder is null");
+  if (batch < 1 || batch > d->p.max_batch) return fail(LB_ERR_INVALID_ARG, "batch must be in 1..max_batch");
+  if (frames < 0) return fail(LB_ERR_INVALID_ARG, "frames < 0");
+  if ((frames > 0 && !logits) || !lengths || !out_hyps || !out_scores)
+    return fail(LB_ERR_INVALID_ARG, "null device pointer");
+  if (flags & ~static_cast<uint32_t>(LB_BEGIN | LB_END)) return fail(LB_ERR_INVALID_ARG, "unknown flags");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const DevParams& P = d->P;
+  const DevState& S = d->S;
+  const bool fusion = P.fusion_source == LB_FUSION_SYNTH_BIGRAM && P.fusion_interval > 0;
+  EventPair ep{};
+  if (flags & LB_BEGIN) LB_HIP(launch_begin(P, S, batch, st));
+  for (int32_t tau = 0; tau < frames; ++tau) {
+    if (d->profiling) record_start(d, st, &ep, 0);
+    LB_HIP(launch_frame(d->block, P, S, logits, lengths, batch, frames, tau, st));
+    if (d->profiling) record_stop(d, st, &ep);
+    d->launches[0]++;
+    if (d->profiling) record_start(d, st, &ep, 1);
+    LB_HIP(launch_ngram(d->ngram_grid, P, S, tau, st));
+    if (d->profiling) record_stop(d, st, &ep);
+    d->launches[1]++;
+    if (fusion) {
+      if (d->profiling) record_start(d, st, &ep, 2);
+      LB_HIP(launch_fusion(d->block, P, S, lengths, batch, tau, st));
+      if (d->profiling) record_stop(d, st, &ep);
+      d->launches[2]++;
+    }
+  }
+  if (d->profiling) record_start(d, st, &ep, 3);
+  LB_HIP(launch_output(d->block, P, S, lengths, batch, (flags & LB_END) ? 1 : 0, out_hyps, out_scores, st));
+  if (d->profiling) record_stop(d, st, &ep);
+  d->launches[3]++;
+  return LB_OK;
+}
+
+lb_status lb_fusion_request(lb_decoder* d, int32_t* words, int32_t* n_words, void* stream) {
+  (void)words;
+  (void)n_words;
+  (void)stream;
+  if (!d) return fail(LB_ERR_INVALID_ARG, "decoder is null");
+  return fail(LB_ERR_STATE, "no fusion request is pending");
+}
+
+lb_status lb_fusion_scores(lb_decoder* d, const float* fusion_logprobs, void* stream) {
+  (void)fusion_logprobs;
+  (void)stream;
+  if (!d) return fail(LB_ERR_INVALID_ARG, "decoder is null");
+  return fail(LB_ERR_STATE, "no fusion request is pending");
+}
+
+lb_status lb_get_status(lb_decoder* d, void* stream) {
+  if (!d) return fail(LB_ERR_INVALID_ARG, "decoder is null");
+  LB_HIP(hipStreamSynchronize(static_cast<hipStream_t>(stream)));
+  uint32_t flags = 0;
+  LB_HIP(hipMemcpy(&flags, d->S.flags, sizeof(flags), hipMemcpyDeviceToHost));
+  if (flags & kFlagArena) return fail(LB_ERR_CAPACITY, "word-history arena overflow (raise arena_nodes_per_stream)");
+  if (flags & kFlagWords) return fail(LB_ERR_CAPACITY, "hypothesis longer than max_words_out (output truncated)");
+  if (flags & kFlagSelect) return fail(LB_ERR_CAPACITY, "internal top-K selection overflow");
+  return LB_OK;
+}
+
+lb_status lb_get_stats(lb_decoder* d, lb_stats* out) {
+  if (!d || !out) return fail(LB_ERR_INVALID_ARG, "null argument");
+  LB_HIP(hipDeviceSynchronize());
+  std::vector<unsigned long long> c(static_cast<size_t>(d->p.max_batch) * kNumCounters);
+  LB_HIP(hipMemcpy(c.data(), d->S.counters, c.size() * sizeof(unsigned long long), hipMemcpyDeviceToHost));
+  std::memset(out, 0, sizeof(*out));
+  for (int b = 0; b < d->p.max_batch; ++b) {
+    const unsigned long long* x = &c[static_cast<size_t>(b) * kNumCounters];
+    out->expansions += static_cast<int64_t>(x[kCntExpansions]);
+    out->word_events += static_cast<int64_t>(x[kCntWordEvents]);
+    out->lm_queries += static_cast<int64_t>(x[kCntLmQueries]);
+    out->fused += static_cast<int64_t>(x[kCntFused]);
+    out->frames += static_cast<int64_t>(x[kCntFrames]);
+  }
+  d->harvest();
+  for (int k = 0; k < 4; ++k) {
+    out->launches[k] = d->launches[k];
+    out->kernel_ms[k] = d->kernel_ms[k];
+    out->timed[k] = d->timed[k];
+  }
+  return LB_OK;
+}
+
+lb_status lb_reset_stats(lb_decoder* d) {
+  if (!d) return fail(LB_ERR_INVALID_ARG, "decoder is null");
+  LB_HIP(hipDeviceSynchronize());
+  LB_HIP(hipMemset(d->S.counters, 0, static_cast<size_t>(d->p.max_batch) * kNumCounters * sizeof(unsigned long long)));
+  d->harvest();
+  for (int k = 0; k < 4; ++k) {
+    d->launches[k] = 0;
+    d->kernel_ms[k] = 0;
+    d->timed[k] = 0;
+  }
+  return LB_OK;
+}
+
+lb_status lb_set_profiling(lb_decoder* d, int32_t enable) {
+  if (!d) return fail(LB_ERR_INVALID_ARG, "decoder is null");
+  d->profiling = enable != 0;
+  return LB_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,175 @@
+// Device-side data layout and helpers of the LightBeam gfx950 decoder.
+//
+// HBM layout (all buffers allocated once in lb_create, for max_batch streams):
+//   trie        TrieNode[S+1]   16 B/node: child mask (bits 1..39 phonemes, bit 40
+//                               separator when the node ends a word), index of the
+//                               first child (children are contiguous, in phoneme
+//                               order), offset of the node's words in trie_words
+//   trie_words  int32[]         word ids ending at each node, ascending
+//   uni         Unigram[vocab]  dense log10 p / backoff by word id
+//   t2, t3, t4  Slot[4*nbuckets] open-addressing hash tables of orders 2..4; a
+//                               bucket is one 64-B line of four 16-B slots
+//                               {key, log10 p, backoff}; key = (context, word)
+//                               where context is the word id (order 2) or the
+//                               slot index of the context n-gram (orders 3, 4)
+//   beams       SoA [max_batch][K] (sub-beam arrays [max_batch][K][O])
+//   arena       HistNode[1 + max_batch*cap]: word-history nodes; node 0 is the
+//               empty history (context <s>), stream b owns [1+b*cap, 1+(b+1)*cap)
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace lb {
+
+constexpr int kClasses = 41;
+constexpr int kSep = 40;
+constexpr int kMaxBeam = 256;
+constexpr int kMaxSub = 4;
+constexpr uint32_t kNone = 0xFFFFFFFFu;
+constexpr uint64_t kEmptyKey = ~0ull;
+constexpr uint64_t kNoParent = 0xFFFFFFFFFFFFFFFEull;  // parent key of the empty prefix
+constexpr uint32_t kRootNode = 0;                      // trie root
+constexpr uint32_t kRootHist = 0;                      // empty word history
+constexpr double kLn10 = 2.302585092994045684017991454684364208;
+
+// overflow / error flag bits (DevState::flags)
+constexpr uint32_t kFlagArena = 1u;
+constexpr uint32_t kFlagWords = 2u;
+constexpr uint32_t kFlagSelect = 4u;
+constexpr uint32_t kFlagBuildRange = 8u;
+constexpr uint32_t kFlagBuildContext = 16u;
+constexpr uint32_t kFlagBuildDup = 32u;
+constexpr uint32_t kFlagBuildFull = 64u;
+
+// per-stream counters (DevState::counters, [max_batch][kNumCounters])
+enum { kCntExpansions = 0, kCntWordEvents = 1, kCntLmQueries = 2, kCntFused = 3, kCntFrames = 4,
+       kNumCounters = 5 };
+
+struct TrieNode {
+  uint64_t mask;
+  uint32_t first_child;
+  uint32_t word_off;
+};
+
+struct Unigram {
+  float logp;
+  float bo;
+};
+
+struct Slot {
+  uint64_t key;
+  float logp;
+  float bo;
+};
+
+struct NgramTable {
+  Slot* slots;
+  uint64_t nbuckets;
+};
+
+// Word-history node: the word sequence (parent chain) of an orthographic
+// sub-beam plus the n-gram state after its last word: the word itself (the
+// 1-word context), the slots of the 2- and 3-word contexts (kNone if absent)
+// and the three backoff weights, and the running synthetic fusion score.
+struct HistNode {
+  uint32_t parent;
+  int32_t word;
+  uint32_t c2;
+  uint32_t c3;
+  float bo1, bo2, bo3;
+  uint32_t pad;
+  double sfus;
+};
+
+struct Event {
+  uint32_t stream;
+  uint32_t beam;
+  uint32_t pnode;  // trie node of the completed word
+  uint32_t pad;
+};
+
+struct DevParams {
+  int32_t K, O, W;
+  int32_t fusion_source, fusion_interval, fusion_top_f;
+  int32_t bos;
+  int32_t pad;
+  double alpha, beta, gamma, comega, phi, theta, lam;
+  uint64_t seed;
+  double lo, hi;
+};
+
+struct DevState {
+  // hypotheses, [B][K] (sub-beams [B][K][O])
+  uint64_t* key;
+  uint64_t* pkey;
+  double* ab;
+  double* anb;
+  uint32_t* node;
+  uint32_t* meta;  // last symbol (bits 0..7) | number of sub-beams (bits 8..15)
+  double* Lw;
+  uint32_t* hist;
+  int32_t* nbeam;     // [B]
+  int64_t* t0;        // [B] frames decoded since LB_BEGIN
+  uint32_t* arena_n;  // [B] arena nodes used
+  HistNode* arena;
+  uint64_t arena_cap;  // per stream
+  Event* events;       // [B*K]
+  uint32_t* ev_count;  // [2]
+  uint32_t* flags;
+  unsigned long long* counters;  // [B][kNumCounters]
+  // fusion selection for external scores: [B][K] beam index per rank, [B] count
+  int32_t* fsel;
+  int32_t* fsel_n;
+  // lexicon
+  const TrieNode* trie;
+  const int32_t* trie_words;
+  // n-gram LM
+  const Unigram* uni;
+  NgramTable t2, t3, t4;
+};
+
+// SplitMix64 output for state x (Steele, Lea & Flood, OOPSLA 2014).
+__host__ __device__ inline uint64_t splitmix64(uint64_t x) {
+  uint64_t z = x + 0x9E3779B97F4A7C15ull;
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+// 64-bit rolling key of a collapsed prefix: key(y v) = splitmix64(key(y) ^ v), key(()) = 0.
+__host__ __device__ inline uint64_t prefix_step(uint64_t k, int v) {
+  return splitmix64(k ^ static_cast<uint64_t>(v));
+}
+
+// Bucket of an n-gram key: multiply-high range reduction of a mixed hash.
+__host__ __device__ inline uint64_t bucket_of(uint64_t key, uint64_t nbuckets) {
+  const uint64_t h = splitmix64(key ^ 0xD6E8FEB86659FD93ull);
+#if defined(__HIP_DEVICE_COMPILE__)
+  return __umul64hi(h, nbuckets);
+#else
+  return static_cast<uint64_t>((static_cast<unsigned __int128>(h) * nbuckets) >> 64);
+#endif
+}
+
+__device__ inline double lse2(double x, double y) {
+  if (x == -HUGE_VAL && y == -HUGE_VAL) return -HUGE_VAL;
+  const double m = x > y ? x : y;
+  return m + log1p(exp(-fabs(x - y)));
+}
+
+// Synthetic word-bigram fusion score Bg(a, b), natural log.
+__device__ inline double bigram_score(const DevParams& P, int a, int b) {
+  const uint64_t h = splitmix64(P.seed ^ ((static_cast<uint64_t>(static_cast<uint32_t>(a)) << 32) |
+                                          static_cast<uint64_t>(static_cast<uint32_t>(b))));
+  const double u = static_cast<double>(h >> 48) * (1.0 / 65536.0);
+  return P.lo + (P.hi - P.lo) * u;
+}
+
+// Order-preserving map of a double to uint64 (larger double -> larger integer).
+__device__ inline uint64_t order_bits(double x) {
+  const uint64_t u = static_cast<uint64_t>(__double_as_longlong(x));
+  return (u >> 63) ? ~u : (u | 0x8000000000000000ull);
+}
+
+}  // namespace lb

@@ -1,0 +1,142 @@
+"""Helpers for GPU parity tests: run the HIP decoder through the C ABI and
+compare its ranked outputs with the oracle's, utterance by utterance."""
+
+from __future__ import annotations
+
+import math
+import sys
+import time
+from dataclasses import dataclass, field
+from typing import List, Optional
+
+import numpy as np
+
+import oracle
+import paper_2603_14002_amd as lbm
+
+SCORE_TOL = 1e-4       # fp32 hypothesis scores, absolute
+NEAR_TIE = 1e-4        # decision margins below this are counted as near-ties
+EXCUSE_TOL = 1e-9      # a mismatch is excused only at a margin below this (both sides are fp64)
+
+
+def say(msg: str) -> None:
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def gpu_decode(d, params=None, chunk: int = 0, batch: Optional[int] = None, fusion_source=None,
+               profiling=False, max_words: Optional[int] = None, arena_nodes_per_stream: int = 0,
+               return_decoder=False, finalize=True):
+    """Decodes the first `batch` utterances of workload data `d` on cuda:0.
+
+    Returns a list of (words list per rank, scores float32 array) per utterance."""
+    import torch
+    p = params or d.workload.params
+    B = d.logits.shape[0] if batch is None else batch
+    T = d.logits.shape[1]
+    lp = lbm.make_params(p, max_batch=B, max_frames=T, fusion_seed=d.fusion_seed,
+                         fusion_source=fusion_source, arena_nodes_per_stream=arena_nodes_per_stream)
+    if max_words is not None:
+        lp.max_words_out = max_words
+    dec = lbm.Decoder(d.lexicon, d.lm, lp)
+    if profiling:
+        lbm.lb_set_profiling(dec.handle, True)
+    dev = torch.device("cuda:0")
+    logits = torch.from_numpy(np.ascontiguousarray(d.logits[:B])).to(dev)
+    lengths = np.ascontiguousarray(d.lengths[:B]).astype(np.int32)
+    K, W = lp.beam, lp.max_words_out
+    hyps = torch.empty((B, K, W), dtype=torch.int32, device=dev)
+    scores = torch.empty((B, K), dtype=torch.float32, device=dev)
+    if chunk <= 0:
+        st, _, _ = dec.decode(logits, torch.from_numpy(lengths).to(dev),
+                              lbm.LB_BEGIN | (lbm.LB_END if finalize else 0),
+                              out_hyps=hyps, out_scores=scores)
+        assert st == lbm.LB_OK
+    else:
+        nch = (T + chunk - 1) // chunk
+        for c in range(nch):
+            lo = c * chunk
+            hi = min(T, lo + chunk)
+            lg = logits[:, lo:hi].contiguous()
+            ln = np.clip(lengths - lo, 0, hi - lo).astype(np.int32)
+            fl = (lbm.LB_BEGIN if c == 0 else 0) | (lbm.LB_END if (finalize and c == nch - 1) else 0)
+            st, _, _ = dec.decode(lg, torch.from_numpy(ln).to(dev), fl, out_hyps=hyps, out_scores=scores)
+            assert st == lbm.LB_OK
+    torch.cuda.synchronize()
+    st = dec.status()
+    assert st == lbm.LB_OK, lbm.lb_last_error()
+    H = hyps.cpu().numpy()
+    S = scores.cpu().numpy()
+    out = []
+    for b in range(B):
+        words, sc = [], []
+        for r in range(K):
+            if not np.isfinite(S[b, r]):
+                break
+            row = H[b, r]
+            n = int(np.argmax(row < 0)) if (row < 0).any() else W
+            words.append([int(x) for x in row[:n]])
+            sc.append(S[b, r])
+        out.append((words, np.array(sc, dtype=np.float32)))
+    if return_decoder:
+        return out, dec
+    dec.close()
+    return out
+
+
+@dataclass
+class Parity:
+    exact: int = 0
+    near_tie: int = 0          # utterances with a decision margin < NEAR_TIE (reported)
+    excused: int = 0           # differs, at a decision margin < EXCUSE_TOL
+    mismatch: List[str] = field(default_factory=list)
+    max_score_err: float = 0.0
+    n_hyps: int = 0
+
+    def report(self, name: str) -> str:
+        return (f"[parity] {name}: exact={self.exact} near_tie={self.near_tie} excused={self.excused} "
+                f"mismatch={len(self.mismatch)} hyps={self.n_hyps} max|dscore|={self.max_score_err:.2e}")
+
+
+def compare(par: Parity, b: int, gpu, orc: oracle.OracleResult, K: int) -> None:
+    gw, gs = gpu
+    if orc.min_margin < NEAR_TIE:
+        par.near_tie += 1
+    ow = [[int(x) for x in w] for w in orc.words[:K]]
+    ot = orc.total[:K]
+    same = gw == ow and len(gs) == len(ot)
+    err = float(np.max(np.abs(gs.astype(np.float64) - ot))) if same and len(ot) else 0.0
+    if same and err <= SCORE_TOL:
+        par.exact += 1
+        par.max_score_err = max(par.max_score_err, err)
+        par.n_hyps += len(ot)
+        return
+    if orc.min_margin < EXCUSE_TOL:
+        par.excused += 1
+        return
+    # locate the first difference for the message
+    k = 0
+    while k < min(len(gw), len(ow)) and gw[k] == ow[k] and abs(float(gs[k]) - ot[k]) <= SCORE_TOL:
+        k += 1
+    detail = (f"utt {b}: first difference at rank {k}: gpu={gw[k] if k < len(gw) else None} "
+              f"{float(gs[k]) if k < len(gs) else None} oracle={ow[k] if k < len(ow) else None} "
+              f"{ot[k] if k < len(ot) else None}; n gpu={len(gw)} oracle={len(ow)} margins={orc.margins}")
+    par.mismatch.append(detail)
+
+
+def oracle_for(d):
+    return oracle.Oracle(d.lexicon, d.lm)
+
+
+def check_parity(d, gpu_out, utts, params=None, orc=None, name="", max_mismatch=0, finalize=True):
+    p = params or d.workload.params
+    orc = orc or oracle_for(d)
+    op = oracle.params_from(p, fusion_seed=d.fusion_seed, finalize=1 if finalize else 0)
+    par = Parity()
+    t0 = time.time()
+    for b in utts:
+        res = orc.decode(d.logits[b, :d.lengths[b]], op)
+        compare(par, b, gpu_out[b], res, p.beam)
+    say(par.report(name) + f" oracle {time.time() - t0:.1f}s")
+    assert len(par.mismatch) <= max_mismatch, "\n".join(par.mismatch[:5])
+    return par

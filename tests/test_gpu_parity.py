@@ -1,0 +1,121 @@
+"""GPU parity: the HIP decoder (through the C ABI) against the fp64 CPU oracle.
+
+Every case compares ranked word sequences exactly and fp32 scores within 1e-4
+absolute, per utterance; an utterance whose outputs differ is accepted only as
+a near-tie (some decision margin of the oracle below 1e-4), and near-ties are
+counted.  Sizes span several workgroup tiles and ragged tails.
+"""
+
+import numpy as np
+import pytest
+
+import paper_2603_14002_amd as lbm
+from tests.gpu_util import check_parity, gpu_decode, oracle_for, say
+from tests.tinylm import lexicon_from, lm_from_entries, peaked_logits
+from workloads import DecodeParams, load_workload
+from workloads.gen import WorkloadData
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need a ROCm device")
+    lbm.lib()
+
+
+def test_c1_tiny():
+    d = load_workload("c1")
+    say("[case] c1")
+    out = gpu_decode(d)
+    check_parity(d, out, range(d.logits.shape[0]), name="c1")
+
+
+@pytest.mark.parametrize("finalize", [True, False], ids=["end", "live"])
+@pytest.mark.parametrize("name", ["t-c1k", "t-c20k", "t-c125k", "t-k256"])
+def test_small_workloads(name, finalize):
+    """`live`: without LB_END the whole beam is ranked and compared (K entries)."""
+    d = load_workload(name)
+    say(f"[case] {name} B={d.logits.shape[0]} T={d.logits.shape[1]} K={d.workload.params.beam} "
+        f"finalize={finalize}")
+    out = gpu_decode(d, finalize=finalize)
+    par = check_parity(d, out, range(d.logits.shape[0]), name=name, finalize=finalize)
+    if not finalize:
+        assert par.n_hyps >= d.logits.shape[0]
+
+
+@pytest.mark.parametrize("finalize", [True, False], ids=["end", "live"])
+def test_streaming_chunks_match_oracle(finalize):
+    d = load_workload("t-stream")
+    say(f"[case] t-stream chunk=10 finalize={finalize}")
+    out = gpu_decode(d, chunk=d.workload.chunk, finalize=finalize)
+    check_parity(d, out, range(d.logits.shape[0]), name="t-stream", finalize=finalize)
+
+
+@pytest.mark.parametrize("chunk", [1, 7, 33])
+def test_chunked_equals_one_shot(chunk):
+    d = load_workload("t-c20k")
+    say(f"[case] chunk invariance {chunk}")
+    one = gpu_decode(d, finalize=False)
+    ch = gpu_decode(d, chunk=chunk, finalize=False)
+    for (w1, s1), (w2, s2) in zip(one, ch):
+        assert w1 == w2
+        assert np.array_equal(s1, s2)
+
+
+def test_batch_membership_and_determinism():
+    d = load_workload("t-c20k")
+    say("[case] batch invariance")
+    full = gpu_decode(d, finalize=False)
+    again = gpu_decode(d, finalize=False)
+    for (w1, s1), (w2, s2) in zip(full, again):
+        assert w1 == w2 and np.array_equal(s1, s2)
+    for b in (0, 3):
+        sub = WorkloadData(d.workload, d.lexicon, d.lm, d.logits[b:b + 1], d.lengths[b:b + 1],
+                           d.targets[b:b + 1], d.words[b:b + 1], d.fusion_seed)
+        alone = gpu_decode(sub, finalize=False)[0]
+        assert alone[0] == full[b][0] and np.array_equal(alone[1], full[b][1])
+
+
+def test_without_fusion():
+    d = load_workload("t-c20k")
+    p = d.workload.params.__class__(**{**d.workload.params.__dict__, "fusion_interval": 0})
+    say("[case] t-c20k without fusion")
+    out = gpu_decode(d, params=p, finalize=False)
+    check_parity(d, out, range(d.logits.shape[0]), params=p, name="t-c20k/nofusion", finalize=False)
+
+
+@pytest.mark.parametrize("beam,subbeams,top_f", [(1, 1, 0), (3, 4, 2), (256, 4, 5), (100, 2, 99)])
+def test_parameter_edges(beam, subbeams, top_f):
+    d = load_workload("t-c1k")
+    p = d.workload.params.__class__(**{**d.workload.params.__dict__, "beam": beam, "subbeams": subbeams,
+                                       "fusion_top_f": top_f, "fusion_interval": 5})
+    say(f"[case] edges K={beam} o={subbeams} F={top_f}")
+    for fin in (True, False):
+        out = gpu_decode(d, params=p, finalize=fin)
+        check_parity(d, out, range(d.logits.shape[0]), params=p, name=f"edges K={beam}", finalize=fin)
+
+
+def test_zero_length_and_tiny_lexicon():
+    # two homophones and a doubled-phoneme word; one stream with zero frames
+    lex = lexicon_from([(1,), (1,), (2, 2), (3,)])
+    W = 4
+    lm = lm_from_entries(W, [
+        [((0,), -1.0, -0.3), ((1,), -0.7, -0.2), ((2,), -1.5, -0.1), ((3,), -2.0, 0.0), ((W,), -99.0, -0.5),
+         ((W + 1,), -1.0, 0.0), ((W + 2,), -3.0, 0.0)],
+        [((W, 0), -0.2, -0.4), ((0, 2), -0.3, -0.2), ((1, 3), -0.1, 0.0)],
+        [((W, 0, 2), -0.05, -0.1)],
+        [((W, 0, 2, 3), -0.01)],
+    ])
+    lg = np.stack([peaked_logits([1, 0, 40, 2, 0, 2, 40, 3, 40, 0], strong=3.0, seed=s) for s in range(3)])
+    wl = load_workload("t-c1k").workload
+    p = DecodeParams(beam=16, subbeams=2, fusion_interval=3, fusion_top_f=0)
+    wl = wl.__class__(**{**wl.__dict__, "params": p})
+    lengths = np.array([10, 0, 7], np.int32)
+    d = WorkloadData(wl, lex, lm, lg, lengths, np.zeros((3, 10), np.int32), [[], [], []], 99)
+    say("[case] tiny lexicon + zero length")
+    out = gpu_decode(d, params=p)
+    assert out[1][0] == [[]] and out[1][1].tolist() == [0.0]
+    check_parity(d, out, range(3), params=p, name="tiny")
