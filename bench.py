@@ -1,0 +1,209 @@
+"""Throughput of the MI355X LightBeam decoding path on one GPU.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c4]
+
+One step decodes one whole batch of the workload (LB_BEGIN | LB_END over all
+frames; streaming workloads are fed chunk by chunk) with the inputs already in
+HBM.  Prints ONE JSON line: beam-token expansions per second (value), decoded
+audio-seconds per wall-second, per-stream real-time factor, the HBM roofline of
+the dominant kernel (per-launch durations from HIP events recorded on the
+decode stream) and the CPU oracle timed on a bounded sample of the workload.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import threading
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "beam-token expansions/sec and decoded audio-sec per wall-sec (RTF) on 1 MI355X"
+HBM_PEAK_GBS = 8000.0
+LINE_BYTES = 64          # one hash-table bucket = one 64-B line
+KERNELS = ("frame", "ngram", "fusion", "output")
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", default="c4")
+    ap.add_argument("--cpu-sample", type=int, default=0,
+                    help="utterances decoded by the CPU oracle (0 = one per host thread, max 16)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-profile", action="store_true", help="skip per-kernel event timing")
+    return ap.parse_args()
+
+
+def cpu_baseline(d, n_utts: int, threads: int):
+    """The oracle, as it stands, on the first n_utts utterances (full length), one
+    utterance per host thread; returns expansions/s and the sample description."""
+    import oracle
+    t0 = time.time()
+    orc = oracle.Oracle(d.lexicon, d.lm)
+    log(f"oracle loaded in {time.time() - t0:.1f}s")
+    op = oracle.params_from(d.workload.params, fusion_seed=d.fusion_seed)
+    exps = [0] * n_utts
+    frames = [0] * n_utts
+    nxt = [0]
+    lock = threading.Lock()
+
+    def worker():
+        while True:
+            with lock:
+                b = nxt[0]
+                nxt[0] += 1
+            if b >= n_utts:
+                return
+            L = int(d.lengths[b])
+            r = orc.decode(d.logits[b, :L], op, max_hyps=d.workload.params.beam)
+            exps[b] = r.stats["expansions"]
+            frames[b] = L
+
+    t0 = time.time()
+    ths = [threading.Thread(target=worker) for _ in range(threads)]
+    for t in ths:
+        t.start()
+    for t in ths:
+        t.join()
+    wall = time.time() - t0
+    orc.close()
+    return dict(value=sum(exps) / wall, unit="beam-token expansions/s", cores=threads, kind="oracle",
+                sample=f"first {n_utts} utterances of {d.workload.name} (all frames), "
+                       f"one per thread on {threads} threads, {wall:.1f}s wall",
+                audio_sec_per_wall_sec=sum(frames) * 0.08 / wall)
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this decoder runs on one GPU; --gpus N>1 is not supported "
+                                   "(streams shard across GPUs with no exchange, see the design notes)"}))
+        sys.exit(2)
+    import torch
+
+    import paper_2603_14002_amd as lbm
+    from workloads import FRAME_SECONDS, load_workload
+
+    t0 = time.time()
+    d = load_workload(args.workload)
+    wl = d.workload
+    p = wl.params
+    B, T = d.logits.shape[:2]
+    log(f"workload {wl.name}: B={B} T={T} K={p.beam} lm={d.lm.counts} ({time.time() - t0:.1f}s)")
+    t0 = time.time()
+    lp = lbm.make_params(p, max_batch=B, max_frames=T, fusion_seed=d.fusion_seed)
+    dec = lbm.Decoder(d.lexicon, d.lm, lp)
+    log(f"lb_create {time.time() - t0:.1f}s")
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+    logits = torch.from_numpy(d.logits).to(dev)
+    lengths_np = d.lengths.astype(np.int32)
+    K, W = lp.beam, lp.max_words_out
+    hyps = torch.empty((B, K, W), dtype=torch.int32, device=dev)
+    scores = torch.empty((B, K), dtype=torch.float32, device=dev)
+    chunk = wl.chunk
+    if chunk > 0:
+        nch = (T + chunk - 1) // chunk
+        chunks = []
+        for c in range(nch):
+            lo, hi = c * chunk, min(T, (c + 1) * chunk)
+            ln = np.clip(lengths_np - lo, 0, hi - lo).astype(np.int32)
+            fl = (lbm.LB_BEGIN if c == 0 else 0) | (lbm.LB_END if c == nch - 1 else 0)
+            chunks.append((logits[:, lo:hi].contiguous(), torch.from_numpy(ln).to(dev), hi - lo, fl))
+    else:
+        chunks = [(logits, torch.from_numpy(lengths_np).to(dev), T, lbm.LB_BEGIN | lbm.LB_END)]
+
+    def step():
+        for lg, ln, tc, fl in chunks:
+            st = lbm.lb_decode_batch(dec.handle, lg, ln, B, tc, fl, stream, hyps, scores)
+            assert st == lbm.LB_OK
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    st = dec.status()
+    if st != lbm.LB_OK:
+        raise RuntimeError(lbm.lb_last_error())
+    lbm.lb_reset_stats(dec.handle)
+    if not args.no_profile:
+        lbm.lb_set_profiling(dec.handle, True)
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        step()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall_ms = ev0.elapsed_time(ev1)
+    s = lbm.lb_get_stats(dec.handle)
+    lbm.lb_set_profiling(dec.handle, False)
+    ms = wall_ms / args.steps
+    exp_per_step = s.expansions / args.steps
+    audio = float(lengths_np.sum()) * FRAME_SECONDS
+    value = exp_per_step / (ms / 1000.0)
+    kern = {}
+    for i, name in enumerate(KERNELS):
+        if s.timed[i]:
+            kern[name] = dict(launches=int(s.launches[i]), total_ms=s.kernel_ms[i],
+                              avg_us=1000.0 * s.kernel_ms[i] / s.timed[i])
+    roof = None
+    if kern:
+        dom = max(kern, key=lambda k: kern[k]["total_ms"])
+        if "ngram" in kern:
+            # the n-gram lookup phase: every probed 64-B bucket line is a random HBM read
+            per_launch_bytes = s.probe_lines * LINE_BYTES / max(1, kern["ngram"]["launches"])
+            achieved = per_launch_bytes / (kern["ngram"]["avg_us"] * 1e-6) / 1e9
+            roof = dict(kernel="k_ngram", bound="hbm", achieved=achieved, peak=HBM_PEAK_GBS, unit="GB/s",
+                        frac=achieved / HBM_PEAK_GBS, traffic=None,
+                        bytes_per_launch=per_launch_bytes, avg_launch_us=kern["ngram"]["avg_us"])
+        kern["dominant"] = dom
+    out = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "beam-token expansions/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f64",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "batch": B, "frames": T, "beam": p.beam, "subbeams": p.subbeams,
+                   "lexicon_words": d.lexicon.n_words, "ngrams": int(sum(d.lm.counts)),
+                   "fusion_interval": p.fusion_interval, "fusion_top_f": p.fusion_top_f,
+                   "chunk": chunk, "parallelism": "none (1 GPU)"},
+        "audio_sec_per_wall_sec": audio / (ms / 1000.0),
+        "rtf_per_stream": (ms / 1000.0) / (T * FRAME_SECONDS) if chunk == 0
+        else (ms / 1000.0) / len(chunks) / (chunk * FRAME_SECONDS),
+        "counters": {"expansions_per_step": exp_per_step, "word_events_per_step": s.word_events / args.steps,
+                     "lm_queries_per_step": s.lm_queries / args.steps, "fused_per_step": s.fused / args.steps,
+                     "probe_lines_per_step": s.probe_lines / args.steps},
+        "kernels": kern,
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        threads = min(os.cpu_count() or 1, 16)
+        n = args.cpu_sample or threads
+        out["cpu_baseline"] = cpu_baseline(d, min(n, B), threads)
+    dec.close()
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

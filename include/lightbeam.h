@@ -119,6 +119,7 @@ typedef struct lb_stats {
   int64_t lm_queries;   /* (sub-beam, homophone) n-gram queries                   */
   int64_t fused;        /* hypotheses rescored by delayed fusion                  */
   int64_t frames;       /* stream-frames decoded                                  */
+  int64_t probe_lines;  /* 64-B n-gram hash-table lines read by the LM lookups    */
   int64_t launches[4];  /* kernel launches: frame, n-gram, fusion, output         */
   double  kernel_ms[4]; /* summed event-timed durations (when profiling is on)    */
   int64_t timed[4];     /* launches included in kernel_ms                         */

@@ -484,6 +484,7 @@ lb_status lb_get_stats(lb_decoder* d, lb_stats* out) {
     out->lm_queries += static_cast<int64_t>(x[kCntLmQueries]);
     out->fused += static_cast<int64_t>(x[kCntFused]);
     out->frames += static_cast<int64_t>(x[kCntFrames]);
+    out->probe_lines += static_cast<int64_t>(x[kCntProbeLines]);
   }
   d->harvest();
   for (int k = 0; k < 4; ++k) {

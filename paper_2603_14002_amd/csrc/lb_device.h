@@ -44,7 +44,7 @@ constexpr uint32_t kFlagBuildFull = 64u;
 
 // per-stream counters (DevState::counters, [max_batch][kNumCounters])
 enum { kCntExpansions = 0, kCntWordEvents = 1, kCntLmQueries = 2, kCntFused = 3, kCntFrames = 4,
-       kNumCounters = 5 };
+       kCntProbeLines = 5, kNumCounters = 6 };
 
 struct TrieNode {
   uint64_t mask;

@@ -121,10 +121,13 @@ __device__ inline void mask_from(int pos, uint64_t* mhi, uint64_t* mlo) {
 
 // ------------------------------------------------------------------ n-gram tables
 
-__device__ inline bool probe(const NgramTable& t, uint64_t key, uint32_t* slot, float* lp, float* bo) {
+// Looks `key` up; `lines` counts the 64-B bucket lines read.
+__device__ inline bool probe(const NgramTable& t, uint64_t key, uint32_t* slot, float* lp, float* bo,
+                             uint32_t* lines) {
   if (t.nbuckets == 0) return false;
   uint64_t bk = bucket_of(key, t.nbuckets);
   for (uint64_t it = 0; it < t.nbuckets; ++it) {
+    ++*lines;
     const uint4* line = reinterpret_cast<const uint4*>(t.slots + bk * 4);
     uint4 q[4];
 #pragma unroll
@@ -180,16 +183,16 @@ __global__ void k_build_order(int order, const int32_t* __restrict__ ids, const 
     }
     uint64_t ctx = static_cast<uint32_t>(r[0]);
     if (order >= 3) {
-      uint32_t s2;
+      uint32_t s2, nl = 0;
       float a, c;
-      if (!probe(t2, (static_cast<uint64_t>(r[0]) << 32) | static_cast<uint32_t>(r[1]), &s2, &a, &c)) {
+      if (!probe(t2, (static_cast<uint64_t>(r[0]) << 32) | static_cast<uint32_t>(r[1]), &s2, &a, &c, &nl)) {
         atomicOr(flags, kFlagBuildContext);
         continue;
       }
       ctx = s2;
       if (order == 4) {
         uint32_t s3;
-        if (!probe(t3, (static_cast<uint64_t>(s2) << 32) | static_cast<uint32_t>(r[2]), &s3, &a, &c)) {
+        if (!probe(t3, (static_cast<uint64_t>(s2) << 32) | static_cast<uint32_t>(r[2]), &s3, &a, &c, &nl)) {
           atomicOr(flags, kFlagBuildContext);
           continue;
         }
@@ -579,6 +582,7 @@ __global__ __launch_bounds__(256) void k_ngram(const DevParams P, const DevState
     const int H = static_cast<int>(S.trie[ev.pnode + 1].word_off - woff);
     const int nq = nsub * H;
 
+    uint32_t lines = 0;
     SubCand top[kMaxSub];
 #pragma unroll
     for (int k = 0; k < kMaxSub; ++k) {
@@ -595,11 +599,11 @@ __global__ __launch_bounds__(256) void k_ngram(const DevParams P, const DevState
       uint32_t s2 = kNone, s3 = kNone, s4;
       float p2 = 0.f, b2 = 0.f, p3 = 0.f, b3 = 0.f, p4 = 0.f, b4;
       const bool f2 = probe(S.t2, (static_cast<uint64_t>(static_cast<uint32_t>(ctx.word)) << 32) |
-                                      static_cast<uint32_t>(w), &s2, &p2, &b2);
+                                      static_cast<uint32_t>(w), &s2, &p2, &b2, &lines);
       const bool f3 = ctx.c2 != kNone &&
-                      probe(S.t3, (static_cast<uint64_t>(ctx.c2) << 32) | static_cast<uint32_t>(w), &s3, &p3, &b3);
+                      probe(S.t3, (static_cast<uint64_t>(ctx.c2) << 32) | static_cast<uint32_t>(w), &s3, &p3, &b3, &lines);
       const bool f4 = ctx.c3 != kNone &&
-                      probe(S.t4, (static_cast<uint64_t>(ctx.c3) << 32) | static_cast<uint32_t>(w), &s4, &p4, &b4);
+                      probe(S.t4, (static_cast<uint64_t>(ctx.c3) << 32) | static_cast<uint32_t>(w), &s4, &p4, &b4, &lines);
       const Unigram u = S.uni[w];
       // log10 P(w | context) by backoff, innermost order first
       double lp;
@@ -637,6 +641,8 @@ __global__ __launch_bounds__(256) void k_ngram(const DevParams P, const DevState
       }
     }
 
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) lines += __shfl_xor(lines, o, 64);
     // merge the per-lane lists: O rounds of a wave arg-max on (L desc, q asc)
     uint32_t abase = 0;
     if (lane == 0) abase = atomicAdd(&S.arena_n[ev.stream], static_cast<uint32_t>(P.O));
@@ -694,6 +700,7 @@ __global__ __launch_bounds__(256) void k_ngram(const DevParams P, const DevState
       unsigned long long* cn = S.counters + static_cast<size_t>(ev.stream) * kNumCounters;
       atomicAdd(&cn[kCntWordEvents], 1ull);
       atomicAdd(&cn[kCntLmQueries], static_cast<unsigned long long>(nq));
+      atomicAdd(&cn[kCntProbeLines], static_cast<unsigned long long>(lines));
     }
   }
 }

@@ -106,21 +106,23 @@ class NGramLM:
 
 
 def _draw_unique_keys(count: int, draw, rng: np.random.Generator) -> np.ndarray:
-    """Draw keys with ``draw(m)`` and reject duplicates until ``count`` are held."""
+    """Sorted unique keys: draw with ``draw(m)``, drop duplicates, and if more
+    than ``count`` distinct keys were drawn, keep a uniformly random subset."""
     kept = np.empty(0, dtype=np.int64)
-    kept_sorted = kept
     while kept.shape[0] < count:
         need = count - kept.shape[0]
-        cand = draw(int(need * 1.03) + 64)
-        _, first = np.unique(cand, return_index=True)
-        cand = cand[np.sort(first)]               # first occurrences, in draw order
-        if kept_sorted.shape[0]:
-            pos = np.searchsorted(kept_sorted, cand)
-            pos[pos >= kept_sorted.shape[0]] = 0
-            cand = cand[kept_sorted[pos] != cand]
-        kept = np.concatenate([kept, cand[:need]])
-        kept_sorted = np.sort(kept)
-    return kept_sorted
+        cand = np.unique(draw(int(need * 1.03) + 64))
+        if kept.shape[0]:
+            pos = np.searchsorted(kept, cand)
+            pos[pos >= kept.shape[0]] = 0
+            cand = cand[kept[pos] != cand]
+        if cand.shape[0] > need:
+            drop = rng.choice(cand.shape[0], cand.shape[0] - need, replace=False)
+            keep = np.ones(cand.shape[0], dtype=bool)
+            keep[drop] = False
+            cand = cand[keep]
+        kept = np.union1d(kept, cand) if kept.shape[0] else cand
+    return kept
 
 
 def make_lm(spec: LMSpec) -> NGramLM:
