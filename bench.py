@@ -27,7 +27,7 @@ sys.path.insert(0, ROOT)
 METRIC = "beam-token expansions/sec and decoded audio-sec per wall-sec (RTF) on 1 MI355X"
 HBM_PEAK_GBS = 8000.0
 LINE_BYTES = 64          # one hash-table bucket = one 64-B line
-KERNELS = ("frame", "ngram", "fusion", "output")
+KERNELS = ("frame", "lmquery", "lmselect", "fusion", "output")
 
 
 def log(msg):
@@ -188,13 +188,13 @@ def main():
     roof = None
     if kern:
         dom = max(kern, key=lambda k: kern[k]["total_ms"])
-        if "ngram" in kern:
+        if "lmquery" in kern:
             # the n-gram lookup phase: every probed 64-B bucket line is a random HBM read
-            per_launch_bytes = s.probe_lines * LINE_BYTES / max(1, kern["ngram"]["launches"])
-            achieved = per_launch_bytes / (kern["ngram"]["avg_us"] * 1e-6) / 1e9
-            roof = dict(kernel="k_ngram", bound="hbm", achieved=achieved, peak=HBM_PEAK_GBS, unit="GB/s",
+            per_launch_bytes = s.probe_lines * LINE_BYTES / max(1, kern["lmquery"]["launches"])
+            achieved = per_launch_bytes / (kern["lmquery"]["avg_us"] * 1e-6) / 1e9
+            roof = dict(kernel="k_lmquery", bound="hbm", achieved=achieved, peak=HBM_PEAK_GBS, unit="GB/s",
                         frac=achieved / HBM_PEAK_GBS, traffic=None,
-                        bytes_per_launch=per_launch_bytes, avg_launch_us=kern["ngram"]["avg_us"])
+                        bytes_per_launch=per_launch_bytes, avg_launch_us=kern["lmquery"]["avg_us"])
         kern["dominant"] = dom
     out = {
         "metric": METRIC,

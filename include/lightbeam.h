@@ -120,9 +120,10 @@ typedef struct lb_stats {
   int64_t fused;        /* hypotheses rescored by delayed fusion                  */
   int64_t frames;       /* stream-frames decoded                                  */
   int64_t probe_lines;  /* 64-B n-gram hash-table lines read by the LM lookups    */
-  int64_t launches[4];  /* kernel launches: frame, n-gram, fusion, output         */
-  double  kernel_ms[4]; /* summed event-timed durations (when profiling is on)    */
-  int64_t timed[4];     /* launches included in kernel_ms                         */
+  int64_t launches[8];  /* kernel launches: [0] frame step, [1] LM query, [2] homophone
+                           selection, [3] delayed fusion, [4] output, [5..7] unused  */
+  double  kernel_ms[8]; /* summed event-timed durations (when profiling is on)    */
+  int64_t timed[8];     /* launches included in kernel_ms                         */
 } lb_stats;
 
 /* Builds a decoder: the lexicon trie (CSR) and the n-gram hash tables are

@@ -390,7 +390,7 @@ Output decode(const Model& M, const Params& p, const float* logits, int T, bool 
     });
     size_t keep = std::min<size_t>(p.beam, ms.size());
     if (ms.size() > keep) out.mg.topk = std::min(out.mg.topk, ms[keep - 1].total - ms[keep].total);
-    const double cut = ms[0].total - p.theta;
+    const double cut = ms.empty() ? kNegInf : ms[0].total - p.theta;
 
     std::vector<Hyp> next;
     for (size_t i = 0; i < keep; ++i) {

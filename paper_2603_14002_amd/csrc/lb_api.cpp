@@ -40,6 +40,7 @@ lb_status fail(lb_status st, const std::string& msg) {
 struct HostTrie {
   std::vector<TrieNode> nodes;  // + sentinel
   std::vector<int32_t> words;
+  uint32_t max_homophones = 0;
 };
 
 HostTrie build_trie(const lb_lexicon_desc& lex) {
@@ -96,6 +97,7 @@ HostTrie build_trie(const lb_lexicon_desc& lex) {
     }
     if (k != 0 && !at[o].empty()) tn.mask |= 1ull << kSep;
     tn.word_off = woff;
+    t.max_homophones = std::max<uint32_t>(t.max_homophones, static_cast<uint32_t>(at[o].size()));
     for (int32_t w : at[o]) t.words.push_back(w);
     woff += static_cast<uint32_t>(at[o].size());
   }
@@ -116,21 +118,25 @@ struct EventPair {
   int kind;
 };
 
+// kernel kinds of lb_stats.launches / kernel_ms
+enum { kKindFrame = 0, kKindLmQuery = 1, kKindLmSelect = 2, kKindFusion = 3, kKindOutput = 4, kKinds = 8 };
+
 }  // namespace
 
 struct lb_decoder {
   lb_params p{};
   DevParams P{};
   DevState S{};
-  int block = 64;       // workgroup size of the per-stream kernels (>= beam)
-  int ngram_grid = 1;   // workgroups of the n-gram kernel
+  int block = 64;       // workgroup size of the fusion / output kernels (>= beam)
+  int lmq_grid = 1;     // workgroups of the LM query kernel
+  int lms_grid = 1;     // workgroups of the homophone selection kernel
   std::vector<void*> allocs;
-  int64_t launches[4] = {0, 0, 0, 0};
+  int64_t launches[kKinds] = {};
   bool profiling = false;
   std::vector<EventPair> pending;
   std::vector<hipEvent_t> pool;
-  double kernel_ms[4] = {0, 0, 0, 0};
-  int64_t timed[4] = {0, 0, 0, 0};
+  double kernel_ms[kKinds] = {};
+  int64_t timed[kKinds] = {};
 
   template <typename T>
   lb_status alloc(T** ptr, size_t count) {
@@ -218,10 +224,9 @@ lb_status validate(const lb_lexicon_desc* lex, const lb_ngram_desc* lm, const lb
   return LB_OK;
 }
 
-lb_status build_tables(lb_decoder* d, const lb_lexicon_desc* lex, const lb_ngram_desc* lm, double lf) {
+lb_status build_tables(lb_decoder* d, const HostTrie& trie, const lb_ngram_desc* lm, double lf) {
   lb_status st;
   // trie
-  HostTrie trie = build_trie(*lex);
   TrieNode* dtrie = nullptr;
   int32_t* dwords = nullptr;
   if ((st = d->alloc(&dtrie, trie.nodes.size())) != LB_OK) return st;
@@ -351,6 +356,13 @@ lb_status lb_create(const lb_lexicon_desc* lex, const lb_ngram_desc* lm, const l
     delete d;
     return fail(LB_ERR_CAPACITY, "word-history arena exceeds 32-bit node ids; lower max_frames or max_batch");
   }
+  // the lexicon trie (host), whose largest homophone set bounds the queries of a frame
+  HostTrie trie = build_trie(*lex);
+  const uint64_t qcap = static_cast<uint64_t>(B) * K * O * std::max<uint32_t>(1, trie.max_homophones);
+  if (qcap >= 0xFFFFFFFFull) {
+    delete d;
+    return fail(LB_ERR_CAPACITY, "per-frame n-gram query bound exceeds 32 bits; lower max_batch or beam");
+  }
   DevState& S = d->S;
   const size_t BK = static_cast<size_t>(B) * K;
   if ((st = d->alloc(&S.key, BK)) != LB_OK || (st = d->alloc(&S.pkey, BK)) != LB_OK ||
@@ -359,24 +371,29 @@ lb_status lb_create(const lb_lexicon_desc* lex, const lb_ngram_desc* lm, const l
       (st = d->alloc(&S.Lw, BK * O)) != LB_OK || (st = d->alloc(&S.hist, BK * O)) != LB_OK ||
       (st = d->alloc(&S.nbeam, B)) != LB_OK || (st = d->alloc(&S.t0, B)) != LB_OK ||
       (st = d->alloc(&S.arena_n, B)) != LB_OK || (st = d->alloc(&S.arena, 1 + cap * B)) != LB_OK ||
-      (st = d->alloc(&S.events, BK)) != LB_OK || (st = d->alloc(&S.ev_count, 2)) != LB_OK ||
+      (st = d->alloc(&S.events, BK)) != LB_OK || (st = d->alloc(&S.evq, 2)) != LB_OK ||
+      (st = d->alloc(&S.qmap, qcap)) != LB_OK || (st = d->alloc(&S.qL, qcap)) != LB_OK ||
+      (st = d->alloc(&S.qS, qcap)) != LB_OK ||
       (st = d->alloc(&S.flags, 1)) != LB_OK || (st = d->alloc(&S.counters, static_cast<size_t>(B) * kNumCounters)) != LB_OK ||
-      (st = d->alloc(&S.fsel, BK)) != LB_OK || (st = d->alloc(&S.fsel_n, B)) != LB_OK) {
+      (st = d->alloc(&S.fsel, BK)) != LB_OK || (st = d->alloc(&S.fsel_n, B)) != LB_OK ||
+      (st = d->alloc(&S.lines, static_cast<size_t>(kSpread) * kSpreadStride)) != LB_OK) {
     std::string msg = g_err;
     delete d;
     return fail(st, msg);
   }
   S.arena_cap = cap;
+  S.qcap = qcap;
   auto init = [&]() -> lb_status {
     LB_HIP(hipMemset(S.nbeam, 0, B * sizeof(int32_t)));
     LB_HIP(hipMemset(S.t0, 0, B * sizeof(int64_t)));
     LB_HIP(hipMemset(S.arena_n, 0, B * sizeof(uint32_t)));
-    LB_HIP(hipMemset(S.ev_count, 0, 2 * sizeof(uint32_t)));
+    LB_HIP(hipMemset(S.evq, 0, 2 * sizeof(unsigned long long)));
     LB_HIP(hipMemset(S.flags, 0, sizeof(uint32_t)));
     LB_HIP(hipMemset(S.counters, 0, static_cast<size_t>(B) * kNumCounters * sizeof(unsigned long long)));
+    LB_HIP(hipMemset(S.lines, 0, static_cast<size_t>(kSpread) * kSpreadStride * sizeof(unsigned long long)));
     return LB_OK;
   };
-  if ((st = init()) != LB_OK || (st = build_tables(d, lex, lm, lf)) != LB_OK) {
+  if ((st = init()) != LB_OK || (st = build_tables(d, trie, lm, lf)) != LB_OK) {
     std::string msg = g_err;
     delete d;
     return fail(st, msg);
@@ -399,8 +416,10 @@ lb_status lb_create(const lb_lexicon_desc* lex, const lb_ngram_desc* lm, const l
   P.seed = p.fusion_seed;
   P.lo = p.fusion_lo;
   P.hi = p.fusion_hi;
-  // enough waves to cover the largest event queue of a frame, capped at 8 per SIMD
-  d->ngram_grid = static_cast<int>(std::max<size_t>(1, std::min<size_t>((BK + 3) / 4, 2048)));
+  // the query kernel strides over the frame's queries; the selection kernel
+  // runs one wavefront per completed word (at most B*K per frame)
+  d->lmq_grid = static_cast<int>(std::max<uint64_t>(1, std::min<uint64_t>((qcap + 255) / 256, 4096)));
+  d->lms_grid = static_cast<int>(std::max<size_t>(1, std::min<size_t>((BK + 3) / 4, 2048)));
   *out = d;
   return LB_OK;
 }
@@ -421,27 +440,23 @@ lb_status lb_decode_batch(lb_decoder* d, const float* logits, const int32_t* len
   const DevState& S = d->S;
   const bool fusion = P.fusion_source == LB_FUSION_SYNTH_BIGRAM && P.fusion_interval > 0;
   EventPair ep{};
+  auto launch = [&](int kind, auto&& fn) -> hipError_t {
+    if (d->profiling) record_start(d, st, &ep, kind);
+    const hipError_t e = fn();
+    if (d->profiling) record_stop(d, st, &ep);
+    d->launches[kind]++;
+    return e;
+  };
   if (flags & LB_BEGIN) LB_HIP(launch_begin(P, S, batch, st));
   for (int32_t tau = 0; tau < frames; ++tau) {
-    if (d->profiling) record_start(d, st, &ep, 0);
-    LB_HIP(launch_frame(d->block, P, S, logits, lengths, batch, frames, tau, st));
-    if (d->profiling) record_stop(d, st, &ep);
-    d->launches[0]++;
-    if (d->profiling) record_start(d, st, &ep, 1);
-    LB_HIP(launch_ngram(d->ngram_grid, P, S, tau, st));
-    if (d->profiling) record_stop(d, st, &ep);
-    d->launches[1]++;
-    if (fusion) {
-      if (d->profiling) record_start(d, st, &ep, 2);
-      LB_HIP(launch_fusion(d->block, P, S, lengths, batch, tau, st));
-      if (d->profiling) record_stop(d, st, &ep);
-      d->launches[2]++;
-    }
+    LB_HIP(launch(kKindFrame, [&] { return launch_frame(P.K, P, S, logits, lengths, batch, frames, tau, st); }));
+    LB_HIP(launch(kKindLmQuery, [&] { return launch_lmquery(d->lmq_grid, P, S, tau, st); }));
+    LB_HIP(launch(kKindLmSelect, [&] { return launch_lmselect(d->lms_grid, P, S, tau, st); }));
+    if (fusion) LB_HIP(launch(kKindFusion, [&] { return launch_fusion(d->block, P, S, lengths, batch, tau, st); }));
   }
-  if (d->profiling) record_start(d, st, &ep, 3);
-  LB_HIP(launch_output(d->block, P, S, lengths, batch, (flags & LB_END) ? 1 : 0, out_hyps, out_scores, st));
-  if (d->profiling) record_stop(d, st, &ep);
-  d->launches[3]++;
+  LB_HIP(launch(kKindOutput, [&] {
+    return launch_output(d->block, P, S, lengths, batch, (flags & LB_END) ? 1 : 0, out_hyps, out_scores, st);
+  }));
   return LB_OK;
 }
 
@@ -486,8 +501,11 @@ lb_status lb_get_stats(lb_decoder* d, lb_stats* out) {
     out->frames += static_cast<int64_t>(x[kCntFrames]);
     out->probe_lines += static_cast<int64_t>(x[kCntProbeLines]);
   }
+  std::vector<unsigned long long> ln(static_cast<size_t>(kSpread) * kSpreadStride);
+  LB_HIP(hipMemcpy(ln.data(), d->S.lines, ln.size() * sizeof(unsigned long long), hipMemcpyDeviceToHost));
+  for (int k = 0; k < kSpread; ++k) out->probe_lines += static_cast<int64_t>(ln[static_cast<size_t>(k) * kSpreadStride]);
   d->harvest();
-  for (int k = 0; k < 4; ++k) {
+  for (int k = 0; k < kKinds; ++k) {
     out->launches[k] = d->launches[k];
     out->kernel_ms[k] = d->kernel_ms[k];
     out->timed[k] = d->timed[k];
@@ -499,8 +517,9 @@ lb_status lb_reset_stats(lb_decoder* d) {
   if (!d) return fail(LB_ERR_INVALID_ARG, "decoder is null");
   LB_HIP(hipDeviceSynchronize());
   LB_HIP(hipMemset(d->S.counters, 0, static_cast<size_t>(d->p.max_batch) * kNumCounters * sizeof(unsigned long long)));
+  LB_HIP(hipMemset(d->S.lines, 0, static_cast<size_t>(kSpread) * kSpreadStride * sizeof(unsigned long long)));
   d->harvest();
-  for (int k = 0; k < 4; ++k) {
+  for (int k = 0; k < kKinds; ++k) {
     d->launches[k] = 0;
     d->kernel_ms[k] = 0;
     d->timed[k] = 0;

@@ -42,6 +42,9 @@ constexpr uint32_t kFlagBuildContext = 16u;
 constexpr uint32_t kFlagBuildDup = 32u;
 constexpr uint32_t kFlagBuildFull = 64u;
 
+constexpr int kSpread = 256;       // slots of DevState::lines
+constexpr int kSpreadStride = 16;  // 16 x 8 B = one 128-B line per slot
+
 // per-stream counters (DevState::counters, [max_batch][kNumCounters])
 enum { kCntExpansions = 0, kCntWordEvents = 1, kCntLmQueries = 2, kCntFused = 3, kCntFrames = 4,
        kCntProbeLines = 5, kNumCounters = 6 };
@@ -82,11 +85,23 @@ struct HistNode {
   double sfus;
 };
 
+// A hypothesis that completed a word this frame (Eq. (1) applies to it).
 struct Event {
   uint32_t stream;
   uint32_t beam;
   uint32_t pnode;  // trie node of the completed word
+  uint32_t woff;   // its first homophone in trie_words
+  uint32_t H;      // number of homophones
+  uint32_t nsub;   // parent sub-beams
+  uint32_t qoff;   // first (sub-beam, homophone) query of the event in the frame's query arrays
   uint32_t pad;
+  uint32_t hist[kMaxSub];  // parent sub-beams' history nodes
+};
+
+// n-gram state after a queried word: slots of its 2- and 3-word contexts and their backoffs.
+struct QState {
+  uint32_t c2, c3;
+  float bo2, bo3;
 };
 
 struct DevParams {
@@ -115,9 +130,15 @@ struct DevState {
   HistNode* arena;
   uint64_t arena_cap;  // per stream
   Event* events;       // [B*K]
-  uint32_t* ev_count;  // [2]
+  unsigned long long* evq;  // [2] per frame parity: events << 32 | queries
+  uint32_t* qmap;      // [qcap] query -> event
+  double* qL;          // [qcap] candidate sub-beam score of each query
+  QState* qS;          // [qcap] n-gram state after the query's word
+  uint64_t qcap;
   uint32_t* flags;
   unsigned long long* counters;  // [B][kNumCounters]
+  // probed bucket lines, spread over kSpread slots 128 B apart (summed on the host)
+  unsigned long long* lines;
   // fusion selection for external scores: [B][K] beam index per rank, [B] count
   int32_t* fsel;
   int32_t* fsel_n;

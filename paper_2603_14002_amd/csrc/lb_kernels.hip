@@ -24,6 +24,8 @@ namespace lb {
 namespace {
 
 constexpr double kNegInf = -HUGE_VAL;
+constexpr int kBins = 1024;         // score bins of the top-K selection
+constexpr int kBoundaryCap = 256;   // candidates resolved exactly inside the boundary bin
 
 // ------------------------------------------------------------------ block helpers
 
@@ -227,34 +229,43 @@ __global__ void k_begin(DevParams P, DevState S, int32_t B) {
 
 // ------------------------------------------------------------------ frame step
 
-template <int BLOCK>
-__global__ __launch_bounds__(BLOCK) void k_frame(const DevParams P, const DevState S,
-                                                 const float* __restrict__ logits,
-                                                 const int32_t* __restrict__ lengths, int32_t Tc,
-                                                 int32_t tau) {
-  constexpr int HS = 2 * BLOCK;  // LDS hash slots for the current prefix keys
+// One workgroup per stream.  Hypothesis i is owned by LPB consecutive lanes:
+// lane s of it handles the extensions v = 1+s, 1+s+LPB, ... (and lane 0 the
+// merged stay), with the hypothesis' scores held in registers.
+template <int KMAX, int LPB>
+__global__ __launch_bounds__(KMAX * LPB) void k_frame(const DevParams P, const DevState S,
+                                                      const float* __restrict__ logits,
+                                                      const int32_t* __restrict__ lengths, int32_t Tc,
+                                                      int32_t tau) {
+  constexpr int BLOCK = KMAX * LPB;
+  constexpr int HS = 2 * KMAX;  // LDS hash slots for the current prefix keys
   constexpr int NW = BLOCK / 64;
   const int b = blockIdx.x;
   const int tid = threadIdx.x;
-  if (b == 0 && tid == 0) S.ev_count[(tau + 1) & 1] = 0;
+  if (b == 0 && tid == 0) S.evq[(tau + 1) & 1] = 0;
   if (tau >= lengths[b]) return;
 
   __shared__ double sD[kClasses];
-  __shared__ uint64_t sKey[BLOCK], sPkey[BLOCK];
-  __shared__ double sAb[BLOCK], sP[BLOCK], sL[BLOCK], sAb2[BLOCK], sAnb2[BLOCK], sStay[BLOCK];
-  __shared__ uint32_t sNode[BLOCK], sMeta[BLOCK], sFirst[BLOCK];
-  __shared__ uint64_t sMask[BLOCK], sTrieMask[BLOCK];
-  __shared__ double sLw[BLOCK * kMaxSub];
-  __shared__ uint32_t sHist[BLOCK * kMaxSub];
+  __shared__ uint64_t sKey[KMAX], sPkey[KMAX];
+  __shared__ double sAb[KMAX], sP[KMAX], sL[KMAX], sAb2[KMAX], sAnb2[KMAX], sStay[KMAX];
+  __shared__ uint32_t sNode[KMAX], sMeta[KMAX], sFirst[KMAX];
+  __shared__ uint64_t sMask[KMAX], sTrieMask[KMAX];
+  __shared__ double sLw[KMAX * kMaxSub];
+  __shared__ uint32_t sHist[KMAX * kMaxSub];
   __shared__ unsigned long long sHKey[HS];
   __shared__ int32_t sHIdx[HS];
-  __shared__ uint32_t sHisto[256];
-  __shared__ double sSelScore[BLOCK];
-  __shared__ uint64_t sSelKey[BLOCK];
-  __shared__ uint32_t sSelSrc[BLOCK];
+  __shared__ uint32_t sHisto[kBins];
+  __shared__ double sBScore[kBoundaryCap];
+  __shared__ uint64_t sBKey[kBoundaryCap];
+  __shared__ int32_t sBCount;
+  __shared__ double sSelScore[KMAX];
+  __shared__ uint64_t sSelKey[KMAX];
+  __shared__ uint32_t sSelSrc[KMAX];
+  __shared__ uint32_t sEvQ[KMAX];
   __shared__ double sRed[NW];
   __shared__ int32_t sScan[NW];
-  __shared__ int32_t sBucket, sAbove, sBucketCnt, sEvBase;
+  __shared__ int32_t sBucket, sAbove, sBucketCnt;
+  __shared__ unsigned long long sEvBase;
 
   const int n = S.nbeam[b];
   const size_t gb = static_cast<size_t>(b) * P.K;
@@ -342,49 +353,128 @@ __global__ __launch_bounds__(BLOCK) void k_frame(const DevParams P, const DevSta
   }
   __syncthreads();
 
-  // candidate c = i*41 + v: v = 0 is hypothesis i's stay, v >= 1 its extension by v
-  auto cand = [&](int c, double* score) -> bool {
-    const int i = c / kClasses;
-    const int v = c - i * kClasses;
-    double s;
-    if (v == 0) {
-      s = sStay[i];
-    } else {
-      if (!((sMask[i] >> v) & 1ull)) return false;
-      const int last = sMeta[i] & 0xFF;
-      const double base = (v == last) ? sAb[i] : sP[i];
-      s = ((base + sD[v]) + (v == kSep ? P.gamma : P.beta)) + sL[i];
+  // ---- this lane's candidates, scores cached in registers: slot k is the
+  // extension by v = 1 + ln + LPB*k, plus the merged stay on lane 0
+  constexpr int NC = (kSep + LPB - 1) / LPB;
+  const int hi_ = tid / LPB;
+  const int ln = tid - hi_ * LPB;
+  const bool live = hi_ < n;
+  uint64_t c_key = 0;
+  double c_stay = kNegInf;
+  double sc[NC];
+  {
+    double c_ab = 0.0, c_p = 0.0, c_L = 0.0;
+    int c_last = 0;
+    uint64_t c_mask = 0;
+    if (live) {
+      c_ab = sAb[hi_];
+      c_p = sP[hi_];
+      c_L = sL[hi_];
+      c_last = sMeta[hi_] & 0xFF;
+      c_mask = sMask[hi_];
+      c_key = sKey[hi_];
+      if (ln == 0) c_stay = sStay[hi_];
     }
-    *score = s;
-    return s != kNegInf;
-  };
-  auto cand_key = [&](int c) -> uint64_t {
-    const int i = c / kClasses;
-    const int v = c - i * kClasses;
-    return v == 0 ? sKey[i] : prefix_step(sKey[i], v);
+#pragma unroll
+    for (int k = 0; k < NC; ++k) {
+      const int v = 1 + ln + LPB * k;
+      double s = kNegInf;
+      if (v <= kSep && ((c_mask >> v) & 1ull)) {
+        const double base = (v == c_last) ? c_ab : c_p;
+        s = ((base + sD[v]) + (v == kSep ? P.gamma : P.beta)) + c_L;
+      }
+      sc[k] = s;
+    }
+  }
+  auto key_of = [&](int v) -> uint64_t { return v == 0 ? c_key : prefix_step(c_key, v); };
+  // f(v, score) for each of this lane's candidates with a finite score
+  auto for_cands = [&](auto&& f) {
+    if (c_stay != kNegInf) f(0, c_stay);
+#pragma unroll
+    for (int k = 0; k < NC; ++k)
+      if (sc[k] != kNegInf) f(1 + ln + LPB * k, sc[k]);
   };
 
-  const int nc = n * kClasses;
-  double mx = kNegInf;
-  for (int c = tid; c < nc; c += BLOCK) {
-    double s;
-    if (cand(c, &s)) mx = fmax(mx, s);
-  }
+  double mx = kNegInf, mn = HUGE_VAL;
+  for_cands([&](int, double s) {
+    mx = fmax(mx, s);
+    mn = fmin(mn, s);
+  });
   const double best = block_max<BLOCK>(mx, sRed);
+  const double lowest = -block_max<BLOCK>(-mn, sRed);
   const double thr = best - P.theta;
 
-  int cnt = 0;
-  for (int c = tid; c < nc; c += BLOCK) {
-    double s;
-    if (cand(c, &s) && s >= thr) ++cnt;
+  // ---- top-K.  Bins of (best - score) over [max(thr, lowest), best] order the
+  // candidates (the map is monotone); bins above the one holding the K-th are
+  // taken whole, and that bin is resolved exactly by rank on (score desc, key
+  // asc).  If that bin is too crowded, an MSD radix select over (ordered score
+  // bits, ~key) decides instead.
+  const double lo_s = fmax(thr, lowest);
+  const double width = best - lo_s;
+  const double inv_w = width > 0.0 ? static_cast<double>(kBins) / width : 0.0;
+  auto bin_of = [&](double s) -> int {
+    const double x = (best - s) * inv_w;
+    return x >= static_cast<double>(kBins - 1) ? kBins - 1 : static_cast<int>(x);
+  };
+  for (int d = tid; d < kBins; d += BLOCK) sHisto[d] = 0;
+  __syncthreads();
+  for_cands([&](int, double s) {
+    if (s >= thr) atomicAdd(&sHisto[bin_of(s)], 1u);
+  });
+  __syncthreads();
+  // bin holding the K-th candidate: each thread sums kBins/BLOCK consecutive bins
+  constexpr int PER = (kBins + BLOCK - 1) / BLOCK;
+  int local = 0;
+#pragma unroll
+  for (int q = 0; q < PER; ++q) {
+    const int d = tid * PER + q;
+    local += d < kBins ? static_cast<int>(sHisto[d]) : 0;
   }
   int nvalid = 0;
-  (void)block_scan<BLOCK>(cnt, sScan, &nvalid);
-
-  // ---- top-K: MSD radix select over (ordered score bits, ~key), 8 bits a pass
-  uint64_t pre_hi = 0, pre_lo = 0, m_hi = 0, m_lo = 0;
+  const int before = block_scan<BLOCK>(local, sScan, &nvalid);
   const bool select_all = nvalid <= P.K;
+  int beta_bin = kBins, need_b = 0, nbc = 0;
+  bool use_radix = false;
+  uint64_t pre_hi = 0, pre_lo = 0;
   if (!select_all) {
+    if (before < P.K && before + local >= P.K) {
+      int acc = before;
+      for (int q = 0; q < PER; ++q) {
+        const int d = tid * PER + q;
+        const int h = static_cast<int>(sHisto[d]);
+        if (acc + h >= P.K) {
+          sBucket = d;
+          sAbove = acc;
+          sBucketCnt = h;
+          break;
+        }
+        acc += h;
+      }
+    }
+    __syncthreads();
+    beta_bin = sBucket;
+    need_b = P.K - sAbove;
+    const int nb_bin = sBucketCnt;
+    if (nb_bin != need_b) {
+      if (nb_bin <= kBoundaryCap) {
+        nbc = nb_bin;
+        if (tid == 0) sBCount = 0;
+        __syncthreads();
+        for_cands([&](int v, double s) {
+          if (s >= thr && bin_of(s) == beta_bin) {
+            const int slot = atomicAdd(&sBCount, 1);
+            sBScore[slot] = s;
+            sBKey[slot] = key_of(v);
+          }
+        });
+        __syncthreads();
+      } else {
+        use_radix = true;
+      }
+    }
+  }
+  if (use_radix) {
+    uint64_t m_hi = 0, m_lo = 0;
     const uint64_t ob_best = order_bits(best), ob_thr = order_bits(thr);
     const int common = (ob_best == ob_thr) ? 64 : __clzll(static_cast<long long>(ob_best ^ ob_thr));
     int pos = ((127 - common) / 8) * 8;
@@ -396,15 +486,14 @@ __global__ __launch_bounds__(BLOCK) void k_frame(const DevParams P, const DevSta
       for (int d = tid; d < 256; d += BLOCK) sHisto[d] = 0;
       __syncthreads();
       const bool want_key = pos < 64;
-      for (int c = tid; c < nc; c += BLOCK) {
-        double s;
-        if (!cand(c, &s) || s < thr) continue;
-        const uint64_t hi = order_bits(s);
-        if ((hi & m_hi) != pre_hi) continue;
-        const uint64_t lo = want_key ? ~cand_key(c) : 0;
-        if ((lo & m_lo) != pre_lo) continue;
-        atomicAdd(&sHisto[digit128(hi, lo, pos)], 1u);
-      }
+      for_cands([&](int v, double s) {
+        if (s < thr) return;
+        const uint64_t h = order_bits(s);
+        if ((h & m_hi) != pre_hi) return;
+        const uint64_t lo = want_key ? ~key_of(v) : 0;
+        if ((lo & m_lo) != pre_lo) return;
+        atomicAdd(&sHisto[digit128(h, lo, pos)], 1u);
+      });
       __syncthreads();
       if (tid < 64) {
         // lane l owns bins 4l..4l+3; find the bin holding the need-th largest
@@ -451,57 +540,66 @@ __global__ __launch_bounds__(BLOCK) void k_frame(const DevParams P, const DevSta
       pos -= 8;
     }
   }
-
-  // ---- gather the selected candidates (prefix-sum order), then sort them
-  int mysel = 0;
-  for (int c = tid; c < nc; c += BLOCK) {
-    double s;
-    if (!cand(c, &s) || s < thr) continue;
-    if (!select_all) {
-      const uint64_t hi = order_bits(s);
-      if (hi < pre_hi || (hi == pre_hi && ~cand_key(c) < pre_lo)) continue;
+  auto selected = [&](int v, double s) -> bool {
+    if (s < thr) return false;
+    if (select_all) return true;
+    if (use_radix) {
+      const uint64_t h = order_bits(s);
+      if (h != pre_hi) return h > pre_hi;
+      return ~key_of(v) >= pre_lo;
     }
-    ++mysel;
-  }
+    const int bn = bin_of(s);
+    if (bn != beta_bin) return bn < beta_bin;
+    if (nbc == 0) return true;
+    // rank inside the boundary bin by (score desc, key asc)
+    const uint64_t k = key_of(v);
+    int rank = 0;
+    for (int u = 0; u < nbc; ++u) rank += ranks_before(sBScore[u], sBKey[u], s, k);
+    return rank < need_b;
+  };
+
+  // ---- selection bits (bit 0: the stay, bit k+1: slot k), then a
+  // deterministic gather in lane order
+  uint64_t sel_bits = 0;
+  if (c_stay != kNegInf && selected(0, c_stay)) sel_bits |= 1ull;
+#pragma unroll
+  for (int k = 0; k < NC; ++k)
+    if (sc[k] != kNegInf && selected(1 + ln + LPB * k, sc[k])) sel_bits |= 2ull << k;
   int nsel = 0;
-  int wpos = block_scan<BLOCK>(mysel, sScan, &nsel);
+  int wpos = block_scan<BLOCK>(__popcll(sel_bits), sScan, &nsel);
   if (nsel > P.K) {  // cannot happen when the selection is exact; never write past K entries
     nsel = P.K;
     if (tid == 0) atomicOr(S.flags, kFlagSelect);
   }
-  for (int c = tid; c < nc; c += BLOCK) {
-    double s;
-    if (!cand(c, &s) || s < thr) continue;
-    const uint64_t hi = order_bits(s);
-    if (!select_all && hi < pre_hi) continue;
-    const uint64_t k = cand_key(c);
-    if (!select_all && hi == pre_hi && ~k < pre_lo) continue;
-    if (wpos >= nsel) break;
-    const int i = c / kClasses;
-    sSelScore[wpos] = s;
-    sSelKey[wpos] = k;
-    sSelSrc[wpos] = static_cast<uint32_t>(i) | (static_cast<uint32_t>(c - i * kClasses) << 16);
+  if ((sel_bits & 1ull) && wpos < nsel) {
+    sSelScore[wpos] = c_stay;
+    sSelKey[wpos] = c_key;
+    sSelSrc[wpos] = static_cast<uint32_t>(hi_);
     ++wpos;
   }
-  __syncthreads();
-  if (tid >= nsel) {
-    sSelScore[tid] = kNegInf;
-    sSelKey[tid] = ~0ull;
-    sSelSrc[tid] = 0;
+#pragma unroll
+  for (int k = 0; k < NC; ++k) {
+    if (((sel_bits >> (k + 1)) & 1ull) && wpos < nsel) {
+      const int v = 1 + ln + LPB * k;
+      sSelScore[wpos] = sc[k];
+      sSelKey[wpos] = prefix_step(c_key, v);
+      sSelSrc[wpos] = static_cast<uint32_t>(hi_) | (static_cast<uint32_t>(v) << 16);
+      ++wpos;
+    }
   }
   __syncthreads();
-  bitonic_sort<BLOCK>(sSelScore, sSelKey, sSelSrc);
 
   // ---- write the new hypotheses (in place: every old value is in LDS)
   const int r = tid;
-  int is_event = 0;
-  uint32_t ev_pnode = 0;
+  int is_event = 0, my_nq = 0, ev_src = 0;
+  uint32_t ev_pnode = 0, ev_woff = 0, ev_H = 0, ev_nsub = 0;
   if (r < nsel) {
     const uint32_t src = sSelSrc[r];
     const int i = src & 0xFFFF;
     const int v = src >> 16;
     const size_t o = gb + r;
     const uint32_t meta_i = sMeta[i];
+    const int nsub = (meta_i >> 8) & 0xFF;
     if (v == 0) {
       S.key[o] = sKey[i];
       S.pkey[o] = sPkey[i];
@@ -523,127 +621,218 @@ __global__ __launch_bounds__(BLOCK) void k_frame(const DevParams P, const DevSta
       if (v == kSep) {
         is_event = 1;
         ev_pnode = sNode[i];
+        ev_woff = S.trie[ev_pnode].word_off;
+        ev_H = S.trie[ev_pnode + 1].word_off - ev_woff;
+        ev_nsub = static_cast<uint32_t>(nsub);
+        my_nq = static_cast<int>(ev_nsub * ev_H);
+        ev_src = i;
       }
     }
-    const int nsub = (meta_i >> 8) & 0xFF;
     for (int j = 0; j < nsub; ++j) {
       S.Lw[o * P.O + j] = sLw[i * kMaxSub + j];
       S.hist[o * P.O + j] = sHist[i * kMaxSub + j];
     }
   }
-  int nev = 0;
-  const int epos = block_scan<BLOCK>(is_event, sScan, &nev);
+  int nev = 0, nq_blk = 0;
+  const int erank = block_scan<BLOCK>(is_event, sScan, &nev);
+  const int qpos = block_scan<BLOCK>(my_nq, sScan, &nq_blk);
   if (tid == 0) {
     S.nbeam[b] = nsel;
-    sEvBase = nev ? static_cast<int>(atomicAdd(&S.ev_count[tau & 1], static_cast<uint32_t>(nev))) : 0;
+    sEvBase = nev ? atomicAdd(&S.evq[tau & 1], (static_cast<unsigned long long>(nev) << 32) |
+                                                   static_cast<unsigned long long>(nq_blk))
+                  : 0ull;
     unsigned long long* cn = S.counters + static_cast<size_t>(b) * kNumCounters;
     cn[kCntExpansions] += static_cast<unsigned long long>(n) * kClasses;
     cn[kCntFrames] += 1;
   }
+  if (is_event) sEvQ[erank] = static_cast<uint32_t>(qpos);
   __syncthreads();
+  const uint32_t ev0 = static_cast<uint32_t>(sEvBase >> 32);
+  const uint32_t q0 = static_cast<uint32_t>(sEvBase);
   if (is_event) {
     Event e;
     e.stream = b;
     e.beam = r;
     e.pnode = ev_pnode;
+    e.woff = ev_woff;
+    e.H = ev_H;
+    e.nsub = ev_nsub;
+    e.qoff = q0 + qpos;
     e.pad = 0;
-    S.events[sEvBase + epos] = e;
+#pragma unroll
+    for (int j = 0; j < kMaxSub; ++j) e.hist[j] = j < static_cast<int>(ev_nsub) ? sHist[ev_src * kMaxSub + j] : 0u;
+    S.events[ev0 + erank] = e;
+  }
+  // query -> event map of this block's queries (events are contiguous, in order)
+  for (int k = tid; k < nq_blk; k += BLOCK) {
+    int lo = 0, hi = nev - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (sEvQ[mid] <= static_cast<uint32_t>(k)) lo = mid; else hi = mid - 1;
+    }
+    S.qmap[q0 + k] = ev0 + lo;
   }
 }
 
 // ------------------------------------------------------------------ n-gram shallow fusion
 
-struct SubCand {
-  double L;
-  int32_t q;       // (parent sub-beam, homophone) index: ties break on it ascending
-  int32_t w;
-  uint32_t ph;     // parent history node
-  uint32_t c2, c3;
-  float bo1, bo2, bo3;
-  double sf;
+// One 64-B bucket: four 16-B slots {key lo, key hi, log10 p, backoff}.
+struct Bucket {
+  uint4 s0, s1, s2, s3;
 };
 
-__device__ inline bool sub_before(const SubCand& a, const SubCand& b) {
-  return a.L > b.L || (a.L == b.L && a.q < b.q);
+__device__ __forceinline__ Bucket load_bucket(const NgramTable& t, uint64_t bk) {
+  const uint4* line = reinterpret_cast<const uint4*>(t.slots + bk * 4);
+  Bucket q;
+  q.s0 = line[0];
+  q.s1 = line[1];
+  q.s2 = line[2];
+  q.s3 = line[3];
+  return q;
 }
 
-__global__ __launch_bounds__(256) void k_ngram(const DevParams P, const DevState S, int32_t tau) {
-  const uint32_t count = S.ev_count[tau & 1];
+__device__ __forceinline__ uint64_t slot_key(const uint4& v) {
+  return static_cast<uint64_t>(v.x) | (static_cast<uint64_t>(v.y) << 32);
+}
+
+// Scans a bucket for `key`: 1 found (slot index and values set), 0 absent, -1 bucket full.
+__device__ __forceinline__ int scan_bucket(const Bucket& q, uint64_t key, uint64_t bk, uint32_t* slot, float* lp,
+                                           float* bo) {
+#define LB_SCAN_SLOT(V, K)                              \
+  {                                                     \
+    const uint64_t kk = slot_key(V);                    \
+    if (kk == key) {                                    \
+      *slot = static_cast<uint32_t>(bk * 4 + (K));      \
+      *lp = __uint_as_float((V).z);                     \
+      *bo = __uint_as_float((V).w);                     \
+      return 1;                                         \
+    }                                                   \
+    if (kk == kEmptyKey) return 0;                      \
+  }
+  LB_SCAN_SLOT(q.s0, 0)
+  LB_SCAN_SLOT(q.s1, 1)
+  LB_SCAN_SLOT(q.s2, 2)
+  LB_SCAN_SLOT(q.s3, 3)
+#undef LB_SCAN_SLOT
+  return -1;
+}
+
+// Resolves a lookup whose first bucket `bk` is already loaded; linear probing
+// continues bucket by bucket while buckets are full.
+__device__ __forceinline__ bool resolve(const NgramTable& t, uint64_t key, uint64_t bk, const Bucket& first,
+                                        uint32_t* slot, float* lp, float* bo, uint32_t* lines) {
+  int r = scan_bucket(first, key, bk, slot, lp, bo);
+  for (uint64_t it = 1; r < 0 && it < t.nbuckets; ++it) {
+    bk = (bk + 1 == t.nbuckets) ? 0 : bk + 1;
+    ++*lines;
+    r = scan_bucket(load_bucket(t, bk), key, bk, slot, lp, bo);
+  }
+  return r == 1;
+}
+
+__device__ __forceinline__ uint32_t hist_of(const Event& ev, uint32_t j) {
+  return j == 0 ? ev.hist[0] : (j == 1 ? ev.hist[1] : (j == 2 ? ev.hist[2] : ev.hist[3]));
+}
+
+// The LM lookup phase: one thread per (completed word, parent sub-beam,
+// homophone) query of the frame, over every stream.  The three bucket lines
+// (orders 2, 3, 4) and the unigram are loaded together, then resolved.
+__global__ __launch_bounds__(256) void k_lmquery(const DevParams P, const DevState S, int32_t tau) {
+  const uint32_t nq = static_cast<uint32_t>(S.evq[tau & 1]);
+  uint32_t lines = 0;
+  const uint32_t stride = gridDim.x * blockDim.x;
+  for (uint32_t q = blockIdx.x * blockDim.x + threadIdx.x; q < nq; q += stride) {
+    const Event ev = S.events[S.qmap[q]];
+    const uint32_t loc = q - ev.qoff;
+    const uint32_t j = loc / ev.H;
+    const uint32_t h = loc - j * ev.H;
+    const int w = S.trie_words[ev.woff + h];
+    const uint32_t ph = hist_of(ev, j);
+    const HistNode ctx = S.arena[ph];
+    const double Lw = S.Lw[(static_cast<size_t>(ev.stream) * P.K + ev.beam) * P.O + j];
+    const uint64_t k2 = (static_cast<uint64_t>(static_cast<uint32_t>(ctx.word)) << 32) | static_cast<uint32_t>(w);
+    const uint64_t k3 = (static_cast<uint64_t>(ctx.c2) << 32) | static_cast<uint32_t>(w);
+    const uint64_t k4 = (static_cast<uint64_t>(ctx.c3) << 32) | static_cast<uint32_t>(w);
+    const bool has3 = ctx.c2 != kNone;
+    const bool has4 = ctx.c3 != kNone;
+    const uint64_t b2 = bucket_of(k2, S.t2.nbuckets);
+    const uint64_t b3 = has3 ? bucket_of(k3, S.t3.nbuckets) : 0;
+    const uint64_t b4 = has4 ? bucket_of(k4, S.t4.nbuckets) : 0;
+    const Bucket q2 = load_bucket(S.t2, b2);
+    const Bucket q3 = has3 ? load_bucket(S.t3, b3) : Bucket{};
+    const Bucket q4 = has4 ? load_bucket(S.t4, b4) : Bucket{};
+    const Unigram u = S.uni[w];
+    lines += 1u + (has3 ? 1u : 0u) + (has4 ? 1u : 0u);
+    uint32_t s2 = kNone, s3 = kNone, s4 = kNone;
+    float p2 = 0.f, bb2 = 0.f, p3 = 0.f, bb3 = 0.f, p4 = 0.f, bb4 = 0.f;
+    const bool f2 = resolve(S.t2, k2, b2, q2, &s2, &p2, &bb2, &lines);
+    const bool f3 = has3 && resolve(S.t3, k3, b3, q3, &s3, &p3, &bb3, &lines);
+    const bool f4 = has4 && resolve(S.t4, k4, b4, q4, &s4, &p4, &bb4, &lines);
+    // log10 P(w | context) by backoff, innermost order first
+    double lp;
+    if (f4) {
+      lp = static_cast<double>(p4);
+    } else {
+      double l3;
+      if (f3) {
+        l3 = static_cast<double>(p3);
+      } else {
+        const double l2 = f2 ? static_cast<double>(p2) : static_cast<double>(ctx.bo1) + static_cast<double>(u.logp);
+        l3 = static_cast<double>(ctx.bo2) + l2;
+      }
+      lp = static_cast<double>(ctx.bo3) + l3;
+    }
+    S.qL[q] = Lw + P.comega * lp;
+    QState st;
+    st.c2 = f2 ? s2 : kNone;
+    st.c3 = f3 ? s3 : kNone;
+    st.bo2 = f2 ? bb2 : 0.0f;
+    st.bo3 = f3 ? bb3 : 0.0f;
+    S.qS[q] = st;
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) lines += __shfl_xor(lines, o, 64);
+  if ((threadIdx.x & 63) == 0 && lines) {
+    const uint32_t slot = ((blockIdx.x * blockDim.x + threadIdx.x) >> 6) & (kSpread - 1);
+    atomicAdd(&S.lines[slot * kSpreadStride], static_cast<unsigned long long>(lines));
+  }
+}
+
+// Homophone top-o (Eq. (1), App. E.3): one wavefront per completed word ranks
+// its queries by (score desc, (sub-beam, homophone) index asc), keeps o, drops
+// those more than lambda below the best, and appends word-history nodes.
+__global__ __launch_bounds__(256) void k_lmselect(const DevParams P, const DevState S, int32_t tau) {
+  const uint32_t nev = static_cast<uint32_t>(S.evq[tau & 1] >> 32);
   const int lane = threadIdx.x & 63;
   const uint32_t wave = (blockIdx.x * blockDim.x + threadIdx.x) >> 6;
   const uint32_t nwaves = (gridDim.x * blockDim.x) >> 6;
   const bool synth = P.fusion_source == 1;
-  for (uint32_t e = wave; e < count; e += nwaves) {
+  for (uint32_t e = wave; e < nev; e += nwaves) {
     const Event ev = S.events[e];
     const size_t bi = static_cast<size_t>(ev.stream) * P.K + ev.beam;
-    const uint32_t meta = S.meta[bi];
-    const int nsub = (meta >> 8) & 0xFF;
-    const uint32_t woff = S.trie[ev.pnode].word_off;
-    const int H = static_cast<int>(S.trie[ev.pnode + 1].word_off - woff);
-    const int nq = nsub * H;
-
-    uint32_t lines = 0;
-    SubCand top[kMaxSub];
+    const int nq = static_cast<int>(ev.nsub * ev.H);
+    double tL[kMaxSub];
+    int tq[kMaxSub];
 #pragma unroll
     for (int k = 0; k < kMaxSub; ++k) {
-      top[k].L = kNegInf;
-      top[k].q = 0x7FFFFFFF;
+      tL[k] = kNegInf;
+      tq[k] = 0x7FFFFFFF;
     }
     for (int q = lane; q < nq; q += 64) {
-      const int j = q / H;
-      const int h = q - j * H;
-      const int w = S.trie_words[woff + h];
-      const uint32_t ph = S.hist[bi * P.O + j];
-      const double Lw = S.Lw[bi * P.O + j];
-      const HistNode ctx = S.arena[ph];
-      uint32_t s2 = kNone, s3 = kNone, s4;
-      float p2 = 0.f, b2 = 0.f, p3 = 0.f, b3 = 0.f, p4 = 0.f, b4;
-      const bool f2 = probe(S.t2, (static_cast<uint64_t>(static_cast<uint32_t>(ctx.word)) << 32) |
-                                      static_cast<uint32_t>(w), &s2, &p2, &b2, &lines);
-      const bool f3 = ctx.c2 != kNone &&
-                      probe(S.t3, (static_cast<uint64_t>(ctx.c2) << 32) | static_cast<uint32_t>(w), &s3, &p3, &b3, &lines);
-      const bool f4 = ctx.c3 != kNone &&
-                      probe(S.t4, (static_cast<uint64_t>(ctx.c3) << 32) | static_cast<uint32_t>(w), &s4, &p4, &b4, &lines);
-      const Unigram u = S.uni[w];
-      // log10 P(w | context) by backoff, innermost order first
-      double lp;
-      if (f4) {
-        lp = static_cast<double>(p4);
-      } else {
-        double l3;
-        if (f3) {
-          l3 = static_cast<double>(p3);
-        } else {
-          const double l2 = f2 ? static_cast<double>(p2)
-                               : static_cast<double>(ctx.bo1) + static_cast<double>(u.logp);
-          l3 = static_cast<double>(ctx.bo2) + l2;
-        }
-        lp = static_cast<double>(ctx.bo3) + l3;
-      }
-      SubCand c;
-      c.L = Lw + P.comega * lp;
-      c.q = q;
-      c.w = w;
-      c.ph = ph;
-      c.c2 = f2 ? s2 : kNone;
-      c.c3 = f3 ? s3 : kNone;
-      c.bo1 = u.bo;
-      c.bo2 = f2 ? b2 : 0.0f;
-      c.bo3 = f3 ? b3 : 0.0f;
-      c.sf = synth ? ctx.sfus + bigram_score(P, ctx.word, w) : 0.0;
+      double L = S.qL[ev.qoff + q];
+      int qq = q;
 #pragma unroll
       for (int k = 0; k < kMaxSub; ++k) {
-        if (k < P.O && sub_before(c, top[k])) {
-          const SubCand t = top[k];
-          top[k] = c;
-          c = t;
+        if (k < P.O && (L > tL[k] || (L == tL[k] && qq < tq[k]))) {
+          const double t = tL[k];
+          const int u = tq[k];
+          tL[k] = L;
+          tq[k] = qq;
+          L = t;
+          qq = u;
         }
       }
     }
-
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) lines += __shfl_xor(lines, o, 64);
-    // merge the per-lane lists: O rounds of a wave arg-max on (L desc, q asc)
     uint32_t abase = 0;
     if (lane == 0) abase = atomicAdd(&S.arena_n[ev.stream], static_cast<uint32_t>(P.O));
     abase = __shfl(abase, 0, 64);
@@ -655,8 +844,8 @@ __global__ __launch_bounds__(256) void k_ngram(const DevParams P, const DevState
 #pragma unroll
     for (int k = 0; k < kMaxSub; ++k) {
       if (k >= P.O) break;
-      double bL = top[0].L;
-      int bq = top[0].q;
+      double bL = tL[0];
+      int bq = tq[0];
       int bl = lane;
 #pragma unroll
       for (int o = 32; o > 0; o >>= 1) {
@@ -674,33 +863,45 @@ __global__ __launch_bounds__(256) void k_ngram(const DevParams P, const DevState
       if (bL < bestL - P.lam) break;
       if (lane == bl) {
         if (room) {
+          const uint32_t j = static_cast<uint32_t>(bq) / ev.H;
+          const uint32_t h = static_cast<uint32_t>(bq) - j * ev.H;
+          const int w = S.trie_words[ev.woff + h];
+          const uint32_t ph = hist_of(ev, j);
+          const QState st = S.qS[ev.qoff + bq];
           HistNode hn;
-          hn.parent = top[0].ph;
-          hn.word = top[0].w;
-          hn.c2 = top[0].c2;
-          hn.c3 = top[0].c3;
-          hn.bo1 = top[0].bo1;
-          hn.bo2 = top[0].bo2;
-          hn.bo3 = top[0].bo3;
+          hn.parent = ph;
+          hn.word = w;
+          hn.c2 = st.c2;
+          hn.c3 = st.c3;
+          hn.bo1 = S.uni[w].bo;
+          hn.bo2 = st.bo2;
+          hn.bo3 = st.bo3;
           hn.pad = 0;
-          hn.sfus = top[0].sf;
+          if (synth) {
+            const HistNode ctx = S.arena[ph];
+            hn.sfus = ctx.sfus + bigram_score(P, ctx.word, w);
+          } else {
+            hn.sfus = 0.0;
+          }
           S.arena[node0 + k] = hn;
-          S.Lw[bi * P.O + k] = top[0].L;
+          S.Lw[bi * P.O + k] = bL;
           S.hist[bi * P.O + k] = node0 + k;
         }
 #pragma unroll
-        for (int m = 0; m + 1 < kMaxSub; ++m) top[m] = top[m + 1];
-        top[kMaxSub - 1].L = kNegInf;
-        top[kMaxSub - 1].q = 0x7FFFFFFF;
+        for (int m = 0; m + 1 < kMaxSub; ++m) {
+          tL[m] = tL[m + 1];
+          tq[m] = tq[m + 1];
+        }
+        tL[kMaxSub - 1] = kNegInf;
+        tq[kMaxSub - 1] = 0x7FFFFFFF;
       }
       kept = k + 1;
     }
     if (lane == 0) {
-      if (room) S.meta[bi] = (meta & 0xFFu) | (static_cast<uint32_t>(kept) << 8);
+      if (room) S.meta[bi] = (S.meta[bi] & 0xFFu) | (static_cast<uint32_t>(kept) << 8);
       unsigned long long* cn = S.counters + static_cast<size_t>(ev.stream) * kNumCounters;
       atomicAdd(&cn[kCntWordEvents], 1ull);
       atomicAdd(&cn[kCntLmQueries], static_cast<unsigned long long>(nq));
-      atomicAdd(&cn[kCntProbeLines], static_cast<unsigned long long>(lines));
     }
   }
 }
@@ -806,8 +1007,8 @@ __global__ __launch_bounds__(BLOCK) void k_output(const DevParams P, const DevSt
   __shared__ uint32_t ix[BLOCK];
   __shared__ int32_t sScan[BLOCK / 64];
   if (b == 0 && tid == 0) {
-    S.ev_count[0] = 0;
-    S.ev_count[1] = 0;
+    S.evq[0] = 0;
+    S.evq[1] = 0;
   }
   if (fin && P.fusion_source == 1 && P.fusion_interval > 0) fuse_stream<BLOCK>(P, S, b, 0, nullptr, sc, ky, ix);
   const int n = S.nbeam[b];
@@ -878,14 +1079,29 @@ hipError_t launch_begin(const DevParams& P, const DevState& S, int32_t B, hipStr
       hipLaunchKernelGGL(KERNEL<256>, dim3(GRID), dim3(256), 0, st, __VA_ARGS__);           \
   } while (0)
 
-hipError_t launch_frame(int block, const DevParams& P, const DevState& S, const float* logits,
+// Frame-kernel shapes: (hypotheses per workgroup, lanes per hypothesis).
+hipError_t launch_frame(int K, const DevParams& P, const DevState& S, const float* logits,
                         const int32_t* lengths, int32_t B, int32_t Tc, int32_t tau, hipStream_t st) {
-  LB_DISPATCH_BLOCK(block, k_frame, B, P, S, logits, lengths, Tc, tau);
+  if (K <= 16)
+    hipLaunchKernelGGL((k_frame<16, 4>), dim3(B), dim3(64), 0, st, P, S, logits, lengths, Tc, tau);
+  else if (K <= 32)
+    hipLaunchKernelGGL((k_frame<32, 4>), dim3(B), dim3(128), 0, st, P, S, logits, lengths, Tc, tau);
+  else if (K <= 64)
+    hipLaunchKernelGGL((k_frame<64, 4>), dim3(B), dim3(256), 0, st, P, S, logits, lengths, Tc, tau);
+  else if (K <= 128)
+    hipLaunchKernelGGL((k_frame<128, 4>), dim3(B), dim3(512), 0, st, P, S, logits, lengths, Tc, tau);
+  else
+    hipLaunchKernelGGL((k_frame<256, 4>), dim3(B), dim3(1024), 0, st, P, S, logits, lengths, Tc, tau);
   return hipGetLastError();
 }
 
-hipError_t launch_ngram(int grid, const DevParams& P, const DevState& S, int32_t tau, hipStream_t st) {
-  hipLaunchKernelGGL(k_ngram, dim3(grid), dim3(256), 0, st, P, S, tau);
+hipError_t launch_lmquery(int grid, const DevParams& P, const DevState& S, int32_t tau, hipStream_t st) {
+  hipLaunchKernelGGL(k_lmquery, dim3(grid), dim3(256), 0, st, P, S, tau);
+  return hipGetLastError();
+}
+
+hipError_t launch_lmselect(int grid, const DevParams& P, const DevState& S, int32_t tau, hipStream_t st) {
+  hipLaunchKernelGGL(k_lmselect, dim3(grid), dim3(256), 0, st, P, S, tau);
   return hipGetLastError();
 }
 

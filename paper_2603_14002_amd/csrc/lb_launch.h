@@ -11,9 +11,10 @@ hipError_t launch_build_order(int order, const int32_t* ids, const float* lp, co
                               int32_t vocab, NgramTable t2, NgramTable t3, NgramTable dst, uint32_t* flags,
                               hipStream_t st);
 hipError_t launch_begin(const DevParams& P, const DevState& S, int32_t B, hipStream_t st);
-hipError_t launch_frame(int block, const DevParams& P, const DevState& S, const float* logits,
+hipError_t launch_frame(int K, const DevParams& P, const DevState& S, const float* logits,
                         const int32_t* lengths, int32_t B, int32_t Tc, int32_t tau, hipStream_t st);
-hipError_t launch_ngram(int grid, const DevParams& P, const DevState& S, int32_t tau, hipStream_t st);
+hipError_t launch_lmquery(int grid, const DevParams& P, const DevState& S, int32_t tau, hipStream_t st);
+hipError_t launch_lmselect(int grid, const DevParams& P, const DevState& S, int32_t tau, hipStream_t st);
 hipError_t launch_fusion(int block, const DevParams& P, const DevState& S, const int32_t* lengths, int32_t B,
                          int32_t tau, hipStream_t st);
 hipError_t launch_output(int block, const DevParams& P, const DevState& S, const int32_t* lengths, int32_t B,
