@@ -96,6 +96,7 @@ HostTrie build_trie(const lb_lexicon_desc& lex) {
       }
     }
     if (k != 0 && !at[o].empty()) tn.mask |= 1ull << kSep;
+    tn.mask |= static_cast<uint64_t>(at[o].size()) << kWordCountShift;
     tn.word_off = woff;
     t.max_homophones = std::max<uint32_t>(t.max_homophones, static_cast<uint32_t>(at[o].size()));
     for (int32_t w : at[o]) t.words.push_back(w);
@@ -358,6 +359,10 @@ lb_status lb_create(const lb_lexicon_desc* lex, const lb_ngram_desc* lm, const l
   }
   // the lexicon trie (host), whose largest homophone set bounds the queries of a frame
   HostTrie trie = build_trie(*lex);
+  if (trie.max_homophones >= (1u << (64 - kWordCountShift))) {
+    delete d;
+    return fail(LB_ERR_INVALID_ARG, "more than 65535 words share one phoneme spelling");
+  }
   const uint64_t qcap = static_cast<uint64_t>(B) * K * O * std::max<uint32_t>(1, trie.max_homophones);
   if (qcap >= 0xFFFFFFFFull) {
     delete d;

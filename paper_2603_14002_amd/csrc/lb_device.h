@@ -2,7 +2,8 @@
 //
 // HBM layout (all buffers allocated once in lb_create, for max_batch streams):
 //   trie        TrieNode[S+1]   16 B/node: child mask (bits 1..39 phonemes, bit 40
-//                               separator when the node ends a word), index of the
+//                               separator when the node ends a word, bits 48..63
+//                               the number of words ending there), index of the
 //                               first child (children are contiguous, in phoneme
 //                               order), offset of the node's words in trie_words
 //   trie_words  int32[]         word ids ending at each node, ascending
@@ -32,6 +33,7 @@ constexpr uint64_t kNoParent = 0xFFFFFFFFFFFFFFFEull;  // parent key of the empt
 constexpr uint32_t kRootNode = 0;                      // trie root
 constexpr uint32_t kRootHist = 0;                      // empty word history
 constexpr double kLn10 = 2.302585092994045684017991454684364208;
+constexpr int kWordCountShift = 48;  // TrieNode::mask bits 48..63: words ending at the node
 
 // overflow / error flag bits (DevState::flags)
 constexpr uint32_t kFlagArena = 1u;

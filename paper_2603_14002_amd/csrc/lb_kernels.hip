@@ -26,6 +26,16 @@ namespace {
 constexpr double kNegInf = -HUGE_VAL;
 constexpr int kBins = 1024;         // score bins of the top-K selection
 constexpr int kBoundaryCap = 256;   // candidates resolved exactly inside the boundary bin
+constexpr int kMaxLevels = 16;      // refinement levels of the top-K selection
+#ifndef LB_CACHE_SCORES
+#define LB_CACHE_SCORES 1
+#endif
+#ifndef LB_CAND_UNROLL
+#define LB_CAND_UNROLL 64
+#endif
+#ifndef LB_LPB_LARGE
+#define LB_LPB_LARGE 4
+#endif
 
 // ------------------------------------------------------------------ block helpers
 
@@ -40,6 +50,31 @@ __device__ inline double block_max(double v, double* red) {
   for (int k = 1; k < BLOCK / 64; ++k) r = fmax(r, red[k]);
   __syncthreads();
   return r;
+}
+
+// Block-wide maximum of `mx` and minimum of `mn` in one reduction.
+template <int BLOCK>
+__device__ inline void block_minmax(double mx, double mn, double* red, double* out_max, double* out_min) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    mx = fmax(mx, __shfl_xor(mx, o, 64));
+    mn = fmin(mn, __shfl_xor(mn, o, 64));
+  }
+  constexpr int NW = BLOCK / 64;
+  if ((threadIdx.x & 63) == 0) {
+    red[threadIdx.x >> 6] = mx;
+    red[NW + (threadIdx.x >> 6)] = mn;
+  }
+  __syncthreads();
+  double a = red[0], c = red[NW];
+#pragma unroll
+  for (int k = 1; k < NW; ++k) {
+    a = fmax(a, red[k]);
+    c = fmin(c, red[NW + k]);
+  }
+  __syncthreads();
+  *out_max = a;
+  *out_min = c;
 }
 
 // Exclusive prefix sum over the block; *total receives the block sum.
@@ -240,6 +275,7 @@ __global__ __launch_bounds__(KMAX * LPB) void k_frame(const DevParams P, const D
   constexpr int BLOCK = KMAX * LPB;
   constexpr int HS = 2 * KMAX;  // LDS hash slots for the current prefix keys
   constexpr int NW = BLOCK / 64;
+  constexpr int NC = (kSep + LPB - 1) / LPB;  // extension slots per lane
   const int b = blockIdx.x;
   const int tid = threadIdx.x;
   if (b == 0 && tid == 0) S.evq[(tau + 1) & 1] = 0;
@@ -248,7 +284,7 @@ __global__ __launch_bounds__(KMAX * LPB) void k_frame(const DevParams P, const D
   __shared__ double sD[kClasses];
   __shared__ uint64_t sKey[KMAX], sPkey[KMAX];
   __shared__ double sAb[KMAX], sP[KMAX], sL[KMAX], sAb2[KMAX], sAnb2[KMAX], sStay[KMAX];
-  __shared__ uint32_t sNode[KMAX], sMeta[KMAX], sFirst[KMAX];
+  __shared__ uint32_t sNode[KMAX], sMeta[KMAX], sFirst[KMAX], sWoff[KMAX], sNwords[KMAX];
   __shared__ uint64_t sMask[KMAX], sTrieMask[KMAX];
   __shared__ double sLw[KMAX * kMaxSub];
   __shared__ uint32_t sHist[KMAX * kMaxSub];
@@ -257,14 +293,13 @@ __global__ __launch_bounds__(KMAX * LPB) void k_frame(const DevParams P, const D
   __shared__ uint32_t sHisto[kBins];
   __shared__ double sBScore[kBoundaryCap];
   __shared__ uint64_t sBKey[kBoundaryCap];
-  __shared__ int32_t sBCount;
-  __shared__ double sSelScore[KMAX];
-  __shared__ uint64_t sSelKey[KMAX];
+  __shared__ double sLvHi[kMaxLevels], sLvInv[kMaxLevels];
+  __shared__ int32_t sLvBeta[kMaxLevels], sLvShift[kMaxLevels];
   __shared__ uint32_t sSelSrc[KMAX];
   __shared__ uint32_t sEvQ[KMAX];
-  __shared__ double sRed[NW];
+  __shared__ double sRed[2 * NW];
   __shared__ int32_t sScan[NW];
-  __shared__ int32_t sBucket, sAbove, sBucketCnt;
+  __shared__ int32_t sBucket, sAbove, sBucketCnt, sBCount;
   __shared__ unsigned long long sEvBase;
 
   const int n = S.nbeam[b];
@@ -284,6 +319,7 @@ __global__ __launch_bounds__(KMAX * LPB) void k_frame(const DevParams P, const D
     my_anb = S.anb[gb + tid];
     const uint32_t node = S.node[gb + tid];
     my_meta = S.meta[gb + tid];
+    const TrieNode tn = S.trie[node];
     sKey[tid] = my_key;
     sPkey[tid] = my_pkey;
     sAb[tid] = ab;
@@ -296,10 +332,11 @@ __global__ __launch_bounds__(KMAX * LPB) void k_frame(const DevParams P, const D
       sHist[tid * kMaxSub + j] = S.hist[(gb + tid) * P.O + j];
     }
     sL[tid] = sLw[tid * kMaxSub];
-    const TrieNode tn = S.trie[node];
     sMask[tid] = tn.mask;
     sTrieMask[tid] = tn.mask;
     sFirst[tid] = tn.first_child;
+    sWoff[tid] = tn.word_off;
+    sNwords[tid] = static_cast<uint32_t>(tn.mask >> kWordCountShift);
   }
   __syncthreads();
 
@@ -353,46 +390,47 @@ __global__ __launch_bounds__(KMAX * LPB) void k_frame(const DevParams P, const D
   }
   __syncthreads();
 
-  // ---- this lane's candidates, scores cached in registers: slot k is the
-  // extension by v = 1 + ln + LPB*k, plus the merged stay on lane 0
-  constexpr int NC = (kSep + LPB - 1) / LPB;
+  // ---- this lane's candidates: slot k is the extension by v = 1 + ln + LPB*k,
+  // plus the merged stay on lane 0; scores are recomputed in every pass (same
+  // operations, same result)
   const int hi_ = tid / LPB;
   const int ln = tid - hi_ * LPB;
   const bool live = hi_ < n;
-  uint64_t c_key = 0;
-  double c_stay = kNegInf;
-  double sc[NC];
-  {
-    double c_ab = 0.0, c_p = 0.0, c_L = 0.0;
-    int c_last = 0;
-    uint64_t c_mask = 0;
-    if (live) {
-      c_ab = sAb[hi_];
-      c_p = sP[hi_];
-      c_L = sL[hi_];
-      c_last = sMeta[hi_] & 0xFF;
-      c_mask = sMask[hi_];
-      c_key = sKey[hi_];
-      if (ln == 0) c_stay = sStay[hi_];
-    }
-#pragma unroll
-    for (int k = 0; k < NC; ++k) {
-      const int v = 1 + ln + LPB * k;
-      double s = kNegInf;
-      if (v <= kSep && ((c_mask >> v) & 1ull)) {
-        const double base = (v == c_last) ? c_ab : c_p;
-        s = ((base + sD[v]) + (v == kSep ? P.gamma : P.beta)) + c_L;
-      }
-      sc[k] = s;
-    }
+  uint64_t c_key = 0, c_mask = 0;
+  double c_stay = kNegInf, c_ab = 0.0, c_p = 0.0, c_L = 0.0;
+  int c_last = 0;
+  if (live) {
+    c_ab = sAb[hi_];
+    c_p = sP[hi_];
+    c_L = sL[hi_];
+    c_last = sMeta[hi_] & 0xFF;
+    c_mask = sMask[hi_];
+    c_key = sKey[hi_];
+    if (ln == 0) c_stay = sStay[hi_];
   }
+  auto score_now = [&](int k) -> double {
+    const int v = 1 + ln + LPB * k;
+    if (v > kSep || !((c_mask >> v) & 1ull)) return kNegInf;
+    const double base = (v == c_last) ? c_ab : c_p;
+    return ((base + sD[v]) + (v == kSep ? P.gamma : P.beta)) + c_L;
+  };
+#if LB_CACHE_SCORES
+  double sc[NC];
+#pragma unroll
+  for (int k = 0; k < NC; ++k) sc[k] = score_now(k);
+  auto score_of = [&](int k) -> double { return sc[k]; };
+#else
+  auto score_of = score_now;
+#endif
   auto key_of = [&](int v) -> uint64_t { return v == 0 ? c_key : prefix_step(c_key, v); };
   // f(v, score) for each of this lane's candidates with a finite score
   auto for_cands = [&](auto&& f) {
     if (c_stay != kNegInf) f(0, c_stay);
-#pragma unroll
-    for (int k = 0; k < NC; ++k)
-      if (sc[k] != kNegInf) f(1 + ln + LPB * k, sc[k]);
+#pragma unroll LB_CAND_UNROLL
+    for (int k = 0; k < NC; ++k) {
+      const double s = score_of(k);
+      if (s != kNegInf) f(1 + ln + LPB * k, s);
+    }
   };
 
   double mx = kNegInf, mn = HUGE_VAL;
@@ -400,49 +438,65 @@ __global__ __launch_bounds__(KMAX * LPB) void k_frame(const DevParams P, const D
     mx = fmax(mx, s);
     mn = fmin(mn, s);
   });
-  const double best = block_max<BLOCK>(mx, sRed);
-  const double lowest = -block_max<BLOCK>(-mn, sRed);
+  double best, lowest;
+  block_minmax<BLOCK>(mx, mn, sRed, &best, &lowest);
   const double thr = best - P.theta;
 
-  // ---- top-K.  Bins of (best - score) over [max(thr, lowest), best] order the
-  // candidates (the map is monotone); bins above the one holding the K-th are
-  // taken whole, and that bin is resolved exactly by rank on (score desc, key
-  // asc).  If that bin is too crowded, an MSD radix select over (ordered score
-  // bits, ~key) decides instead.
-  const double lo_s = fmax(thr, lowest);
-  const double width = best - lo_s;
-  const double inv_w = width > 0.0 ? static_cast<double>(kBins) / width : 0.0;
-  auto bin_of = [&](double s) -> int {
-    const double x = (best - s) * inv_w;
+  // ---- top-K.  Level 0 bins (best - score) over [max(thr, lowest), best] into
+  // kBins; the map is monotone, so bins above the one holding the K-th
+  // candidate are taken whole.  That bin is resolved exactly by rank on
+  // (score desc, key asc) when it holds at most kBoundaryCap candidates;
+  // otherwise it is re-binned over its own score range (deeper levels), and
+  // when its scores are all equal, by the bits of the key (smaller key first).
+  const double lo0 = fmax(thr, lowest);
+  const double inv0 = best > lo0 ? static_cast<double>(kBins) / (best - lo0) : 0.0;
+  const int shift0 = best > lo0 ? -1 : 64 - 10;
+  auto bin_score = [&](double hi, double inv, double s) -> int {
+    const double x = (hi - s) * inv;
     return x >= static_cast<double>(kBins - 1) ? kBins - 1 : static_cast<int>(x);
   };
-  for (int d = tid; d < kBins; d += BLOCK) sHisto[d] = 0;
-  __syncthreads();
-  for_cands([&](int, double s) {
-    if (s >= thr) atomicAdd(&sHisto[bin_of(s)], 1u);
-  });
-  __syncthreads();
-  // bin holding the K-th candidate: each thread sums kBins/BLOCK consecutive bins
-  constexpr int PER = (kBins + BLOCK - 1) / BLOCK;
-  int local = 0;
+  auto bin0 = [&](int v, double s) -> int {
+    return shift0 < 0 ? bin_score(best, inv0, s) : static_cast<int>((key_of(v) >> shift0) & (kBins - 1));
+  };
+  // deeper levels (rare): parameters in LDS
+  auto bin_at = [&](int l, int v, double s) -> int {
+    const int sh = sLvShift[l];
+    if (sh >= 0) return static_cast<int>((key_of(v) >> sh) & (kBins - 1));
+    return bin_score(sLvHi[l], sLvInv[l], s);
+  };
+  // candidates in the boundary bin of levels 0..L-1
+  auto member = [&](int L, int v, double s) -> bool {
+    if (s < thr || bin0(v, s) != sLvBeta[0]) return false;
+    for (int l = 1; l < L; ++l)
+      if (bin_at(l, v, s) != sLvBeta[l]) return false;
+    return true;
+  };
+  // the lane's candidates with scores recomputed (no register array): for the rare levels
+  auto for_cands_rt = [&](auto&& f) {
+    if (c_stay != kNegInf) f(0, c_stay);
+#pragma unroll 1
+    for (int k = 0; k < NC; ++k) {
+      const double s = score_now(k);
+      if (s != kNegInf) f(1 + ln + LPB * k, s);
+    }
+  };
+  // finds the bin holding the need-th candidate of sHisto; returns via sBucket/sAbove/sBucketCnt
+  auto find_bin = [&](int need_in) -> int {
+    constexpr int PER = (kBins + BLOCK - 1) / BLOCK;
+    int local = 0;
 #pragma unroll
-  for (int q = 0; q < PER; ++q) {
-    const int d = tid * PER + q;
-    local += d < kBins ? static_cast<int>(sHisto[d]) : 0;
-  }
-  int nvalid = 0;
-  const int before = block_scan<BLOCK>(local, sScan, &nvalid);
-  const bool select_all = nvalid <= P.K;
-  int beta_bin = kBins, need_b = 0, nbc = 0;
-  bool use_radix = false;
-  uint64_t pre_hi = 0, pre_lo = 0;
-  if (!select_all) {
-    if (before < P.K && before + local >= P.K) {
+    for (int q = 0; q < PER; ++q) {
+      const int d = tid * PER + q;
+      local += d < kBins ? static_cast<int>(sHisto[d]) : 0;
+    }
+    int tot = 0;
+    const int before = block_scan<BLOCK>(local, sScan, &tot);
+    if (need_in > 0 && before < need_in && before + local >= need_in) {
       int acc = before;
       for (int q = 0; q < PER; ++q) {
         const int d = tid * PER + q;
         const int h = static_cast<int>(sHisto[d]);
-        if (acc + h >= P.K) {
+        if (acc + h >= need_in) {
           sBucket = d;
           sAbove = acc;
           sBucketCnt = h;
@@ -452,141 +506,119 @@ __global__ __launch_bounds__(KMAX * LPB) void k_frame(const DevParams P, const D
       }
     }
     __syncthreads();
-    beta_bin = sBucket;
-    need_b = P.K - sAbove;
-    const int nb_bin = sBucketCnt;
-    if (nb_bin != need_b) {
-      if (nb_bin <= kBoundaryCap) {
-        nbc = nb_bin;
-        if (tid == 0) sBCount = 0;
-        __syncthreads();
-        for_cands([&](int v, double s) {
-          if (s >= thr && bin_of(s) == beta_bin) {
-            const int slot = atomicAdd(&sBCount, 1);
-            sBScore[slot] = s;
-            sBKey[slot] = key_of(v);
-          }
-        });
-        __syncthreads();
-      } else {
-        use_radix = true;
-      }
+    return tot;
+  };
+
+  for (int d = tid; d < kBins; d += BLOCK) sHisto[d] = 0;
+  __syncthreads();
+  for_cands([&](int v, double s) {
+    if (s >= thr) atomicAdd(&sHisto[bin0(v, s)], 1u);
+  });
+  __syncthreads();
+  const int nvalid = find_bin(P.K);
+  const bool select_all = nvalid <= P.K;
+  int beta0 = kBins, nlev = 1, need = P.K, nbc = 0;
+  bool all_bin = false;
+  if (!select_all) {
+    beta0 = sBucket;
+    need -= sAbove;
+    int cntb = sBucketCnt;
+    if (tid == 0) {
+      sLvBeta[0] = beta0;
+      sLvShift[0] = shift0;
     }
-  }
-  if (use_radix) {
-    uint64_t m_hi = 0, m_lo = 0;
-    const uint64_t ob_best = order_bits(best), ob_thr = order_bits(thr);
-    const int common = (ob_best == ob_thr) ? 64 : __clzll(static_cast<long long>(ob_best ^ ob_thr));
-    int pos = ((127 - common) / 8) * 8;
-    mask_from(pos + 8, &m_hi, &m_lo);
-    pre_hi = ob_best & m_hi;
-    pre_lo = 0;
-    int need = P.K;
-    for (;;) {
-      for (int d = tid; d < 256; d += BLOCK) sHisto[d] = 0;
+    __syncthreads();
+    int key_shift = shift0 >= 0 ? shift0 - 10 : 64 - 10;
+    bool key_level = shift0 >= 0;
+    while (cntb != need && cntb > kBoundaryCap && !(key_level && sLvShift[nlev - 1] == 0) && nlev < kMaxLevels) {
+      // refine: score range of the boundary bin's members, or key bits when it is flat
+      const int L = nlev;
+      double bmx = kNegInf, bmn = HUGE_VAL;
+      for_cands_rt([&](int v, double s) {
+        if (member(L, v, s)) {
+          bmx = fmax(bmx, s);
+          bmn = fmin(bmn, s);
+        }
+      });
+      double lv_hi, lv_lo;
+      block_minmax<BLOCK>(bmx, bmn, sRed, &lv_hi, &lv_lo);
+      if (tid == 0) {
+        sLvHi[L] = lv_hi;
+        sLvInv[L] = lv_hi > lv_lo ? static_cast<double>(kBins) / (lv_hi - lv_lo) : 0.0;
+        sLvShift[L] = lv_hi > lv_lo ? -1 : (key_shift > 0 ? key_shift : 0);
+      }
+      for (int d = tid; d < kBins; d += BLOCK) sHisto[d] = 0;
       __syncthreads();
-      const bool want_key = pos < 64;
-      for_cands([&](int v, double s) {
-        if (s < thr) return;
-        const uint64_t h = order_bits(s);
-        if ((h & m_hi) != pre_hi) return;
-        const uint64_t lo = want_key ? ~key_of(v) : 0;
-        if ((lo & m_lo) != pre_lo) return;
-        atomicAdd(&sHisto[digit128(h, lo, pos)], 1u);
+      key_level = sLvShift[L] >= 0;
+      if (key_level) key_shift -= 10;
+      for_cands_rt([&](int v, double s) {
+        if (member(L, v, s)) atomicAdd(&sHisto[bin_at(L, v, s)], 1u);
       });
       __syncthreads();
-      if (tid < 64) {
-        // lane l owns bins 4l..4l+3; find the bin holding the need-th largest
-        const int l = tid;
-        const uint32_t h0 = sHisto[4 * l], h1 = sHisto[4 * l + 1], h2 = sHisto[4 * l + 2],
-                       h3 = sHisto[4 * l + 3];
-        const int mine = static_cast<int>(h0 + h1 + h2 + h3);
-        int suf = mine;  // inclusive suffix sum over lanes >= l
-#pragma unroll
-        for (int o = 1; o < 64; o <<= 1) {
-          const int y = __shfl_down(suf, o, 64);
-          if (l + o < 64) suf += y;
-        }
-        const int above_lane = suf - mine;
-        if (above_lane < need && suf >= need) {
-          int acc = above_lane;
-          const uint32_t hh[4] = {h0, h1, h2, h3};
-          for (int q = 3; q >= 0; --q) {
-            if (acc + static_cast<int>(hh[q]) >= need) {
-              sBucket = 4 * l + q;
-              sAbove = acc;
-              sBucketCnt = static_cast<int>(hh[q]);
-              break;
-            }
-            acc += static_cast<int>(hh[q]);
-          }
-        }
-      }
-      __syncthreads();
-      const int bucket = sBucket;
+      (void)find_bin(need);
+      if (tid == 0) sLvBeta[L] = sBucket;
       need -= sAbove;
-      const int bcnt = sBucketCnt;
+      cntb = sBucketCnt;
+      nlev = L + 1;
       __syncthreads();
-      if (pos >= 64) {
-        pre_hi |= static_cast<uint64_t>(bucket) << (pos - 64);
-      } else if (pos > 56) {
-        pre_hi |= static_cast<uint64_t>(bucket) >> (64 - pos);
-        pre_lo |= static_cast<uint64_t>(bucket) << pos;
-      } else {
-        pre_lo |= static_cast<uint64_t>(bucket) << pos;
-      }
-      mask_from(pos, &m_hi, &m_lo);
-      if (bcnt == need || pos == 0) break;
-      pos -= 8;
+    }
+    if (cntb == need) {
+      all_bin = true;
+    } else {
+      // exact rank inside the boundary bin (a flat key level of shift 0 holds one key)
+      if (tid == 0) sBCount = 0;
+      __syncthreads();
+      const int L = nlev;
+      for_cands_rt([&](int v, double s) {
+        if (!member(L, v, s)) return;
+        const int slot = atomicAdd(&sBCount, 1);
+        if (slot < kBoundaryCap) {
+          sBScore[slot] = s;
+          sBKey[slot] = key_of(v);
+        }
+      });
+      __syncthreads();
+      nbc = sBCount < kBoundaryCap ? sBCount : kBoundaryCap;
+      if (sBCount > kBoundaryCap && tid == 0) atomicOr(S.flags, kFlagSelect);
     }
   }
   auto selected = [&](int v, double s) -> bool {
     if (s < thr) return false;
     if (select_all) return true;
-    if (use_radix) {
-      const uint64_t h = order_bits(s);
-      if (h != pre_hi) return h > pre_hi;
-      return ~key_of(v) >= pre_lo;
+    const int bn = bin0(v, s);
+    if (bn != beta0) return bn < beta0;
+    for (int l = 1; l < nlev; ++l) {
+      const int bl = bin_at(l, v, s);
+      if (bl != sLvBeta[l]) return bl < sLvBeta[l];
     }
-    const int bn = bin_of(s);
-    if (bn != beta_bin) return bn < beta_bin;
-    if (nbc == 0) return true;
+    if (all_bin) return true;
     // rank inside the boundary bin by (score desc, key asc)
     const uint64_t k = key_of(v);
     int rank = 0;
     for (int u = 0; u < nbc; ++u) rank += ranks_before(sBScore[u], sBKey[u], s, k);
-    return rank < need_b;
+    return rank < need;
   };
 
   // ---- selection bits (bit 0: the stay, bit k+1: slot k), then a
-  // deterministic gather in lane order
+  // deterministic gather of the sources in lane order
   uint64_t sel_bits = 0;
   if (c_stay != kNegInf && selected(0, c_stay)) sel_bits |= 1ull;
-#pragma unroll
-  for (int k = 0; k < NC; ++k)
-    if (sc[k] != kNegInf && selected(1 + ln + LPB * k, sc[k])) sel_bits |= 2ull << k;
+#pragma unroll LB_CAND_UNROLL
+  for (int k = 0; k < NC; ++k) {
+    const double s = score_of(k);
+    if (s != kNegInf && selected(1 + ln + LPB * k, s)) sel_bits |= 2ull << k;
+  }
   int nsel = 0;
   int wpos = block_scan<BLOCK>(__popcll(sel_bits), sScan, &nsel);
   if (nsel > P.K) {  // cannot happen when the selection is exact; never write past K entries
     nsel = P.K;
     if (tid == 0) atomicOr(S.flags, kFlagSelect);
   }
-  if ((sel_bits & 1ull) && wpos < nsel) {
-    sSelScore[wpos] = c_stay;
-    sSelKey[wpos] = c_key;
-    sSelSrc[wpos] = static_cast<uint32_t>(hi_);
-    ++wpos;
-  }
-#pragma unroll
-  for (int k = 0; k < NC; ++k) {
-    if (((sel_bits >> (k + 1)) & 1ull) && wpos < nsel) {
-      const int v = 1 + ln + LPB * k;
-      sSelScore[wpos] = sc[k];
-      sSelKey[wpos] = prefix_step(c_key, v);
-      sSelSrc[wpos] = static_cast<uint32_t>(hi_) | (static_cast<uint32_t>(v) << 16);
-      ++wpos;
-    }
-  }
+  if ((sel_bits & 1ull) && wpos < nsel) sSelSrc[wpos++] = static_cast<uint32_t>(hi_);
+#pragma unroll LB_CAND_UNROLL
+  for (int k = 0; k < NC; ++k)
+    if (((sel_bits >> (k + 1)) & 1ull) && wpos < nsel)
+      sSelSrc[wpos++] = static_cast<uint32_t>(hi_) | (static_cast<uint32_t>(1 + ln + LPB * k) << 16);
   __syncthreads();
 
   // ---- write the new hypotheses (in place: every old value is in LDS)
@@ -610,7 +642,7 @@ __global__ __launch_bounds__(KMAX * LPB) void k_frame(const DevParams P, const D
     } else {
       const int last = meta_i & 0xFF;
       const double base = (v == last) ? sAb[i] : sP[i];
-      S.key[o] = sSelKey[r];
+      S.key[o] = prefix_step(sKey[i], v);
       S.pkey[o] = sKey[i];
       S.ab[o] = kNegInf;
       S.anb[o] = (base + sD[v]) + (v == kSep ? P.gamma : P.beta);
@@ -621,8 +653,8 @@ __global__ __launch_bounds__(KMAX * LPB) void k_frame(const DevParams P, const D
       if (v == kSep) {
         is_event = 1;
         ev_pnode = sNode[i];
-        ev_woff = S.trie[ev_pnode].word_off;
-        ev_H = S.trie[ev_pnode + 1].word_off - ev_woff;
+        ev_woff = sWoff[i];
+        ev_H = sNwords[i];
         ev_nsub = static_cast<uint32_t>(nsub);
         my_nq = static_cast<int>(ev_nsub * ev_H);
         ev_src = i;
@@ -1089,9 +1121,11 @@ hipError_t launch_frame(int K, const DevParams& P, const DevState& S, const floa
   else if (K <= 64)
     hipLaunchKernelGGL((k_frame<64, 4>), dim3(B), dim3(256), 0, st, P, S, logits, lengths, Tc, tau);
   else if (K <= 128)
-    hipLaunchKernelGGL((k_frame<128, 4>), dim3(B), dim3(512), 0, st, P, S, logits, lengths, Tc, tau);
+    hipLaunchKernelGGL((k_frame<128, LB_LPB_LARGE>), dim3(B), dim3(128 * LB_LPB_LARGE), 0, st, P, S, logits, lengths,
+                       Tc, tau);
   else
-    hipLaunchKernelGGL((k_frame<256, 4>), dim3(B), dim3(1024), 0, st, P, S, logits, lengths, Tc, tau);
+    hipLaunchKernelGGL((k_frame<256, LB_LPB_LARGE>), dim3(B), dim3(256 * LB_LPB_LARGE), 0, st, P, S, logits, lengths,
+                       Tc, tau);
   return hipGetLastError();
 }
 
