@@ -152,21 +152,26 @@ void lb_destroy(lb_decoder* dec);
  * outputs rank the current hypotheses (completed words only).  With
  * LB_FUSION_EXTERNAL the call may return LB_NEED_FUSION: the caller then calls
  * lb_fusion_request and lb_fusion_scores and repeats this call with the same
- * arguments, which resumes after the fused frame.  Asynchronous on `stream`. */
+ * arguments, which resumes after the fused frame (with LB_END, a last
+ * LB_NEED_FUSION precedes the final outputs).  Asynchronous on `stream`, except
+ * with LB_FUSION_EXTERNAL, where the call reads `lengths` to the host. */
 lb_status lb_decode_batch(lb_decoder* dec, const float* logits, const int32_t* lengths,
                           int32_t batch, int32_t frames, uint32_t flags, void* stream,
                           int32_t* out_hyps, float* out_scores);
 
-/* Exports the word sequences of a pending fusion event (after LB_NEED_FUSION):
- *   words    device int32 [batch][F][subbeams][max_words_out], -1 padded
- *   n_words  device int32 [batch][F][subbeams]; -1 where no sub-beam is to be
- *            scored (stream not fusing, fewer hypotheses or sub-beams)
- * F = fusion_top_f (or beam when 0; beam for the final event).
+/* Exports the word sequences of a pending fusion event (after LB_NEED_FUSION).
+ * Entry [b][r][j] is sub-beam j of the stream's r-th fused hypothesis; the
+ * fused hypotheses are the top fusion_top_f (all when 0) by total score at a
+ * fusion frame, and all hypotheses at the end of an utterance:
+ *   words    device int32 [batch][beam][subbeams][max_words_out], -1 padded
+ *   n_words  device int32 [batch][beam][subbeams]: number of words, or -1
+ *            where nothing is to be scored (stream not fusing this frame,
+ *            fewer hypotheses or sub-beams)
  * LB_ERR_STATE if no fusion is pending. */
 lb_status lb_fusion_request(lb_decoder* dec, int32_t* words, int32_t* n_words, void* stream);
 
 /* Applies Eq. (2) with caller-computed fusion scores for the pending event:
- *   fusion_logprobs  device float32 [batch][F][subbeams], natural-log
+ *   fusion_logprobs  device float32 [batch][beam][subbeams], natural-log
  *                    full-sequence scores sum_t log p(w_t | w_<t) of the
  *                    requested sequences (entries with n_words == -1 ignored)
  * Each requested sub-beam's word-level score becomes phi * score and the

@@ -138,6 +138,20 @@ struct lb_decoder {
   std::vector<hipEvent_t> pool;
   double kernel_ms[kKinds] = {};
   int64_t timed[kKinds] = {};
+  // external fusion round trip (LB_FUSION_EXTERNAL): host mirrors of the
+  // streams' frame counters and the state of an interrupted decode call
+  struct {
+    int pending = 0;  // 0 none, 1 fusion frame, 2 end of utterance
+    bool in_call = false, requested = false, final_done = false;
+    int32_t resume_tau = 0;
+    const float* logits = nullptr;
+    const int32_t* lengths = nullptr;
+    int32_t B = 0, Tc = 0;
+    uint32_t flags = 0;
+    std::vector<int64_t> t0;
+    std::vector<int32_t> len, flag;
+    int32_t* d_flag = nullptr;
+  } ext;
 
   template <typename T>
   lb_status alloc(T** ptr, size_t count) {
@@ -215,7 +229,6 @@ lb_status validate(const lb_lexicon_desc* lex, const lb_ngram_desc* lm, const lb
   if (p->fusion_source != LB_FUSION_NONE && p->fusion_interval < 1)
     return fail(LB_ERR_INVALID_ARG, "fusion needs fusion_interval >= 1");
   if (p->fusion_top_f < 0) return fail(LB_ERR_INVALID_ARG, "fusion_top_f < 0");
-  if (p->fusion_source == LB_FUSION_EXTERNAL) return fail(LB_ERR_INVALID_ARG, "external fusion is not supported yet");
   const double lf = p->lm_load_factor == 0.0 ? 0.5 : p->lm_load_factor;
   if (!(lf > 0.0 && lf <= 0.9)) return fail(LB_ERR_INVALID_ARG, "lm_load_factor must be in (0, 0.9]");
   for (double x : {p->alpha, p->beta, p->gamma, p->omega, p->phi, p->theta, p->lambda, p->fusion_lo, p->fusion_hi})
@@ -381,13 +394,17 @@ lb_status lb_create(const lb_lexicon_desc* lex, const lb_ngram_desc* lm, const l
       (st = d->alloc(&S.qS, qcap)) != LB_OK ||
       (st = d->alloc(&S.flags, 1)) != LB_OK || (st = d->alloc(&S.counters, static_cast<size_t>(B) * kNumCounters)) != LB_OK ||
       (st = d->alloc(&S.fsel, BK)) != LB_OK || (st = d->alloc(&S.fsel_n, B)) != LB_OK ||
-      (st = d->alloc(&S.lines, static_cast<size_t>(kSpread) * kSpreadStride)) != LB_OK) {
+      (st = d->alloc(&S.lines, static_cast<size_t>(kSpread) * kSpreadStride)) != LB_OK ||
+      (st = d->alloc(&d->ext.d_flag, B)) != LB_OK) {
     std::string msg = g_err;
     delete d;
     return fail(st, msg);
   }
   S.arena_cap = cap;
   S.qcap = qcap;
+  d->ext.t0.assign(B, 0);
+  d->ext.len.assign(B, 0);
+  d->ext.flag.assign(B, 0);
   auto init = [&]() -> lb_status {
     LB_HIP(hipMemset(S.nbeam, 0, B * sizeof(int32_t)));
     LB_HIP(hipMemset(S.t0, 0, B * sizeof(int64_t)));
@@ -443,7 +460,8 @@ lb_status lb_decode_batch(lb_decoder* d, const float* logits, const int32_t* len
   hipStream_t st = static_cast<hipStream_t>(stream);
   const DevParams& P = d->P;
   const DevState& S = d->S;
-  const bool fusion = P.fusion_source == LB_FUSION_SYNTH_BIGRAM && P.fusion_interval > 0;
+  const bool synth = P.fusion_source == LB_FUSION_SYNTH_BIGRAM && P.fusion_interval > 0;
+  const bool external = P.fusion_source == LB_FUSION_EXTERNAL;
   EventPair ep{};
   auto launch = [&](int kind, auto&& fn) -> hipError_t {
     if (d->profiling) record_start(d, st, &ep, kind);
@@ -452,32 +470,100 @@ lb_status lb_decode_batch(lb_decoder* d, const float* logits, const int32_t* len
     d->launches[kind]++;
     return e;
   };
-  if (flags & LB_BEGIN) LB_HIP(launch_begin(P, S, batch, st));
-  for (int32_t tau = 0; tau < frames; ++tau) {
+  auto& X = d->ext;
+  int32_t start = 0;
+  bool resuming = false;
+  if (external) {
+    if (X.in_call) {
+      resuming = true;
+      // resuming a call that returned LB_NEED_FUSION
+      if (logits != X.logits || lengths != X.lengths || batch != X.B || frames != X.Tc || flags != X.flags)
+        return fail(LB_ERR_STATE, "a decode call awaiting fusion scores must be repeated with the same arguments");
+      if (X.pending) return fail(LB_ERR_STATE, "fusion scores for the pending request have not been supplied");
+      start = X.resume_tau;
+    } else {
+      // the frame counters of the streams decide where fusion happens: read the lengths
+      LB_HIP(hipMemcpyAsync(X.len.data(), lengths, batch * sizeof(int32_t), hipMemcpyDeviceToHost, st));
+      LB_HIP(hipStreamSynchronize(st));
+      for (int32_t b = 0; b < batch; ++b)
+        if (X.len[b] < 0 || X.len[b] > frames) return fail(LB_ERR_INVALID_ARG, "lengths must be in 0..frames");
+      if (flags & LB_BEGIN)
+        for (int32_t b = 0; b < batch; ++b) X.t0[b] = 0;
+      X.in_call = true;
+      X.final_done = false;
+      X.logits = logits;
+      X.lengths = lengths;
+      X.B = batch;
+      X.Tc = frames;
+      X.flags = flags;
+    }
+  }
+  if (!resuming && (flags & LB_BEGIN)) LB_HIP(launch_begin(P, S, batch, st));
+  for (int32_t tau = start; tau < frames; ++tau) {
     LB_HIP(launch(kKindFrame, [&] { return launch_frame(P.K, P, S, logits, lengths, batch, frames, tau, st); }));
     LB_HIP(launch(kKindLmQuery, [&] { return launch_lmquery(d->lmq_grid, P, S, tau, st); }));
     LB_HIP(launch(kKindLmSelect, [&] { return launch_lmselect(d->lms_grid, P, S, tau, st); }));
-    if (fusion) LB_HIP(launch(kKindFusion, [&] { return launch_fusion(d->block, P, S, lengths, batch, tau, st); }));
+    if (synth) LB_HIP(launch(kKindFusion, [&] { return launch_fusion(d->block, P, S, lengths, batch, tau, st); }));
+    if (external) {
+      bool any = false;
+      for (int32_t b = 0; b < batch; ++b) {
+        const int64_t t = X.t0[b] + tau;
+        X.flag[b] = (tau < X.len[b] && t > 0 && t % P.fusion_interval == 0) ? 1 : 0;
+        any = any || X.flag[b];
+      }
+      if (any) {
+        LB_HIP(hipMemcpyAsync(X.d_flag, X.flag.data(), batch * sizeof(int32_t), hipMemcpyHostToDevice, st));
+        LB_HIP(hipStreamSynchronize(st));
+        X.pending = 1;
+        X.requested = false;
+        X.resume_tau = tau + 1;
+        return LB_NEED_FUSION;
+      }
+    }
+  }
+  if (external && (flags & LB_END) && !X.final_done) {
+    for (int32_t b = 0; b < batch; ++b) X.flag[b] = 2;
+    LB_HIP(hipMemcpyAsync(X.d_flag, X.flag.data(), batch * sizeof(int32_t), hipMemcpyHostToDevice, st));
+    LB_HIP(hipStreamSynchronize(st));
+    X.pending = 2;
+    X.requested = false;
+    X.final_done = true;
+    X.resume_tau = frames;
+    return LB_NEED_FUSION;
   }
   LB_HIP(launch(kKindOutput, [&] {
     return launch_output(d->block, P, S, lengths, batch, (flags & LB_END) ? 1 : 0, out_hyps, out_scores, st);
   }));
+  if (external) {
+    for (int32_t b = 0; b < batch; ++b) X.t0[b] += X.len[b];
+    X.in_call = false;
+  }
   return LB_OK;
 }
 
 lb_status lb_fusion_request(lb_decoder* d, int32_t* words, int32_t* n_words, void* stream) {
-  (void)words;
-  (void)n_words;
-  (void)stream;
+  g_err.clear();
   if (!d) return fail(LB_ERR_INVALID_ARG, "decoder is null");
-  return fail(LB_ERR_STATE, "no fusion request is pending");
+  if (!d->ext.pending) return fail(LB_ERR_STATE, "no fusion request is pending");
+  if (!words || !n_words) return fail(LB_ERR_INVALID_ARG, "null device pointer");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  LB_HIP(launch_fuse_select(d->block, d->P, d->S, d->ext.d_flag, d->ext.B, st));
+  LB_HIP(launch_fuse_export(d->block, d->P, d->S, words, n_words, d->ext.B, st));
+  d->ext.requested = true;
+  return LB_OK;
 }
 
 lb_status lb_fusion_scores(lb_decoder* d, const float* fusion_logprobs, void* stream) {
-  (void)fusion_logprobs;
-  (void)stream;
+  g_err.clear();
   if (!d) return fail(LB_ERR_INVALID_ARG, "decoder is null");
-  return fail(LB_ERR_STATE, "no fusion request is pending");
+  if (!d->ext.pending) return fail(LB_ERR_STATE, "no fusion request is pending");
+  if (!fusion_logprobs) return fail(LB_ERR_INVALID_ARG, "null device pointer");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (!d->ext.requested) LB_HIP(launch_fuse_select(d->block, d->P, d->S, d->ext.d_flag, d->ext.B, st));
+  LB_HIP(launch_fuse_apply(d->block, d->P, d->S, fusion_logprobs, d->ext.B, st));
+  d->ext.pending = 0;
+  d->ext.requested = false;
+  return LB_OK;
 }
 
 lb_status lb_get_status(lb_decoder* d, void* stream) {

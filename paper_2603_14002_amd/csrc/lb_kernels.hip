@@ -940,13 +940,11 @@ __global__ __launch_bounds__(256) void k_lmselect(const DevParams P, const DevSt
 
 // ------------------------------------------------------------------ delayed fusion
 
-// Replaces the sub-beam scores of the top-F hypotheses of stream b by
-// phi * fusion score and re-ranks the sub-beams (stable).  `ext` (optional)
-// holds caller scores [K][O] by fusion rank; otherwise the synthetic score of
-// the history node is used.  Also records the selection in fsel.
+// Selects the top-F hypotheses of stream b by (total desc, key asc) into
+// S.fsel[b][0..F) and S.fsel_n[b] (F = all hypotheses when top_f <= 0).
 template <int BLOCK>
-__device__ void fuse_stream(const DevParams& P, const DevState& S, int b, int top_f, const float* ext,
-                            double* sc, uint64_t* ky, uint32_t* ix) {
+__device__ void select_fused(const DevParams& P, const DevState& S, int b, int top_f, double* sc, uint64_t* ky,
+                             uint32_t* ix) {
   const int tid = threadIdx.x;
   const int n = S.nbeam[b];
   const size_t gb = static_cast<size_t>(b) * P.K;
@@ -964,9 +962,22 @@ __device__ void fuse_stream(const DevParams& P, const DevState& S, int b, int to
     __syncthreads();
     bitonic_sort<BLOCK>(sc, ky, ix);
   }
+  if (tid < F) S.fsel[gb + tid] = (F < n) ? static_cast<int32_t>(ix[tid]) : tid;
+  if (tid == 0) S.fsel_n[b] = F;
+  __syncthreads();
+}
+
+// Delayed fusion on the selected hypotheses of stream b (Eq. (2)): each
+// sub-beam's word-level score becomes phi * its fusion score -- the synthetic
+// score kept in its history node, or the caller's ext[b][rank][j] -- and the
+// sub-beams are re-ranked (stable).
+template <int BLOCK>
+__device__ void apply_fused(const DevParams& P, const DevState& S, int b, const float* ext) {
+  const int tid = threadIdx.x;
+  const size_t gb = static_cast<size_t>(b) * P.K;
+  const int F = S.fsel_n[b];
   if (tid < F) {
-    const int i = (F < n) ? static_cast<int>(ix[tid]) : tid;
-    const size_t bi = gb + i;
+    const size_t bi = gb + S.fsel[gb + tid];
     const uint32_t meta = S.meta[bi];
     const int nsub = (meta >> 8) & 0xFF;
     double L[kMaxSub];
@@ -975,7 +986,7 @@ __device__ void fuse_stream(const DevParams& P, const DevState& S, int b, int to
     for (int j = 0; j < kMaxSub; ++j) {
       if (j < nsub) {
         h[j] = S.hist[bi * P.O + j];
-        const double f = ext ? static_cast<double>(ext[static_cast<size_t>(tid) * P.O + j]) : S.arena[h[j]].sfus;
+        const double f = ext ? static_cast<double>(ext[(gb + tid) * P.O + j]) : S.arena[h[j]].sfus;
         L[j] = P.phi * f;
       } else {
         L[j] = kNegInf;
@@ -1022,7 +1033,67 @@ __global__ __launch_bounds__(BLOCK) void k_fusion(const DevParams P, const DevSt
   __shared__ double sc[BLOCK];
   __shared__ uint64_t ky[BLOCK];
   __shared__ uint32_t ix[BLOCK];
-  fuse_stream<BLOCK>(P, S, b, P.fusion_top_f, nullptr, sc, ky, ix);
+  select_fused<BLOCK>(P, S, b, P.fusion_top_f, sc, ky, ix);
+  apply_fused<BLOCK>(P, S, b, nullptr);
+}
+
+// External scorer, step 1: per stream, the hypotheses to fuse (flag 1: a
+// fusion frame, top-F; flag 2: end of utterance, all; 0: none).
+template <int BLOCK>
+__global__ __launch_bounds__(BLOCK) void k_fuse_select(const DevParams P, const DevState S,
+                                                       const int32_t* __restrict__ flag) {
+  const int b = blockIdx.x;
+  __shared__ double sc[BLOCK];
+  __shared__ uint64_t ky[BLOCK];
+  __shared__ uint32_t ix[BLOCK];
+  if (flag[b] == 0) {
+    if (threadIdx.x == 0) S.fsel_n[b] = 0;
+    return;
+  }
+  select_fused<BLOCK>(P, S, b, flag[b] == 1 ? P.fusion_top_f : 0, sc, ky, ix);
+}
+
+// External scorer, step 2: word sequences of every sub-beam of the selected
+// hypotheses, words [B][K][O][W] (-1 padded) and n_words [B][K][O] (-1 where
+// nothing is to be scored).
+template <int BLOCK>
+__global__ __launch_bounds__(BLOCK) void k_fuse_export(const DevParams P, const DevState S,
+                                                       int32_t* __restrict__ words, int32_t* __restrict__ n_words) {
+  const int b = blockIdx.x;
+  const size_t gb = static_cast<size_t>(b) * P.K;
+  const int F = S.fsel_n[b];
+  for (int idx = threadIdx.x; idx < P.K * P.O; idx += BLOCK) {
+    const int r = idx / P.O;
+    const int j = idx - r * P.O;
+    const size_t slot = (gb + r) * P.O + j;
+    int32_t* row = words + slot * P.W;
+    int len = -1;
+    if (r < F) {
+      const size_t bi = gb + S.fsel[gb + r];
+      const int nsub = (S.meta[bi] >> 8) & 0xFF;
+      if (j < nsub) {
+        const uint32_t h = S.hist[bi * P.O + j];
+        len = 0;
+        for (uint32_t x = h; x != kRootHist && static_cast<uint64_t>(len) <= S.arena_cap; x = S.arena[x].parent) ++len;
+        if (len > P.W) atomicOr(S.flags, kFlagWords);
+        int k = len - 1;
+        for (uint32_t x = h; x != kRootHist && k >= 0; x = S.arena[x].parent, --k)
+          if (k < P.W) row[k] = S.arena[x].word;
+        for (int k2 = len; k2 < P.W; ++k2) row[k2] = -1;
+        if (len > P.W) len = P.W;
+      }
+    }
+    if (len < 0)
+      for (int k2 = 0; k2 < P.W; ++k2) row[k2] = -1;
+    n_words[slot] = len;
+  }
+}
+
+// External scorer, step 3: apply the caller's scores [B][K][O] to the selection.
+template <int BLOCK>
+__global__ __launch_bounds__(BLOCK) void k_fuse_apply(const DevParams P, const DevState S,
+                                                      const float* __restrict__ scores) {
+  apply_fused<BLOCK>(P, S, blockIdx.x, scores);
 }
 
 // ------------------------------------------------------------------ output
@@ -1042,7 +1113,10 @@ __global__ __launch_bounds__(BLOCK) void k_output(const DevParams P, const DevSt
     S.evq[0] = 0;
     S.evq[1] = 0;
   }
-  if (fin && P.fusion_source == 1 && P.fusion_interval > 0) fuse_stream<BLOCK>(P, S, b, 0, nullptr, sc, ky, ix);
+  if (fin && P.fusion_source == 1 && P.fusion_interval > 0) {
+    select_fused<BLOCK>(P, S, b, 0, sc, ky, ix);
+    apply_fused<BLOCK>(P, S, b, nullptr);
+  }
   const int n = S.nbeam[b];
   const size_t gb = static_cast<size_t>(b) * P.K;
   bool ok = false;
@@ -1142,6 +1216,24 @@ hipError_t launch_lmselect(int grid, const DevParams& P, const DevState& S, int3
 hipError_t launch_fusion(int block, const DevParams& P, const DevState& S, const int32_t* lengths, int32_t B,
                          int32_t tau, hipStream_t st) {
   LB_DISPATCH_BLOCK(block, k_fusion, B, P, S, lengths, tau);
+  return hipGetLastError();
+}
+
+hipError_t launch_fuse_select(int block, const DevParams& P, const DevState& S, const int32_t* flag, int32_t B,
+                              hipStream_t st) {
+  LB_DISPATCH_BLOCK(block, k_fuse_select, B, P, S, flag);
+  return hipGetLastError();
+}
+
+hipError_t launch_fuse_export(int block, const DevParams& P, const DevState& S, int32_t* words, int32_t* n_words,
+                              int32_t B, hipStream_t st) {
+  LB_DISPATCH_BLOCK(block, k_fuse_export, B, P, S, words, n_words);
+  return hipGetLastError();
+}
+
+hipError_t launch_fuse_apply(int block, const DevParams& P, const DevState& S, const float* scores, int32_t B,
+                             hipStream_t st) {
+  LB_DISPATCH_BLOCK(block, k_fuse_apply, B, P, S, scores);
   return hipGetLastError();
 }
 

@@ -17,6 +17,12 @@ hipError_t launch_lmquery(int grid, const DevParams& P, const DevState& S, int32
 hipError_t launch_lmselect(int grid, const DevParams& P, const DevState& S, int32_t tau, hipStream_t st);
 hipError_t launch_fusion(int block, const DevParams& P, const DevState& S, const int32_t* lengths, int32_t B,
                          int32_t tau, hipStream_t st);
+hipError_t launch_fuse_select(int block, const DevParams& P, const DevState& S, const int32_t* flag, int32_t B,
+                              hipStream_t st);
+hipError_t launch_fuse_export(int block, const DevParams& P, const DevState& S, int32_t* words, int32_t* n_words,
+                              int32_t B, hipStream_t st);
+hipError_t launch_fuse_apply(int block, const DevParams& P, const DevState& S, const float* scores, int32_t B,
+                             hipStream_t st);
 hipError_t launch_output(int block, const DevParams& P, const DevState& S, const int32_t* lengths, int32_t B,
                          int32_t fin, int32_t* out_hyps, float* out_scores, hipStream_t st);
 

@@ -119,3 +119,96 @@ def test_zero_length_and_tiny_lexicon():
     out = gpu_decode(d, params=p)
     assert out[1][0] == [[]] and out[1][1].tolist() == [0.0]
     check_parity(d, out, range(3), params=p, name="tiny")
+
+
+@pytest.mark.parametrize("sigma", [0.0, 1e-3], ids=["exact-ties", "clustered"])
+def test_crowded_boundary_bins(sigma):
+    """Uniform (or nearly uniform) log-probs make thousands of candidates share
+    the boundary score bin: exact ties are ordered by key bits, clustered
+    scores by refined score bins; both must match the oracle."""
+    base = load_workload("t-k256")
+    rng = np.random.default_rng(11)
+    B, T = 2, 7
+    raw = sigma * rng.standard_normal((B, T, 41))
+    lg = (raw - np.log(np.exp(raw).sum(-1, keepdims=True))).astype(np.float32)
+    p = DecodeParams(beam=256, subbeams=3, fusion_interval=3, fusion_top_f=0)
+    wl = base.workload.__class__(**{**base.workload.__dict__, "params": p})
+    d = WorkloadData(wl, base.lexicon, base.lm, lg, np.full(B, T, np.int32), np.zeros((B, T), np.int32),
+                     [[], []], base.fusion_seed)
+    say(f"[case] crowded bins sigma={sigma}")
+    for fin in (False, True):
+        out = gpu_decode(d, params=p, finalize=fin)
+        par = check_parity(d, out, range(B), params=p, name=f"crowded/{sigma}", finalize=fin)
+        if not fin:
+            assert par.n_hyps == B * 256
+
+
+@pytest.mark.parametrize("name", ["t-c20k", "t-c125k"])
+def test_external_fusion_round_trip(name):
+    """LB_FUSION_EXTERNAL: the decoder stops at every fusion event, exports the
+    word sequences of the fused sub-beams, and applies the caller's scores.
+    Scoring them with the synthetic scorer must reproduce the oracle's
+    synthetic-fusion decode exactly (final and live outputs)."""
+    import torch
+    import oracle
+    d = load_workload(name)
+    p = d.workload.params
+    B, T = d.logits.shape[:2]
+    orc = oracle_for(d)
+    op = oracle.params_from(p, fusion_seed=d.fusion_seed)
+    dev = torch.device("cuda:0")
+    for fin in (True, False):
+        lp = lbm.make_params(p, max_batch=B, max_frames=T, fusion_seed=d.fusion_seed,
+                             fusion_source=lbm.LB_FUSION_EXTERNAL)
+        dec = lbm.Decoder(d.lexicon, d.lm, lp)
+        K, O, W = lp.beam, lp.subbeams, lp.max_words_out
+        logits = torch.from_numpy(d.logits).to(dev)
+        lengths = torch.from_numpy(d.lengths).to(dev)
+        hyps = torch.empty((B, K, W), dtype=torch.int32, device=dev)
+        scores = torch.empty((B, K), dtype=torch.float32, device=dev)
+        words = torch.empty((B, K, O, W), dtype=torch.int32, device=dev)
+        nw = torch.empty((B, K, O), dtype=torch.int32, device=dev)
+        flags = lbm.LB_BEGIN | (lbm.LB_END if fin else 0)
+        with pytest.raises(lbm.LBError) as e:  # nothing pending yet
+            lbm.lb_fusion_request(dec.handle, words, nw, None)
+        assert e.value.status == lbm.LB_ERR_STATE
+        events = 0
+        while True:
+            st, _, _ = dec.decode(logits, lengths, flags, out_hyps=hyps, out_scores=scores)
+            if st == lbm.LB_OK:
+                break
+            assert st == lbm.LB_NEED_FUSION
+            if events == 0:
+                # resuming before the scores arrive, or with other arguments, is refused
+                with pytest.raises(lbm.LBError) as e:
+                    dec.decode(logits, lengths, flags, out_hyps=hyps, out_scores=scores)
+                assert e.value.status == lbm.LB_ERR_STATE
+            events += 1
+            lbm.lb_fusion_request(dec.handle, words, nw, None)
+            torch.cuda.synchronize()
+            Wh, Nh = words.cpu().numpy(), nw.cpu().numpy()
+            fs = np.zeros((B, K, O), np.float32)
+            for b, r, j in zip(*np.nonzero(Nh >= 0)):
+                s = orc.fusion_score(op, [int(x) for x in Wh[b, r, j, :Nh[b, r, j]]])
+                assert float(np.float32(s)) == s  # the score travels exactly in float32
+                fs[b, r, j] = s
+            lbm.lb_fusion_scores(dec.handle, torch.from_numpy(fs).to(dev), None)
+        torch.cuda.synchronize()
+        assert dec.status() == lbm.LB_OK
+        # one event per fusion frame reached by some stream, plus the final one
+        expect = len({t for L in d.lengths for t in range(p.fusion_interval, int(L), p.fusion_interval)})
+        assert events == expect + (1 if fin else 0), (events, expect)
+        H, S = hyps.cpu().numpy(), scores.cpu().numpy()
+        out = []
+        for b in range(B):
+            ws, sc = [], []
+            for r in range(K):
+                if not np.isfinite(S[b, r]):
+                    break
+                row = H[b, r]
+                ws.append([int(x) for x in row[row >= 0]])
+                sc.append(S[b, r])
+            out.append((ws, np.array(sc, np.float32)))
+        say(f"[case] external fusion {name} finalize={fin}: {events} events")
+        check_parity(d, out, range(B), orc=orc, name=f"external/{name}", finalize=fin)
+        dec.close()
