@@ -188,8 +188,12 @@ lb_status lb_get_status(lb_decoder* dec, void* stream);
 lb_status lb_get_stats(lb_decoder* dec, lb_stats* out);
 lb_status lb_reset_stats(lb_decoder* dec);
 
-/* Enables (1) or disables (0) HIP-event timing around every kernel launch. */
-lb_status lb_set_profiling(lb_decoder* dec, int32_t enable);
+/* HIP-event timing around kernel launches: bit k of kernel_mask times the
+ * kernels of kind k (the index of lb_stats.launches); 0 disables timing and
+ * LB_PROFILE_ALL times every launch.  The events add a few microseconds per
+ * timed launch to the stream. */
+enum { LB_PROFILE_ALL = 0xFFu };
+lb_status lb_set_profiling(lb_decoder* dec, uint32_t kernel_mask);
 
 /* Thread-local description of the last error ("" if none). */
 const char* lb_last_error(void);

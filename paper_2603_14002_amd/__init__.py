@@ -99,7 +99,7 @@ def lib():
         L.lb_reset_stats.restype = ctypes.c_int32
         L.lb_reset_stats.argtypes = [P]
         L.lb_set_profiling.restype = ctypes.c_int32
-        L.lb_set_profiling.argtypes = [P, ctypes.c_int32]
+        L.lb_set_profiling.argtypes = [P, ctypes.c_uint32]
         L.lb_last_error.restype = ctypes.c_char_p
         L.lb_last_error.argtypes = []
         _lib = L
@@ -180,8 +180,13 @@ def lb_reset_stats(dec: int) -> None:
     _check(lib().lb_reset_stats(dec))
 
 
-def lb_set_profiling(dec: int, enable: bool) -> None:
-    _check(lib().lb_set_profiling(dec, 1 if enable else 0))
+KIND_FRAME, KIND_LMQUERY, KIND_LMSELECT, KIND_FUSION, KIND_OUTPUT = 0, 1, 2, 3, 4
+LB_PROFILE_ALL = 0xFF
+
+
+def lb_set_profiling(dec: int, kernel_mask: int) -> None:
+    """bit k times kernel kind k with HIP events (0 = off, LB_PROFILE_ALL = all)."""
+    _check(lib().lb_set_profiling(dec, int(kernel_mask) & 0xFFFFFFFF))
 
 
 # ------------------------------------------------------------------ descriptor marshalling

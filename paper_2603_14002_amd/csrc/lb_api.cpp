@@ -133,7 +133,7 @@ struct lb_decoder {
   int lms_grid = 1;     // workgroups of the homophone selection kernel
   std::vector<void*> allocs;
   int64_t launches[kKinds] = {};
-  bool profiling = false;
+  uint32_t profile_mask = 0;  // kernel kinds timed with HIP events (bit k = kind k)
   std::vector<EventPair> pending;
   std::vector<hipEvent_t> pool;
   double kernel_ms[kKinds] = {};
@@ -385,6 +385,7 @@ lb_status lb_create(const lb_lexicon_desc* lex, const lb_ngram_desc* lm, const l
   const size_t BK = static_cast<size_t>(B) * K;
   if ((st = d->alloc(&S.key, BK)) != LB_OK || (st = d->alloc(&S.pkey, BK)) != LB_OK ||
       (st = d->alloc(&S.ab, BK)) != LB_OK || (st = d->alloc(&S.anb, BK)) != LB_OK ||
+      (st = d->alloc(&S.pt, BK)) != LB_OK ||
       (st = d->alloc(&S.node, BK)) != LB_OK || (st = d->alloc(&S.meta, BK)) != LB_OK ||
       (st = d->alloc(&S.Lw, BK * O)) != LB_OK || (st = d->alloc(&S.hist, BK * O)) != LB_OK ||
       (st = d->alloc(&S.nbeam, B)) != LB_OK || (st = d->alloc(&S.t0, B)) != LB_OK ||
@@ -464,9 +465,10 @@ lb_status lb_decode_batch(lb_decoder* d, const float* logits, const int32_t* len
   const bool external = P.fusion_source == LB_FUSION_EXTERNAL;
   EventPair ep{};
   auto launch = [&](int kind, auto&& fn) -> hipError_t {
-    if (d->profiling) record_start(d, st, &ep, kind);
+    const bool timed = (d->profile_mask >> kind) & 1u;
+    if (timed) record_start(d, st, &ep, kind);
     const hipError_t e = fn();
-    if (d->profiling) record_stop(d, st, &ep);
+    if (timed) record_stop(d, st, &ep);
     d->launches[kind]++;
     return e;
   };
@@ -618,9 +620,9 @@ lb_status lb_reset_stats(lb_decoder* d) {
   return LB_OK;
 }
 
-lb_status lb_set_profiling(lb_decoder* d, int32_t enable) {
+lb_status lb_set_profiling(lb_decoder* d, uint32_t kernel_mask) {
   if (!d) return fail(LB_ERR_INVALID_ARG, "decoder is null");
-  d->profiling = enable != 0;
+  d->profile_mask = kernel_mask;
   return LB_OK;
 }
 

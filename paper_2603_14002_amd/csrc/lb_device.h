@@ -122,6 +122,7 @@ struct DevState {
   uint64_t* pkey;
   double* ab;
   double* anb;
+  double* pt;  // log-sum-exp(ab, anb)
   uint32_t* node;
   uint32_t* meta;  // last symbol (bits 0..7) | number of sub-beams (bits 8..15)
   double* Lw;

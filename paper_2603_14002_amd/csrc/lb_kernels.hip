@@ -27,9 +27,6 @@ constexpr double kNegInf = -HUGE_VAL;
 constexpr int kBins = 1024;         // score bins of the top-K selection
 constexpr int kBoundaryCap = 256;   // candidates resolved exactly inside the boundary bin
 constexpr int kMaxLevels = 16;      // refinement levels of the top-K selection
-#ifndef LB_CACHE_SCORES
-#define LB_CACHE_SCORES 1
-#endif
 #ifndef LB_CAND_UNROLL
 #define LB_CAND_UNROLL 64
 #endif
@@ -254,6 +251,7 @@ __global__ void k_begin(DevParams P, DevState S, int32_t B) {
   S.pkey[i] = kNoParent;
   S.ab[i] = 0.0;
   S.anb[i] = kNegInf;
+  S.pt[i] = lse2(0.0, kNegInf);
   S.node[i] = kRootNode;
   S.meta[i] = 1u << 8;  // no last symbol, one sub-beam
   S.Lw[i * P.O] = 0.0;
@@ -283,7 +281,7 @@ __global__ __launch_bounds__(KMAX * LPB) void k_frame(const DevParams P, const D
 
   __shared__ double sD[kClasses];
   __shared__ uint64_t sKey[KMAX], sPkey[KMAX];
-  __shared__ double sAb[KMAX], sP[KMAX], sL[KMAX], sAb2[KMAX], sAnb2[KMAX], sStay[KMAX];
+  __shared__ double sAb[KMAX], sP[KMAX], sL[KMAX], sAb2[KMAX], sAnb2[KMAX], sPt2[KMAX], sStay[KMAX];
   __shared__ uint32_t sNode[KMAX], sMeta[KMAX], sFirst[KMAX], sWoff[KMAX], sNwords[KMAX];
   __shared__ uint64_t sMask[KMAX], sTrieMask[KMAX];
   __shared__ double sLw[KMAX * kMaxSub];
@@ -323,7 +321,7 @@ __global__ __launch_bounds__(KMAX * LPB) void k_frame(const DevParams P, const D
     sKey[tid] = my_key;
     sPkey[tid] = my_pkey;
     sAb[tid] = ab;
-    sP[tid] = lse2(ab, my_anb);
+    sP[tid] = S.pt[gb + tid];  // log-sum-exp(ab, anb), kept with the hypothesis
     sNode[tid] = node;
     sMeta[tid] = my_meta;
     const int nsub = (my_meta >> 8) & 0xFF;
@@ -384,9 +382,11 @@ __global__ __launch_bounds__(KMAX * LPB) void k_frame(const DevParams P, const D
       ext = (base + sD[last]) + (last == kSep ? P.gamma : P.beta);
     }
     const double anb2 = lse2(rep, ext);
+    const double pt2 = lse2(ab2, anb2);
     sAb2[tid] = ab2;
     sAnb2[tid] = anb2;
-    sStay[tid] = lse2(ab2, anb2) + sL[tid];
+    sPt2[tid] = pt2;
+    sStay[tid] = pt2 + sL[tid];
   }
   __syncthreads();
 
@@ -414,14 +414,7 @@ __global__ __launch_bounds__(KMAX * LPB) void k_frame(const DevParams P, const D
     const double base = (v == c_last) ? c_ab : c_p;
     return ((base + sD[v]) + (v == kSep ? P.gamma : P.beta)) + c_L;
   };
-#if LB_CACHE_SCORES
-  double sc[NC];
-#pragma unroll
-  for (int k = 0; k < NC; ++k) sc[k] = score_now(k);
-  auto score_of = [&](int k) -> double { return sc[k]; };
-#else
   auto score_of = score_now;
-#endif
   auto key_of = [&](int v) -> uint64_t { return v == 0 ? c_key : prefix_step(c_key, v); };
   // f(v, score) for each of this lane's candidates with a finite score
   auto for_cands = [&](auto&& f) {
@@ -509,11 +502,29 @@ __global__ __launch_bounds__(KMAX * LPB) void k_frame(const DevParams P, const D
     return tot;
   };
 
+  // level-0 bin of each of the lane's candidates, kept packed 16 bits per slot
+  // (0xFFFF: no candidate); exact scores are recomputed only inside the boundary bin
+  uint32_t binp[(NC + 1) / 2];
+  uint32_t bin_stay = 0xFFFFu;
   for (int d = tid; d < kBins; d += BLOCK) sHisto[d] = 0;
   __syncthreads();
-  for_cands([&](int v, double s) {
-    if (s >= thr) atomicAdd(&sHisto[bin0(v, s)], 1u);
-  });
+  if (c_stay != kNegInf && c_stay >= thr) {
+    bin_stay = static_cast<uint32_t>(bin0(0, c_stay));
+    atomicAdd(&sHisto[bin_stay], 1u);
+  }
+#pragma unroll
+  for (int k = 0; k < NC; ++k) {
+    const double s = score_now(k);
+    uint32_t bn = 0xFFFFu;
+    if (s != kNegInf && s >= thr) {
+      bn = static_cast<uint32_t>(bin0(1 + ln + LPB * k, s));
+      atomicAdd(&sHisto[bn], 1u);
+    }
+    if (k & 1)
+      binp[k >> 1] |= bn << 16;
+    else
+      binp[k >> 1] = bn;
+  }
   __syncthreads();
   const int nvalid = find_bin(P.K);
   const bool select_all = nvalid <= P.K;
@@ -582,11 +593,13 @@ __global__ __launch_bounds__(KMAX * LPB) void k_frame(const DevParams P, const D
       if (sBCount > kBoundaryCap && tid == 0) atomicOr(S.flags, kFlagSelect);
     }
   }
-  auto selected = [&](int v, double s) -> bool {
-    if (s < thr) return false;
+  // selection of a candidate from its level-0 bin; the exact score (score_fn)
+  // is needed only inside the boundary bin
+  auto selected = [&](uint32_t bn, int v, auto&& score_fn) -> bool {
+    if (bn == 0xFFFFu) return false;
     if (select_all) return true;
-    const int bn = bin0(v, s);
-    if (bn != beta0) return bn < beta0;
+    if (static_cast<int>(bn) != beta0) return static_cast<int>(bn) < beta0;
+    const double s = score_fn();
     for (int l = 1; l < nlev; ++l) {
       const int bl = bin_at(l, v, s);
       if (bl != sLvBeta[l]) return bl < sLvBeta[l];
@@ -602,11 +615,11 @@ __global__ __launch_bounds__(KMAX * LPB) void k_frame(const DevParams P, const D
   // ---- selection bits (bit 0: the stay, bit k+1: slot k), then a
   // deterministic gather of the sources in lane order
   uint64_t sel_bits = 0;
-  if (c_stay != kNegInf && selected(0, c_stay)) sel_bits |= 1ull;
-#pragma unroll LB_CAND_UNROLL
+  if (selected(bin_stay, 0, [&] { return c_stay; })) sel_bits |= 1ull;
+#pragma unroll
   for (int k = 0; k < NC; ++k) {
-    const double s = score_of(k);
-    if (s != kNegInf && selected(1 + ln + LPB * k, s)) sel_bits |= 2ull << k;
+    const uint32_t bn = (binp[k >> 1] >> ((k & 1) * 16)) & 0xFFFFu;
+    if (selected(bn, 1 + ln + LPB * k, [&] { return score_now(k); })) sel_bits |= 2ull << k;
   }
   int nsel = 0;
   int wpos = block_scan<BLOCK>(__popcll(sel_bits), sScan, &nsel);
@@ -637,15 +650,18 @@ __global__ __launch_bounds__(KMAX * LPB) void k_frame(const DevParams P, const D
       S.pkey[o] = sPkey[i];
       S.ab[o] = sAb2[i];
       S.anb[o] = sAnb2[i];
+      S.pt[o] = sPt2[i];
       S.node[o] = sNode[i];
       S.meta[o] = meta_i;
     } else {
       const int last = meta_i & 0xFF;
       const double base = (v == last) ? sAb[i] : sP[i];
+      const double anb = (base + sD[v]) + (v == kSep ? P.gamma : P.beta);
       S.key[o] = prefix_step(sKey[i], v);
       S.pkey[o] = sKey[i];
       S.ab[o] = kNegInf;
-      S.anb[o] = (base + sD[v]) + (v == kSep ? P.gamma : P.beta);
+      S.anb[o] = anb;
+      S.pt[o] = lse2(kNegInf, anb);
       uint32_t child = kRootNode;
       if (v != kSep) child = sFirst[i] + __popcll(sTrieMask[i] & ((1ull << v) - 1ull));
       S.node[o] = child;
@@ -850,9 +866,7 @@ __global__ __launch_bounds__(256) void k_lmselect(const DevParams P, const DevSt
       tL[k] = kNegInf;
       tq[k] = 0x7FFFFFFF;
     }
-    for (int q = lane; q < nq; q += 64) {
-      double L = S.qL[ev.qoff + q];
-      int qq = q;
+    auto insert = [&](double L, int qq) {
 #pragma unroll
       for (int k = 0; k < kMaxSub; ++k) {
         if (k < P.O && (L > tL[k] || (L == tL[k] && qq < tq[k]))) {
@@ -864,7 +878,18 @@ __global__ __launch_bounds__(256) void k_lmselect(const DevParams P, const DevSt
           qq = u;
         }
       }
+    };
+    // four independent loads in flight per lane, then the insertions
+    const double* ql = S.qL + ev.qoff;
+    int q = lane;
+    for (; q + 192 < nq; q += 256) {
+      const double a0 = ql[q], a1 = ql[q + 64], a2 = ql[q + 128], a3 = ql[q + 192];
+      insert(a0, q);
+      insert(a1, q + 64);
+      insert(a2, q + 128);
+      insert(a3, q + 192);
     }
+    for (; q < nq; q += 64) insert(ql[q], q);
     uint32_t abase = 0;
     if (lane == 0) abase = atomicAdd(&S.arena_n[ev.stream], static_cast<uint32_t>(P.O));
     abase = __shfl(abase, 0, 64);
@@ -951,7 +976,7 @@ __device__ void select_fused(const DevParams& P, const DevState& S, int b, int t
   const int F = (top_f <= 0 || top_f >= n) ? n : top_f;
   if (F < n) {
     if (tid < n) {
-      sc[tid] = lse2(S.ab[gb + tid], S.anb[gb + tid]) + S.Lw[(gb + tid) * P.O];
+      sc[tid] = S.pt[gb + tid] + S.Lw[(gb + tid) * P.O];
       ky[tid] = S.key[gb + tid];
       ix[tid] = tid;
     } else {
@@ -1122,7 +1147,7 @@ __global__ __launch_bounds__(BLOCK) void k_output(const DevParams P, const DevSt
   bool ok = false;
   if (tid < n) {
     ok = !fin || S.node[gb + tid] == kRootNode;
-    sc[tid] = ok ? lse2(S.ab[gb + tid], S.anb[gb + tid]) + S.Lw[(gb + tid) * P.O] : kNegInf;
+    sc[tid] = ok ? S.pt[gb + tid] + S.Lw[(gb + tid) * P.O] : kNegInf;
     ky[tid] = ok ? S.key[gb + tid] : ~0ull;
     ix[tid] = tid;
   } else {

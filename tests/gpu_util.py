@@ -40,7 +40,7 @@ def gpu_decode(d, params=None, chunk: int = 0, batch: Optional[int] = None, fusi
         lp.max_words_out = max_words
     dec = lbm.Decoder(d.lexicon, d.lm, lp)
     if profiling:
-        lbm.lb_set_profiling(dec.handle, True)
+        lbm.lb_set_profiling(dec.handle, lbm.LB_PROFILE_ALL)
     dev = torch.device("cuda:0")
     logits = torch.from_numpy(np.ascontiguousarray(d.logits[:B])).to(dev)
     lengths = np.ascontiguousarray(d.lengths[:B]).astype(np.int32)
