@@ -27,7 +27,6 @@ sys.path.insert(0, ROOT)
 METRIC = "beam-token expansions/sec and decoded audio-sec per wall-sec (RTF) on 1 MI355X"
 HBM_PEAK_GBS = 8000.0
 LINE_BYTES = 64          # one hash-table bucket = one 64-B line
-KERNELS = ("frame", "lmquery", "lmselect", "fusion", "output")
 
 
 def log(msg):
@@ -37,7 +36,7 @@ def log(msg):
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="c4")
     ap.add_argument("--cpu-sample", type=int, default=0,
@@ -67,6 +66,27 @@ def copy_calibration(mib: int) -> None:
     ms = ev0.elapsed_time(ev1)
     print(json.dumps({"copy_calibration_mib": mib, "bytes_read": n * 4, "bytes_written": n * 4,
                       "ms": ms, "GBps_read_plus_write": 2 * n * 4 / (ms * 1e-3) / 1e9}), flush=True)
+
+
+def algorithmic_bytes(s, B, T, p, lp):
+    """Bytes the method itself moves in the counted work (all launches of the
+    pass): the logits once, a 16-B trie node per 41 expansions, the beam state
+    read and written once per call, per n-gram query the probed 64-B bucket
+    lines plus the unigram entry (8 B), the word id (4 B) and the parent's
+    32-B history node, and a 32-B history node written per kept word (at most
+    o per completed word)."""
+    state = 48 + 12 * p.subbeams          # key, pkey, a_b, a_nb, total, node, meta + o x (L, hist)
+    calls = max(1, int(s.launches[0]))
+    parts = {
+        "logits": float(s.frames) * 164.0,
+        "trie": float(s.expansions) * 16.0 / 41.0,
+        "state": 2.0 * calls * B * p.beam * state,
+        "ngram_lines": float(s.probe_lines) * LINE_BYTES,
+        "ngram_other": float(s.lm_queries) * (8 + 4 + 32),
+        "history_nodes": float(s.word_events) * p.subbeams * 32.0,
+    }
+    parts["total"] = sum(parts.values())
+    return parts
 
 
 def cpu_baseline(d, n_utts: int, threads: int):
@@ -187,27 +207,26 @@ def main():
     roof = None
     kern = {}
     if not args.no_profile:
-        # (2) the same K steps with HIP events around every k_lmquery launch only:
-        # the duration of the lookup phase for its roofline
-        wall_q, sq = timed_pass(1 << lbm.KIND_LMQUERY)
-        i = lbm.KIND_LMQUERY
-        avg_us = 1000.0 * sq.kernel_ms[i] / max(1, sq.timed[i])
-        # every probed 64-B bucket line is one random read of the n-gram tables
-        per_launch_bytes = sq.probe_lines * LINE_BYTES / max(1, sq.launches[i])
-        achieved = per_launch_bytes / (avg_us * 1e-6) / 1e9
-        roof = dict(kernel="k_lmquery", bound="hbm", achieved=achieved, peak=HBM_PEAK_GBS, unit="GB/s",
-                    frac=achieved / HBM_PEAK_GBS, traffic=None, bytes_per_launch=per_launch_bytes,
-                    avg_launch_us=avg_us, launches=int(sq.launches[i]),
-                    timing="HIP events around each k_lmquery launch, a second pass of the same steps",
-                    wall_ms_per_step_in_that_pass=wall_q / args.steps)
-        # (3) every kernel timed: the breakdown of a step
-        _, sa = timed_pass(lbm.LB_PROFILE_ALL)
-        for k, name in enumerate(KERNELS):
-            if sa.timed[k]:
-                kern[name] = dict(launches=int(sa.launches[k]), total_ms=sa.kernel_ms[k],
-                                  avg_us=1000.0 * sa.kernel_ms[k] / sa.timed[k])
+        # (2) the same K steps with every kernel timed by events carried in its
+        # own dispatch: k_decode's duration for the roofline, and the breakdown
+        wall_p, sp = timed_pass(lbm.LB_PROFILE_ALL)
+        for k, name in enumerate(lbm.KIND_NAMES):
+            if sp.timed[k]:
+                kern[name] = dict(launches=int(sp.launches[k]), total_ms=sp.kernel_ms[k],
+                                  avg_us=1000.0 * sp.kernel_ms[k] / sp.timed[k])
         if kern:
             kern["dominant"] = max(kern, key=lambda k: kern[k]["total_ms"])
+        i = lbm.KIND_DECODE
+        nl = max(1, int(sp.launches[i]))
+        avg_us = 1000.0 * sp.kernel_ms[i] / max(1, sp.timed[i])
+        alg = {k: v / nl for k, v in algorithmic_bytes(sp, B, T, p, lp).items()}
+        roof = dict(kernel="k_decode", bound="hbm", achieved=alg["total"] / (avg_us * 1e-6) / 1e9,
+                    peak=HBM_PEAK_GBS, unit="GB/s", frac=None, traffic=None,
+                    bytes_per_launch=alg, avg_launch_us=avg_us, launches=nl,
+                    timing="start/stop events carried by each k_decode dispatch (hipExtLaunchKernel), "
+                           "a second pass of the same steps",
+                    wall_ms_per_step_in_that_pass=wall_p / args.steps)
+        roof["frac"] = roof["achieved"] / HBM_PEAK_GBS
     out = {
         "metric": METRIC,
         "value": value,

@@ -120,8 +120,9 @@ typedef struct lb_stats {
   int64_t fused;        /* hypotheses rescored by delayed fusion                  */
   int64_t frames;       /* stream-frames decoded                                  */
   int64_t probe_lines;  /* 64-B n-gram hash-table lines read by the LM lookups    */
-  int64_t launches[8];  /* kernel launches: [0] frame step, [1] LM query, [2] homophone
-                           selection, [3] delayed fusion, [4] output, [5..7] unused  */
+  int64_t launches[8];  /* kernel launches: [0] decode (all frames of a call), [1]
+                           output, [2] external-fusion select, [3] export, [4]
+                           apply, [5] stream reset, [6..7] unused                */
   double  kernel_ms[8]; /* summed event-timed durations (when profiling is on)    */
   int64_t timed[8];     /* launches included in kernel_ms                         */
 } lb_stats;
@@ -179,8 +180,8 @@ lb_status lb_fusion_request(lb_decoder* dec, int32_t* words, int32_t* n_words, v
 lb_status lb_fusion_scores(lb_decoder* dec, const float* fusion_logprobs, void* stream);
 
 /* Synchronises `stream` and reports device-side overflow flags: LB_ERR_CAPACITY
- * if a word-history arena, an output buffer (words beyond max_words_out) or an
- * internal queue overflowed since lb_create. */
+ * if a word-history arena, an output buffer (words beyond max_words_out) or the
+ * top-K selection's boundary buffer overflowed since lb_create. */
 lb_status lb_get_status(lb_decoder* dec, void* stream);
 
 /* Reads the counters (synchronises the device).  With profiling on (see
@@ -188,10 +189,11 @@ lb_status lb_get_status(lb_decoder* dec, void* stream);
 lb_status lb_get_stats(lb_decoder* dec, lb_stats* out);
 lb_status lb_reset_stats(lb_decoder* dec);
 
-/* HIP-event timing around kernel launches: bit k of kernel_mask times the
- * kernels of kind k (the index of lb_stats.launches); 0 disables timing and
- * LB_PROFILE_ALL times every launch.  The events add a few microseconds per
- * timed launch to the stream. */
+/* Kernel timing with HIP events: bit k of kernel_mask times the kernels of
+ * kind k (the index of lb_stats.launches); 0 disables timing and
+ * LB_PROFILE_ALL times every launch.  The start / stop events are carried by
+ * the kernel's own dispatch (hipExtLaunchKernel), so they time its execution
+ * only. */
 enum { LB_PROFILE_ALL = 0xFFu };
 lb_status lb_set_profiling(lb_decoder* dec, uint32_t kernel_mask);
 

@@ -180,7 +180,9 @@ def lb_reset_stats(dec: int) -> None:
     _check(lib().lb_reset_stats(dec))
 
 
-KIND_FRAME, KIND_LMQUERY, KIND_LMSELECT, KIND_FUSION, KIND_OUTPUT = 0, 1, 2, 3, 4
+# kernel kinds (index of lb_stats.launches / kernel_ms)
+KIND_DECODE, KIND_OUTPUT, KIND_FUSE_SELECT, KIND_FUSE_EXPORT, KIND_FUSE_APPLY, KIND_BEGIN = 0, 1, 2, 3, 4, 5
+KIND_NAMES = ("decode", "output", "fuse_select", "fuse_export", "fuse_apply", "begin")
 LB_PROFILE_ALL = 0xFF
 
 

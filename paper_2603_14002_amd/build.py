@@ -14,6 +14,9 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "liblightbeam.so")
 SOURCES = ["lb_kernels.hip", "lb_api.cpp"]
+# k_decode loops over frames: machine-level hoisting of loop-invariant values
+# out of that loop keeps them live across it and makes the kernel spill
+EXTRA = {"lb_kernels.hip": ["-mllvm", "-disable-machine-licm"]}
 ARCH = os.environ.get("LB_OFFLOAD_ARCH", "gfx950")
 
 COMMON = [
@@ -37,7 +40,7 @@ def build(verbose: bool = False) -> str:
         objs = []
         for src in SOURCES:
             obj = os.path.join(tmp, os.path.splitext(src)[0] + ".o")
-            cmd = [cc, *COMMON, "-c", os.path.join(CSRC, src), "-o", obj]
+            cmd = [cc, *COMMON, *EXTRA.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj]
             if verbose:
                 print(" ".join(cmd), flush=True)
             r = subprocess.run(cmd, capture_output=True, text=True)

@@ -120,7 +120,8 @@ struct EventPair {
 };
 
 // kernel kinds of lb_stats.launches / kernel_ms
-enum { kKindFrame = 0, kKindLmQuery = 1, kKindLmSelect = 2, kKindFusion = 3, kKindOutput = 4, kKinds = 8 };
+enum { kKindDecode = 0, kKindOutput = 1, kKindFuseSelect = 2, kKindFuseExport = 3, kKindFuseApply = 4, kKindBegin = 5,
+       kKinds = 8 };
 
 }  // namespace
 
@@ -129,8 +130,6 @@ struct lb_decoder {
   DevParams P{};
   DevState S{};
   int block = 64;       // workgroup size of the fusion / output kernels (>= beam)
-  int lmq_grid = 1;     // workgroups of the LM query kernel
-  int lms_grid = 1;     // workgroups of the homophone selection kernel
   std::vector<void*> allocs;
   int64_t launches[kKinds] = {};
   uint32_t profile_mask = 0;  // kernel kinds timed with HIP events (bit k = kind k)
@@ -329,18 +328,28 @@ lb_status build_tables(lb_decoder* d, const HostTrie& trie, const lb_ngram_desc*
   return LB_OK;
 }
 
-void record_start(lb_decoder* d, hipStream_t st, EventPair* ep, int kind) {
+void record_start(lb_decoder* d, EventPair* ep, int kind) {
   ep->kind = kind;
   ep->a = d->get_event();
   ep->b = d->get_event();
-  if (ep->a) (void)hipEventRecord(ep->a, st);
+  if (ep->a && ep->b) set_launch_events(ep->a, ep->b);
 }
 
-void record_stop(lb_decoder* d, hipStream_t st, EventPair* ep) {
-  if (ep->a && ep->b) {
-    (void)hipEventRecord(ep->b, st);
-    d->pending.push_back(*ep);
-  }
+void record_stop(lb_decoder* d, EventPair* ep) {
+  set_launch_events(nullptr, nullptr);
+  if (ep->a && ep->b) d->pending.push_back(*ep);
+}
+
+// Launches through fn(); with kind's bit in the profiling mask the launch
+// carries start / stop events.
+template <typename F>
+hipError_t timed_launch(lb_decoder* d, EventPair* ep, int kind, F&& fn) {
+  const bool timed = (d->profile_mask >> kind) & 1u;
+  if (timed) record_start(d, ep, kind);
+  const hipError_t e = fn();
+  if (timed) record_stop(d, ep);
+  d->launches[kind]++;
+  return e;
 }
 
 }  // namespace
@@ -376,10 +385,14 @@ lb_status lb_create(const lb_lexicon_desc* lex, const lb_ngram_desc* lm, const l
     delete d;
     return fail(LB_ERR_INVALID_ARG, "more than 65535 words share one phoneme spelling");
   }
-  const uint64_t qcap = static_cast<uint64_t>(B) * K * O * std::max<uint32_t>(1, trie.max_homophones);
-  if (qcap >= 0xFFFFFFFFull) {
+  const uint64_t scap = static_cast<uint64_t>(K) * O * std::max<uint32_t>(1, trie.max_homophones);
+  if (scap >= 0x7FFFFFFFull) {
     delete d;
-    return fail(LB_ERR_CAPACITY, "per-frame n-gram query bound exceeds 32 bits; lower max_batch or beam");
+    return fail(LB_ERR_CAPACITY, "per-frame n-gram query bound exceeds 31 bits; lower beam or subbeams");
+  }
+  if (trie.words.size() >= (1ull << 30)) {
+    delete d;
+    return fail(LB_ERR_INVALID_ARG, "lexicon too large (2^30 words)");
   }
   DevState& S = d->S;
   const size_t BK = static_cast<size_t>(B) * K;
@@ -390,19 +403,17 @@ lb_status lb_create(const lb_lexicon_desc* lex, const lb_ngram_desc* lm, const l
       (st = d->alloc(&S.Lw, BK * O)) != LB_OK || (st = d->alloc(&S.hist, BK * O)) != LB_OK ||
       (st = d->alloc(&S.nbeam, B)) != LB_OK || (st = d->alloc(&S.t0, B)) != LB_OK ||
       (st = d->alloc(&S.arena_n, B)) != LB_OK || (st = d->alloc(&S.arena, 1 + cap * B)) != LB_OK ||
-      (st = d->alloc(&S.events, BK)) != LB_OK || (st = d->alloc(&S.evq, 2)) != LB_OK ||
-      (st = d->alloc(&S.qmap, qcap)) != LB_OK || (st = d->alloc(&S.qL, qcap)) != LB_OK ||
-      (st = d->alloc(&S.qS, qcap)) != LB_OK ||
+      (st = d->alloc(&S.scrL, static_cast<size_t>(B) * scap)) != LB_OK ||
+      (st = d->alloc(&S.scrS, static_cast<size_t>(B) * scap)) != LB_OK ||
       (st = d->alloc(&S.flags, 1)) != LB_OK || (st = d->alloc(&S.counters, static_cast<size_t>(B) * kNumCounters)) != LB_OK ||
       (st = d->alloc(&S.fsel, BK)) != LB_OK || (st = d->alloc(&S.fsel_n, B)) != LB_OK ||
-      (st = d->alloc(&S.lines, static_cast<size_t>(kSpread) * kSpreadStride)) != LB_OK ||
       (st = d->alloc(&d->ext.d_flag, B)) != LB_OK) {
     std::string msg = g_err;
     delete d;
     return fail(st, msg);
   }
   S.arena_cap = cap;
-  S.qcap = qcap;
+  S.scap = scap;
   d->ext.t0.assign(B, 0);
   d->ext.len.assign(B, 0);
   d->ext.flag.assign(B, 0);
@@ -410,10 +421,8 @@ lb_status lb_create(const lb_lexicon_desc* lex, const lb_ngram_desc* lm, const l
     LB_HIP(hipMemset(S.nbeam, 0, B * sizeof(int32_t)));
     LB_HIP(hipMemset(S.t0, 0, B * sizeof(int64_t)));
     LB_HIP(hipMemset(S.arena_n, 0, B * sizeof(uint32_t)));
-    LB_HIP(hipMemset(S.evq, 0, 2 * sizeof(unsigned long long)));
     LB_HIP(hipMemset(S.flags, 0, sizeof(uint32_t)));
     LB_HIP(hipMemset(S.counters, 0, static_cast<size_t>(B) * kNumCounters * sizeof(unsigned long long)));
-    LB_HIP(hipMemset(S.lines, 0, static_cast<size_t>(kSpread) * kSpreadStride * sizeof(unsigned long long)));
     return LB_OK;
   };
   if ((st = init()) != LB_OK || (st = build_tables(d, trie, lm, lf)) != LB_OK) {
@@ -439,10 +448,6 @@ lb_status lb_create(const lb_lexicon_desc* lex, const lb_ngram_desc* lm, const l
   P.seed = p.fusion_seed;
   P.lo = p.fusion_lo;
   P.hi = p.fusion_hi;
-  // the query kernel strides over the frame's queries; the selection kernel
-  // runs one wavefront per completed word (at most B*K per frame)
-  d->lmq_grid = static_cast<int>(std::max<uint64_t>(1, std::min<uint64_t>((qcap + 255) / 256, 4096)));
-  d->lms_grid = static_cast<int>(std::max<size_t>(1, std::min<size_t>((BK + 3) / 4, 2048)));
   *out = d;
   return LB_OK;
 }
@@ -461,17 +466,9 @@ lb_status lb_decode_batch(lb_decoder* d, const float* logits, const int32_t* len
   hipStream_t st = static_cast<hipStream_t>(stream);
   const DevParams& P = d->P;
   const DevState& S = d->S;
-  const bool synth = P.fusion_source == LB_FUSION_SYNTH_BIGRAM && P.fusion_interval > 0;
   const bool external = P.fusion_source == LB_FUSION_EXTERNAL;
   EventPair ep{};
-  auto launch = [&](int kind, auto&& fn) -> hipError_t {
-    const bool timed = (d->profile_mask >> kind) & 1u;
-    if (timed) record_start(d, st, &ep, kind);
-    const hipError_t e = fn();
-    if (timed) record_stop(d, st, &ep);
-    d->launches[kind]++;
-    return e;
-  };
+  auto launch = [&](int kind, auto&& fn) -> hipError_t { return timed_launch(d, &ep, kind, fn); };
   auto& X = d->ext;
   int32_t start = 0;
   bool resuming = false;
@@ -500,28 +497,34 @@ lb_status lb_decode_batch(lb_decoder* d, const float* logits, const int32_t* len
       X.flags = flags;
     }
   }
-  if (!resuming && (flags & LB_BEGIN)) LB_HIP(launch_begin(P, S, batch, st));
-  for (int32_t tau = start; tau < frames; ++tau) {
-    LB_HIP(launch(kKindFrame, [&] { return launch_frame(P.K, P, S, logits, lengths, batch, frames, tau, st); }));
-    LB_HIP(launch(kKindLmQuery, [&] { return launch_lmquery(d->lmq_grid, P, S, tau, st); }));
-    LB_HIP(launch(kKindLmSelect, [&] { return launch_lmselect(d->lms_grid, P, S, tau, st); }));
-    if (synth) LB_HIP(launch(kKindFusion, [&] { return launch_fusion(d->block, P, S, lengths, batch, tau, st); }));
-    if (external) {
-      bool any = false;
-      for (int32_t b = 0; b < batch; ++b) {
-        const int64_t t = X.t0[b] + tau;
-        X.flag[b] = (tau < X.len[b] && t > 0 && t % P.fusion_interval == 0) ? 1 : 0;
-        any = any || X.flag[b];
-      }
-      if (any) {
-        LB_HIP(hipMemcpyAsync(X.d_flag, X.flag.data(), batch * sizeof(int32_t), hipMemcpyHostToDevice, st));
-        LB_HIP(hipStreamSynchronize(st));
-        X.pending = 1;
-        X.requested = false;
-        X.resume_tau = tau + 1;
-        return LB_NEED_FUSION;
-      }
+  if (!resuming && (flags & LB_BEGIN)) LB_HIP(launch(kKindBegin, [&] { return launch_begin(P, S, batch, st); }));
+  // frames [start, stop) in one launch; with the external scorer, stop follows
+  // the first frame at which some stream fuses
+  int32_t stop = frames, fuse_tau = -1;
+  if (external) {
+    const int64_t I = P.fusion_interval;
+    for (int32_t b = 0; b < batch; ++b) {
+      // first frame tau >= start of stream b with t = t0 + tau > 0 a multiple of I
+      const int64_t t_lo = std::max<int64_t>(X.t0[b] + start, 1);
+      const int64_t tau = ((t_lo + I - 1) / I) * I - X.t0[b];
+      if (tau < X.len[b] && (fuse_tau < 0 || tau < fuse_tau)) fuse_tau = static_cast<int32_t>(tau);
     }
+    if (fuse_tau >= 0) stop = fuse_tau + 1;
+  }
+  if (start < stop)
+    LB_HIP(launch(kKindDecode,
+                  [&] { return launch_decode(P.K, P, S, logits, lengths, batch, frames, start, stop, st); }));
+  if (fuse_tau >= 0) {
+    for (int32_t b = 0; b < batch; ++b) {
+      const int64_t t = X.t0[b] + fuse_tau;
+      X.flag[b] = (fuse_tau < X.len[b] && t > 0 && t % P.fusion_interval == 0) ? 1 : 0;
+    }
+    LB_HIP(hipMemcpyAsync(X.d_flag, X.flag.data(), batch * sizeof(int32_t), hipMemcpyHostToDevice, st));
+    LB_HIP(hipStreamSynchronize(st));
+    X.pending = 1;
+    X.requested = false;
+    X.resume_tau = fuse_tau + 1;
+    return LB_NEED_FUSION;
   }
   if (external && (flags & LB_END) && !X.final_done) {
     for (int32_t b = 0; b < batch; ++b) X.flag[b] = 2;
@@ -549,8 +552,10 @@ lb_status lb_fusion_request(lb_decoder* d, int32_t* words, int32_t* n_words, voi
   if (!d->ext.pending) return fail(LB_ERR_STATE, "no fusion request is pending");
   if (!words || !n_words) return fail(LB_ERR_INVALID_ARG, "null device pointer");
   hipStream_t st = static_cast<hipStream_t>(stream);
-  LB_HIP(launch_fuse_select(d->block, d->P, d->S, d->ext.d_flag, d->ext.B, st));
-  LB_HIP(launch_fuse_export(d->block, d->P, d->S, words, n_words, d->ext.B, st));
+  EventPair ep{};
+  auto launch = [&](int kind, auto&& fn) -> hipError_t { return timed_launch(d, &ep, kind, fn); };
+  LB_HIP(launch(kKindFuseSelect, [&] { return launch_fuse_select(d->block, d->P, d->S, d->ext.d_flag, d->ext.B, st); }));
+  LB_HIP(launch(kKindFuseExport, [&] { return launch_fuse_export(d->block, d->P, d->S, words, n_words, d->ext.B, st); }));
   d->ext.requested = true;
   return LB_OK;
 }
@@ -561,8 +566,11 @@ lb_status lb_fusion_scores(lb_decoder* d, const float* fusion_logprobs, void* st
   if (!d->ext.pending) return fail(LB_ERR_STATE, "no fusion request is pending");
   if (!fusion_logprobs) return fail(LB_ERR_INVALID_ARG, "null device pointer");
   hipStream_t st = static_cast<hipStream_t>(stream);
-  if (!d->ext.requested) LB_HIP(launch_fuse_select(d->block, d->P, d->S, d->ext.d_flag, d->ext.B, st));
-  LB_HIP(launch_fuse_apply(d->block, d->P, d->S, fusion_logprobs, d->ext.B, st));
+  EventPair ep{};
+  auto launch = [&](int kind, auto&& fn) -> hipError_t { return timed_launch(d, &ep, kind, fn); };
+  if (!d->ext.requested)
+    LB_HIP(launch(kKindFuseSelect, [&] { return launch_fuse_select(d->block, d->P, d->S, d->ext.d_flag, d->ext.B, st); }));
+  LB_HIP(launch(kKindFuseApply, [&] { return launch_fuse_apply(d->block, d->P, d->S, fusion_logprobs, d->ext.B, st); }));
   d->ext.pending = 0;
   d->ext.requested = false;
   return LB_OK;
@@ -594,9 +602,6 @@ lb_status lb_get_stats(lb_decoder* d, lb_stats* out) {
     out->frames += static_cast<int64_t>(x[kCntFrames]);
     out->probe_lines += static_cast<int64_t>(x[kCntProbeLines]);
   }
-  std::vector<unsigned long long> ln(static_cast<size_t>(kSpread) * kSpreadStride);
-  LB_HIP(hipMemcpy(ln.data(), d->S.lines, ln.size() * sizeof(unsigned long long), hipMemcpyDeviceToHost));
-  for (int k = 0; k < kSpread; ++k) out->probe_lines += static_cast<int64_t>(ln[static_cast<size_t>(k) * kSpreadStride]);
   d->harvest();
   for (int k = 0; k < kKinds; ++k) {
     out->launches[k] = d->launches[k];
@@ -610,7 +615,6 @@ lb_status lb_reset_stats(lb_decoder* d) {
   if (!d) return fail(LB_ERR_INVALID_ARG, "decoder is null");
   LB_HIP(hipDeviceSynchronize());
   LB_HIP(hipMemset(d->S.counters, 0, static_cast<size_t>(d->p.max_batch) * kNumCounters * sizeof(unsigned long long)));
-  LB_HIP(hipMemset(d->S.lines, 0, static_cast<size_t>(kSpread) * kSpreadStride * sizeof(unsigned long long)));
   d->harvest();
   for (int k = 0; k < kKinds; ++k) {
     d->launches[k] = 0;

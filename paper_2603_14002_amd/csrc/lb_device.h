@@ -16,6 +16,8 @@
 //   beams       SoA [max_batch][K] (sub-beam arrays [max_batch][K][O])
 //   arena       HistNode[1 + max_batch*cap]: word-history nodes; node 0 is the
 //               empty history (context <s>), stream b owns [1+b*cap, 1+(b+1)*cap)
+//   scrL, scrS  [max_batch][K*O*Hmax] per-stream n-gram lookup results of a
+//               frame (Hmax: the largest homophone set)
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -43,9 +45,6 @@ constexpr uint32_t kFlagBuildRange = 8u;
 constexpr uint32_t kFlagBuildContext = 16u;
 constexpr uint32_t kFlagBuildDup = 32u;
 constexpr uint32_t kFlagBuildFull = 64u;
-
-constexpr int kSpread = 256;       // slots of DevState::lines
-constexpr int kSpreadStride = 16;  // 16 x 8 B = one 128-B line per slot
 
 // per-stream counters (DevState::counters, [max_batch][kNumCounters])
 enum { kCntExpansions = 0, kCntWordEvents = 1, kCntLmQueries = 2, kCntFused = 3, kCntFrames = 4,
@@ -87,19 +86,6 @@ struct HistNode {
   double sfus;
 };
 
-// A hypothesis that completed a word this frame (Eq. (1) applies to it).
-struct Event {
-  uint32_t stream;
-  uint32_t beam;
-  uint32_t pnode;  // trie node of the completed word
-  uint32_t woff;   // its first homophone in trie_words
-  uint32_t H;      // number of homophones
-  uint32_t nsub;   // parent sub-beams
-  uint32_t qoff;   // first (sub-beam, homophone) query of the event in the frame's query arrays
-  uint32_t pad;
-  uint32_t hist[kMaxSub];  // parent sub-beams' history nodes
-};
-
 // n-gram state after a queried word: slots of its 2- and 3-word contexts and their backoffs.
 struct QState {
   uint32_t c2, c3;
@@ -132,16 +118,12 @@ struct DevState {
   uint32_t* arena_n;  // [B] arena nodes used
   HistNode* arena;
   uint64_t arena_cap;  // per stream
-  Event* events;       // [B*K]
-  unsigned long long* evq;  // [2] per frame parity: events << 32 | queries
-  uint32_t* qmap;      // [qcap] query -> event
-  double* qL;          // [qcap] candidate sub-beam score of each query
-  QState* qS;          // [qcap] n-gram state after the query's word
-  uint64_t qcap;
+  // per-stream LM lookup results of a frame: [B][scap] log10 p and n-gram state
+  double* scrL;
+  QState* scrS;
+  uint64_t scap;
   uint32_t* flags;
   unsigned long long* counters;  // [B][kNumCounters]
-  // probed bucket lines, spread over kSpread slots 128 B apart (summed on the host)
-  unsigned long long* lines;
   // fusion selection for external scores: [B][K] beam index per rank, [B] count
   int32_t* fsel;
   int32_t* fsel_n;

@@ -1,19 +1,14 @@
 // HIP kernels of the LightBeam gfx950 decoder (wave64, CDNA4).
 //
-// One frame of Alg. 1 is three launches on the caller's stream:
-//   k_frame   one workgroup per stream: fan-out of every hypothesis by blank,
-//             repeat and each lexicon-valid symbol (trie child mask), token /
-//             word bonuses, recombination of equal prefixes by log-sum-exp,
-//             theta pruning, top-K selection (MSD radix select on the ordered
-//             score bits and the 64-bit prefix key), beam update and trie-state
-//             advance; hypotheses that completed a word are queued.
-//   k_ngram   one wavefront per queued hypothesis: every (sub-beam, homophone)
-//             pair is scored with the 4-gram backoff LM by probing the HBM hash
-//             tables, the top-o survive, lambda pruning, word-history append
-//             (Eq. (1), App. E.3).
-//   k_fusion  one workgroup per stream, only on fusion frames: top-F selection
-//             and replacement of the sub-beam scores by phi * S_fus (Eq. (2)).
-// k_output ranks the hypotheses of each stream and writes word ids / scores.
+// A decode call is one launch of k_decode on the caller's stream: one
+// workgroup per stream runs Alg. 1 over the call's frames with the stream's
+// beam resident in LDS (fan-out, recombination, theta / top-K pruning, trie
+// advance, Eq. (1) with the hashed 4-gram LM, Eq. (2) with the synthetic
+// scorer).  k_output ranks the hypotheses of each stream and writes word ids /
+// scores (after the final fusion at the end of an utterance).  k_fuse_select,
+// k_fuse_export and k_fuse_apply carry the round trip to an external fusion
+// scorer; k_build_order fills the n-gram hash tables; k_begin resets streams.
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include "lb_device.h"
@@ -27,12 +22,6 @@ constexpr double kNegInf = -HUGE_VAL;
 constexpr int kBins = 1024;         // score bins of the top-K selection
 constexpr int kBoundaryCap = 256;   // candidates resolved exactly inside the boundary bin
 constexpr int kMaxLevels = 16;      // refinement levels of the top-K selection
-#ifndef LB_CAND_UNROLL
-#define LB_CAND_UNROLL 64
-#endif
-#ifndef LB_LPB_LARGE
-#define LB_LPB_LARGE 4
-#endif
 
 // ------------------------------------------------------------------ block helpers
 
@@ -104,14 +93,15 @@ __device__ inline bool ranks_before(double sa, uint64_t ka, double sb, uint64_t 
   return sa > sb || (sa == sb && ka < kb);
 }
 
-// In-place bitonic sort of BLOCK entries (one per thread) by (score desc, key asc).
-template <int BLOCK>
+// In-place bitonic sort of N entries (N a power of two, at most the block
+// size) by (score desc, key asc); every thread of the block calls it.
+template <int N>
 __device__ inline void bitonic_sort(double* sc, uint64_t* ky, uint32_t* val) {
   const int i = threadIdx.x;
-  for (int k = 2; k <= BLOCK; k <<= 1) {
+  for (int k = 2; k <= N; k <<= 1) {
     for (int j = k >> 1; j > 0; j >>= 1) {
       const int ixj = i ^ j;
-      if (ixj > i) {
+      if (i < N && ixj > i) {
         const bool up = (i & k) == 0;
         const bool swap = up ? ranks_before(sc[ixj], ky[ixj], sc[i], ky[i])
                              : ranks_before(sc[i], ky[i], sc[ixj], ky[ixj]);
@@ -129,27 +119,6 @@ __device__ inline void bitonic_sort(double* sc, uint64_t* ky, uint32_t* val) {
       }
       __syncthreads();
     }
-  }
-}
-
-// 8-bit digit of the 128-bit value (hi:lo) starting at bit `pos` (0..120).
-__device__ inline uint32_t digit128(uint64_t hi, uint64_t lo, int pos) {
-  if (pos >= 64) return static_cast<uint32_t>(hi >> (pos - 64)) & 0xFFu;
-  if (pos > 56) return static_cast<uint32_t>((hi << (64 - pos)) | (lo >> pos)) & 0xFFu;
-  return static_cast<uint32_t>(lo >> pos) & 0xFFu;
-}
-
-// Mask of the bits >= pos of a 128-bit value, split in (hi, lo).
-__device__ inline void mask_from(int pos, uint64_t* mhi, uint64_t* mlo) {
-  if (pos >= 128) {
-    *mhi = 0;
-    *mlo = 0;
-  } else if (pos >= 64) {
-    *mhi = ~0ull << (pos - 64);
-    *mlo = 0;
-  } else {
-    *mhi = ~0ull;
-    *mlo = pos == 0 ? ~0ull : (~0ull << pos);
   }
 }
 
@@ -260,469 +229,7 @@ __global__ void k_begin(DevParams P, DevState S, int32_t B) {
   S.arena_n[b] = 0;
 }
 
-// ------------------------------------------------------------------ frame step
-
-// One workgroup per stream.  Hypothesis i is owned by LPB consecutive lanes:
-// lane s of it handles the extensions v = 1+s, 1+s+LPB, ... (and lane 0 the
-// merged stay), with the hypothesis' scores held in registers.
-template <int KMAX, int LPB>
-__global__ __launch_bounds__(KMAX * LPB) void k_frame(const DevParams P, const DevState S,
-                                                      const float* __restrict__ logits,
-                                                      const int32_t* __restrict__ lengths, int32_t Tc,
-                                                      int32_t tau) {
-  constexpr int BLOCK = KMAX * LPB;
-  constexpr int HS = 2 * KMAX;  // LDS hash slots for the current prefix keys
-  constexpr int NW = BLOCK / 64;
-  constexpr int NC = (kSep + LPB - 1) / LPB;  // extension slots per lane
-  const int b = blockIdx.x;
-  const int tid = threadIdx.x;
-  if (b == 0 && tid == 0) S.evq[(tau + 1) & 1] = 0;
-  if (tau >= lengths[b]) return;
-
-  __shared__ double sD[kClasses];
-  __shared__ uint64_t sKey[KMAX], sPkey[KMAX];
-  __shared__ double sAb[KMAX], sP[KMAX], sL[KMAX], sAb2[KMAX], sAnb2[KMAX], sPt2[KMAX], sStay[KMAX];
-  __shared__ uint32_t sNode[KMAX], sMeta[KMAX], sFirst[KMAX], sWoff[KMAX], sNwords[KMAX];
-  __shared__ uint64_t sMask[KMAX], sTrieMask[KMAX];
-  __shared__ double sLw[KMAX * kMaxSub];
-  __shared__ uint32_t sHist[KMAX * kMaxSub];
-  __shared__ unsigned long long sHKey[HS];
-  __shared__ int32_t sHIdx[HS];
-  __shared__ uint32_t sHisto[kBins];
-  __shared__ double sBScore[kBoundaryCap];
-  __shared__ uint64_t sBKey[kBoundaryCap];
-  __shared__ double sLvHi[kMaxLevels], sLvInv[kMaxLevels];
-  __shared__ int32_t sLvBeta[kMaxLevels], sLvShift[kMaxLevels];
-  __shared__ uint32_t sSelSrc[KMAX];
-  __shared__ uint32_t sEvQ[KMAX];
-  __shared__ double sRed[2 * NW];
-  __shared__ int32_t sScan[NW];
-  __shared__ int32_t sBucket, sAbove, sBucketCnt, sBCount;
-  __shared__ unsigned long long sEvBase;
-
-  const int n = S.nbeam[b];
-  const size_t gb = static_cast<size_t>(b) * P.K;
-
-  // ---- load the frame's scaled log-probs and the hypotheses
-  for (int v = tid; v < kClasses; v += BLOCK)
-    sD[v] = P.alpha * static_cast<double>(logits[(static_cast<size_t>(b) * Tc + tau) * kClasses + v]);
-  for (int s = tid; s < HS; s += BLOCK) sHKey[s] = kEmptyKey;
-  uint64_t my_key = 0, my_pkey = kNoParent;
-  double my_anb = kNegInf;
-  uint32_t my_meta = 0;
-  if (tid < n) {
-    my_key = S.key[gb + tid];
-    my_pkey = S.pkey[gb + tid];
-    const double ab = S.ab[gb + tid];
-    my_anb = S.anb[gb + tid];
-    const uint32_t node = S.node[gb + tid];
-    my_meta = S.meta[gb + tid];
-    const TrieNode tn = S.trie[node];
-    sKey[tid] = my_key;
-    sPkey[tid] = my_pkey;
-    sAb[tid] = ab;
-    sP[tid] = S.pt[gb + tid];  // log-sum-exp(ab, anb), kept with the hypothesis
-    sNode[tid] = node;
-    sMeta[tid] = my_meta;
-    const int nsub = (my_meta >> 8) & 0xFF;
-    for (int j = 0; j < nsub; ++j) {
-      sLw[tid * kMaxSub + j] = S.Lw[(gb + tid) * P.O + j];
-      sHist[tid * kMaxSub + j] = S.hist[(gb + tid) * P.O + j];
-    }
-    sL[tid] = sLw[tid * kMaxSub];
-    sMask[tid] = tn.mask;
-    sTrieMask[tid] = tn.mask;
-    sFirst[tid] = tn.first_child;
-    sWoff[tid] = tn.word_off;
-    sNwords[tid] = static_cast<uint32_t>(tn.mask >> kWordCountShift);
-  }
-  __syncthreads();
-
-  // ---- prefix keys into an LDS hash table
-  if (tid < n) {
-    uint32_t s = static_cast<uint32_t>(my_key) & (HS - 1);
-    for (;;) {
-      const unsigned long long prev = atomicCAS(&sHKey[s], kEmptyKey, my_key);
-      if (prev == kEmptyKey) {
-        sHIdx[s] = tid;
-        break;
-      }
-      s = (s + 1) & (HS - 1);
-    }
-  }
-  __syncthreads();
-
-  // ---- recombination: a hypothesis whose parent prefix is also live receives
-  // the parent's extension by its last symbol; that extension is removed from
-  // the parent's fan-out.
-  int par = -1;
-  if (tid < n && my_pkey != kNoParent) {
-    uint32_t s = static_cast<uint32_t>(my_pkey) & (HS - 1);
-    for (int probes = 0; probes < HS; ++probes) {
-      const unsigned long long k = sHKey[s];
-      if (k == kEmptyKey) break;
-      if (k == my_pkey) {
-        par = sHIdx[s];
-        break;
-      }
-      s = (s + 1) & (HS - 1);
-    }
-    if (par >= 0) atomicAnd(reinterpret_cast<unsigned long long*>(&sMask[par]), ~(1ull << (my_meta & 0xFF)));
-  }
-  __syncthreads();
-
-  // ---- stay candidates (blank-stay, repeat-stay, merged parent extension)
-  if (tid < n) {
-    const int last = my_meta & 0xFF;
-    const double ab2 = sP[tid] + sD[0];
-    const double rep = last ? my_anb + sD[last] : kNegInf;
-    double ext = kNegInf;
-    if (par >= 0) {
-      const double base = (last == static_cast<int>(sMeta[par] & 0xFF)) ? sAb[par] : sP[par];
-      ext = (base + sD[last]) + (last == kSep ? P.gamma : P.beta);
-    }
-    const double anb2 = lse2(rep, ext);
-    const double pt2 = lse2(ab2, anb2);
-    sAb2[tid] = ab2;
-    sAnb2[tid] = anb2;
-    sPt2[tid] = pt2;
-    sStay[tid] = pt2 + sL[tid];
-  }
-  __syncthreads();
-
-  // ---- this lane's candidates: slot k is the extension by v = 1 + ln + LPB*k,
-  // plus the merged stay on lane 0; scores are recomputed in every pass (same
-  // operations, same result)
-  const int hi_ = tid / LPB;
-  const int ln = tid - hi_ * LPB;
-  const bool live = hi_ < n;
-  uint64_t c_key = 0, c_mask = 0;
-  double c_stay = kNegInf, c_ab = 0.0, c_p = 0.0, c_L = 0.0;
-  int c_last = 0;
-  if (live) {
-    c_ab = sAb[hi_];
-    c_p = sP[hi_];
-    c_L = sL[hi_];
-    c_last = sMeta[hi_] & 0xFF;
-    c_mask = sMask[hi_];
-    c_key = sKey[hi_];
-    if (ln == 0) c_stay = sStay[hi_];
-  }
-  auto score_now = [&](int k) -> double {
-    const int v = 1 + ln + LPB * k;
-    if (v > kSep || !((c_mask >> v) & 1ull)) return kNegInf;
-    const double base = (v == c_last) ? c_ab : c_p;
-    return ((base + sD[v]) + (v == kSep ? P.gamma : P.beta)) + c_L;
-  };
-  auto score_of = score_now;
-  auto key_of = [&](int v) -> uint64_t { return v == 0 ? c_key : prefix_step(c_key, v); };
-  // f(v, score) for each of this lane's candidates with a finite score
-  auto for_cands = [&](auto&& f) {
-    if (c_stay != kNegInf) f(0, c_stay);
-#pragma unroll LB_CAND_UNROLL
-    for (int k = 0; k < NC; ++k) {
-      const double s = score_of(k);
-      if (s != kNegInf) f(1 + ln + LPB * k, s);
-    }
-  };
-
-  double mx = kNegInf, mn = HUGE_VAL;
-  for_cands([&](int, double s) {
-    mx = fmax(mx, s);
-    mn = fmin(mn, s);
-  });
-  double best, lowest;
-  block_minmax<BLOCK>(mx, mn, sRed, &best, &lowest);
-  const double thr = best - P.theta;
-
-  // ---- top-K.  Level 0 bins (best - score) over [max(thr, lowest), best] into
-  // kBins; the map is monotone, so bins above the one holding the K-th
-  // candidate are taken whole.  That bin is resolved exactly by rank on
-  // (score desc, key asc) when it holds at most kBoundaryCap candidates;
-  // otherwise it is re-binned over its own score range (deeper levels), and
-  // when its scores are all equal, by the bits of the key (smaller key first).
-  const double lo0 = fmax(thr, lowest);
-  const double inv0 = best > lo0 ? static_cast<double>(kBins) / (best - lo0) : 0.0;
-  const int shift0 = best > lo0 ? -1 : 64 - 10;
-  auto bin_score = [&](double hi, double inv, double s) -> int {
-    const double x = (hi - s) * inv;
-    return x >= static_cast<double>(kBins - 1) ? kBins - 1 : static_cast<int>(x);
-  };
-  auto bin0 = [&](int v, double s) -> int {
-    return shift0 < 0 ? bin_score(best, inv0, s) : static_cast<int>((key_of(v) >> shift0) & (kBins - 1));
-  };
-  // deeper levels (rare): parameters in LDS
-  auto bin_at = [&](int l, int v, double s) -> int {
-    const int sh = sLvShift[l];
-    if (sh >= 0) return static_cast<int>((key_of(v) >> sh) & (kBins - 1));
-    return bin_score(sLvHi[l], sLvInv[l], s);
-  };
-  // candidates in the boundary bin of levels 0..L-1
-  auto member = [&](int L, int v, double s) -> bool {
-    if (s < thr || bin0(v, s) != sLvBeta[0]) return false;
-    for (int l = 1; l < L; ++l)
-      if (bin_at(l, v, s) != sLvBeta[l]) return false;
-    return true;
-  };
-  // the lane's candidates with scores recomputed (no register array): for the rare levels
-  auto for_cands_rt = [&](auto&& f) {
-    if (c_stay != kNegInf) f(0, c_stay);
-#pragma unroll 1
-    for (int k = 0; k < NC; ++k) {
-      const double s = score_now(k);
-      if (s != kNegInf) f(1 + ln + LPB * k, s);
-    }
-  };
-  // finds the bin holding the need-th candidate of sHisto; returns via sBucket/sAbove/sBucketCnt
-  auto find_bin = [&](int need_in) -> int {
-    constexpr int PER = (kBins + BLOCK - 1) / BLOCK;
-    int local = 0;
-#pragma unroll
-    for (int q = 0; q < PER; ++q) {
-      const int d = tid * PER + q;
-      local += d < kBins ? static_cast<int>(sHisto[d]) : 0;
-    }
-    int tot = 0;
-    const int before = block_scan<BLOCK>(local, sScan, &tot);
-    if (need_in > 0 && before < need_in && before + local >= need_in) {
-      int acc = before;
-      for (int q = 0; q < PER; ++q) {
-        const int d = tid * PER + q;
-        const int h = static_cast<int>(sHisto[d]);
-        if (acc + h >= need_in) {
-          sBucket = d;
-          sAbove = acc;
-          sBucketCnt = h;
-          break;
-        }
-        acc += h;
-      }
-    }
-    __syncthreads();
-    return tot;
-  };
-
-  // level-0 bin of each of the lane's candidates, kept packed 16 bits per slot
-  // (0xFFFF: no candidate); exact scores are recomputed only inside the boundary bin
-  uint32_t binp[(NC + 1) / 2];
-  uint32_t bin_stay = 0xFFFFu;
-  for (int d = tid; d < kBins; d += BLOCK) sHisto[d] = 0;
-  __syncthreads();
-  if (c_stay != kNegInf && c_stay >= thr) {
-    bin_stay = static_cast<uint32_t>(bin0(0, c_stay));
-    atomicAdd(&sHisto[bin_stay], 1u);
-  }
-#pragma unroll
-  for (int k = 0; k < NC; ++k) {
-    const double s = score_now(k);
-    uint32_t bn = 0xFFFFu;
-    if (s != kNegInf && s >= thr) {
-      bn = static_cast<uint32_t>(bin0(1 + ln + LPB * k, s));
-      atomicAdd(&sHisto[bn], 1u);
-    }
-    if (k & 1)
-      binp[k >> 1] |= bn << 16;
-    else
-      binp[k >> 1] = bn;
-  }
-  __syncthreads();
-  const int nvalid = find_bin(P.K);
-  const bool select_all = nvalid <= P.K;
-  int beta0 = kBins, nlev = 1, need = P.K, nbc = 0;
-  bool all_bin = false;
-  if (!select_all) {
-    beta0 = sBucket;
-    need -= sAbove;
-    int cntb = sBucketCnt;
-    if (tid == 0) {
-      sLvBeta[0] = beta0;
-      sLvShift[0] = shift0;
-    }
-    __syncthreads();
-    int key_shift = shift0 >= 0 ? shift0 - 10 : 64 - 10;
-    bool key_level = shift0 >= 0;
-    while (cntb != need && cntb > kBoundaryCap && !(key_level && sLvShift[nlev - 1] == 0) && nlev < kMaxLevels) {
-      // refine: score range of the boundary bin's members, or key bits when it is flat
-      const int L = nlev;
-      double bmx = kNegInf, bmn = HUGE_VAL;
-      for_cands_rt([&](int v, double s) {
-        if (member(L, v, s)) {
-          bmx = fmax(bmx, s);
-          bmn = fmin(bmn, s);
-        }
-      });
-      double lv_hi, lv_lo;
-      block_minmax<BLOCK>(bmx, bmn, sRed, &lv_hi, &lv_lo);
-      if (tid == 0) {
-        sLvHi[L] = lv_hi;
-        sLvInv[L] = lv_hi > lv_lo ? static_cast<double>(kBins) / (lv_hi - lv_lo) : 0.0;
-        sLvShift[L] = lv_hi > lv_lo ? -1 : (key_shift > 0 ? key_shift : 0);
-      }
-      for (int d = tid; d < kBins; d += BLOCK) sHisto[d] = 0;
-      __syncthreads();
-      key_level = sLvShift[L] >= 0;
-      if (key_level) key_shift -= 10;
-      for_cands_rt([&](int v, double s) {
-        if (member(L, v, s)) atomicAdd(&sHisto[bin_at(L, v, s)], 1u);
-      });
-      __syncthreads();
-      (void)find_bin(need);
-      if (tid == 0) sLvBeta[L] = sBucket;
-      need -= sAbove;
-      cntb = sBucketCnt;
-      nlev = L + 1;
-      __syncthreads();
-    }
-    if (cntb == need) {
-      all_bin = true;
-    } else {
-      // exact rank inside the boundary bin (a flat key level of shift 0 holds one key)
-      if (tid == 0) sBCount = 0;
-      __syncthreads();
-      const int L = nlev;
-      for_cands_rt([&](int v, double s) {
-        if (!member(L, v, s)) return;
-        const int slot = atomicAdd(&sBCount, 1);
-        if (slot < kBoundaryCap) {
-          sBScore[slot] = s;
-          sBKey[slot] = key_of(v);
-        }
-      });
-      __syncthreads();
-      nbc = sBCount < kBoundaryCap ? sBCount : kBoundaryCap;
-      if (sBCount > kBoundaryCap && tid == 0) atomicOr(S.flags, kFlagSelect);
-    }
-  }
-  // selection of a candidate from its level-0 bin; the exact score (score_fn)
-  // is needed only inside the boundary bin
-  auto selected = [&](uint32_t bn, int v, auto&& score_fn) -> bool {
-    if (bn == 0xFFFFu) return false;
-    if (select_all) return true;
-    if (static_cast<int>(bn) != beta0) return static_cast<int>(bn) < beta0;
-    const double s = score_fn();
-    for (int l = 1; l < nlev; ++l) {
-      const int bl = bin_at(l, v, s);
-      if (bl != sLvBeta[l]) return bl < sLvBeta[l];
-    }
-    if (all_bin) return true;
-    // rank inside the boundary bin by (score desc, key asc)
-    const uint64_t k = key_of(v);
-    int rank = 0;
-    for (int u = 0; u < nbc; ++u) rank += ranks_before(sBScore[u], sBKey[u], s, k);
-    return rank < need;
-  };
-
-  // ---- selection bits (bit 0: the stay, bit k+1: slot k), then a
-  // deterministic gather of the sources in lane order
-  uint64_t sel_bits = 0;
-  if (selected(bin_stay, 0, [&] { return c_stay; })) sel_bits |= 1ull;
-#pragma unroll
-  for (int k = 0; k < NC; ++k) {
-    const uint32_t bn = (binp[k >> 1] >> ((k & 1) * 16)) & 0xFFFFu;
-    if (selected(bn, 1 + ln + LPB * k, [&] { return score_now(k); })) sel_bits |= 2ull << k;
-  }
-  int nsel = 0;
-  int wpos = block_scan<BLOCK>(__popcll(sel_bits), sScan, &nsel);
-  if (nsel > P.K) {  // cannot happen when the selection is exact; never write past K entries
-    nsel = P.K;
-    if (tid == 0) atomicOr(S.flags, kFlagSelect);
-  }
-  if ((sel_bits & 1ull) && wpos < nsel) sSelSrc[wpos++] = static_cast<uint32_t>(hi_);
-#pragma unroll LB_CAND_UNROLL
-  for (int k = 0; k < NC; ++k)
-    if (((sel_bits >> (k + 1)) & 1ull) && wpos < nsel)
-      sSelSrc[wpos++] = static_cast<uint32_t>(hi_) | (static_cast<uint32_t>(1 + ln + LPB * k) << 16);
-  __syncthreads();
-
-  // ---- write the new hypotheses (in place: every old value is in LDS)
-  const int r = tid;
-  int is_event = 0, my_nq = 0, ev_src = 0;
-  uint32_t ev_pnode = 0, ev_woff = 0, ev_H = 0, ev_nsub = 0;
-  if (r < nsel) {
-    const uint32_t src = sSelSrc[r];
-    const int i = src & 0xFFFF;
-    const int v = src >> 16;
-    const size_t o = gb + r;
-    const uint32_t meta_i = sMeta[i];
-    const int nsub = (meta_i >> 8) & 0xFF;
-    if (v == 0) {
-      S.key[o] = sKey[i];
-      S.pkey[o] = sPkey[i];
-      S.ab[o] = sAb2[i];
-      S.anb[o] = sAnb2[i];
-      S.pt[o] = sPt2[i];
-      S.node[o] = sNode[i];
-      S.meta[o] = meta_i;
-    } else {
-      const int last = meta_i & 0xFF;
-      const double base = (v == last) ? sAb[i] : sP[i];
-      const double anb = (base + sD[v]) + (v == kSep ? P.gamma : P.beta);
-      S.key[o] = prefix_step(sKey[i], v);
-      S.pkey[o] = sKey[i];
-      S.ab[o] = kNegInf;
-      S.anb[o] = anb;
-      S.pt[o] = lse2(kNegInf, anb);
-      uint32_t child = kRootNode;
-      if (v != kSep) child = sFirst[i] + __popcll(sTrieMask[i] & ((1ull << v) - 1ull));
-      S.node[o] = child;
-      S.meta[o] = static_cast<uint32_t>(v) | (meta_i & 0xFF00u);
-      if (v == kSep) {
-        is_event = 1;
-        ev_pnode = sNode[i];
-        ev_woff = sWoff[i];
-        ev_H = sNwords[i];
-        ev_nsub = static_cast<uint32_t>(nsub);
-        my_nq = static_cast<int>(ev_nsub * ev_H);
-        ev_src = i;
-      }
-    }
-    for (int j = 0; j < nsub; ++j) {
-      S.Lw[o * P.O + j] = sLw[i * kMaxSub + j];
-      S.hist[o * P.O + j] = sHist[i * kMaxSub + j];
-    }
-  }
-  int nev = 0, nq_blk = 0;
-  const int erank = block_scan<BLOCK>(is_event, sScan, &nev);
-  const int qpos = block_scan<BLOCK>(my_nq, sScan, &nq_blk);
-  if (tid == 0) {
-    S.nbeam[b] = nsel;
-    sEvBase = nev ? atomicAdd(&S.evq[tau & 1], (static_cast<unsigned long long>(nev) << 32) |
-                                                   static_cast<unsigned long long>(nq_blk))
-                  : 0ull;
-    unsigned long long* cn = S.counters + static_cast<size_t>(b) * kNumCounters;
-    cn[kCntExpansions] += static_cast<unsigned long long>(n) * kClasses;
-    cn[kCntFrames] += 1;
-  }
-  if (is_event) sEvQ[erank] = static_cast<uint32_t>(qpos);
-  __syncthreads();
-  const uint32_t ev0 = static_cast<uint32_t>(sEvBase >> 32);
-  const uint32_t q0 = static_cast<uint32_t>(sEvBase);
-  if (is_event) {
-    Event e;
-    e.stream = b;
-    e.beam = r;
-    e.pnode = ev_pnode;
-    e.woff = ev_woff;
-    e.H = ev_H;
-    e.nsub = ev_nsub;
-    e.qoff = q0 + qpos;
-    e.pad = 0;
-#pragma unroll
-    for (int j = 0; j < kMaxSub; ++j) e.hist[j] = j < static_cast<int>(ev_nsub) ? sHist[ev_src * kMaxSub + j] : 0u;
-    S.events[ev0 + erank] = e;
-  }
-  // query -> event map of this block's queries (events are contiguous, in order)
-  for (int k = tid; k < nq_blk; k += BLOCK) {
-    int lo = 0, hi = nev - 1;
-    while (lo < hi) {
-      const int mid = (lo + hi + 1) >> 1;
-      if (sEvQ[mid] <= static_cast<uint32_t>(k)) lo = mid; else hi = mid - 1;
-    }
-    S.qmap[q0 + k] = ev0 + lo;
-  }
-}
-
-// ------------------------------------------------------------------ n-gram shallow fusion
+// ------------------------------------------------------------------ n-gram lookup
 
 // One 64-B bucket: four 16-B slots {key lo, key hi, log10 p, backoff}.
 struct Bucket {
@@ -778,188 +285,915 @@ __device__ __forceinline__ bool resolve(const NgramTable& t, uint64_t key, uint6
   return r == 1;
 }
 
-__device__ __forceinline__ uint32_t hist_of(const Event& ev, uint32_t j) {
-  return j == 0 ? ev.hist[0] : (j == 1 ? ev.hist[1] : (j == 2 ? ev.hist[2] : ev.hist[3]));
-}
+// log10 P(w | the last three words of history ctx) by Katz backoff over the
+// hashed tables (Eq. (1), App. E.3), and the n-gram state after w.  The three
+// bucket lines (orders 2, 3, 4) and the unigram are loaded together, then
+// resolved; `lines` counts the bucket lines read.
+struct LmResult {
+  double lp;
+  QState st;
+};
 
-// The LM lookup phase: one thread per (completed word, parent sub-beam,
-// homophone) query of the frame, over every stream.  The three bucket lines
-// (orders 2, 3, 4) and the unigram are loaded together, then resolved.
-__global__ __launch_bounds__(256) void k_lmquery(const DevParams P, const DevState S, int32_t tau) {
-  const uint32_t nq = static_cast<uint32_t>(S.evq[tau & 1]);
-  uint32_t lines = 0;
-  const uint32_t stride = gridDim.x * blockDim.x;
-  for (uint32_t q = blockIdx.x * blockDim.x + threadIdx.x; q < nq; q += stride) {
-    const Event ev = S.events[S.qmap[q]];
-    const uint32_t loc = q - ev.qoff;
-    const uint32_t j = loc / ev.H;
-    const uint32_t h = loc - j * ev.H;
-    const int w = S.trie_words[ev.woff + h];
-    const uint32_t ph = hist_of(ev, j);
-    const HistNode ctx = S.arena[ph];
-    const double Lw = S.Lw[(static_cast<size_t>(ev.stream) * P.K + ev.beam) * P.O + j];
-    const uint64_t k2 = (static_cast<uint64_t>(static_cast<uint32_t>(ctx.word)) << 32) | static_cast<uint32_t>(w);
-    const uint64_t k3 = (static_cast<uint64_t>(ctx.c2) << 32) | static_cast<uint32_t>(w);
-    const uint64_t k4 = (static_cast<uint64_t>(ctx.c3) << 32) | static_cast<uint32_t>(w);
-    const bool has3 = ctx.c2 != kNone;
-    const bool has4 = ctx.c3 != kNone;
-    const uint64_t b2 = bucket_of(k2, S.t2.nbuckets);
-    const uint64_t b3 = has3 ? bucket_of(k3, S.t3.nbuckets) : 0;
-    const uint64_t b4 = has4 ? bucket_of(k4, S.t4.nbuckets) : 0;
-    const Bucket q2 = load_bucket(S.t2, b2);
-    const Bucket q3 = has3 ? load_bucket(S.t3, b3) : Bucket{};
-    const Bucket q4 = has4 ? load_bucket(S.t4, b4) : Bucket{};
-    const Unigram u = S.uni[w];
-    lines += 1u + (has3 ? 1u : 0u) + (has4 ? 1u : 0u);
-    uint32_t s2 = kNone, s3 = kNone, s4 = kNone;
-    float p2 = 0.f, bb2 = 0.f, p3 = 0.f, bb3 = 0.f, p4 = 0.f, bb4 = 0.f;
-    const bool f2 = resolve(S.t2, k2, b2, q2, &s2, &p2, &bb2, &lines);
-    const bool f3 = has3 && resolve(S.t3, k3, b3, q3, &s3, &p3, &bb3, &lines);
-    const bool f4 = has4 && resolve(S.t4, k4, b4, q4, &s4, &p4, &bb4, &lines);
-    // log10 P(w | context) by backoff, innermost order first
-    double lp;
-    if (f4) {
-      lp = static_cast<double>(p4);
+__device__ __forceinline__ LmResult lm_lookup(const DevState& S, int32_t w, const HistNode& ctx, uint32_t* lines) {
+  const uint64_t k2 = (static_cast<uint64_t>(static_cast<uint32_t>(ctx.word)) << 32) | static_cast<uint32_t>(w);
+  const uint64_t k3 = (static_cast<uint64_t>(ctx.c2) << 32) | static_cast<uint32_t>(w);
+  const uint64_t k4 = (static_cast<uint64_t>(ctx.c3) << 32) | static_cast<uint32_t>(w);
+  const bool has3 = ctx.c2 != kNone;
+  const bool has4 = ctx.c3 != kNone;
+  const uint64_t b2 = bucket_of(k2, S.t2.nbuckets);
+  const uint64_t b3 = has3 ? bucket_of(k3, S.t3.nbuckets) : 0;
+  const uint64_t b4 = has4 ? bucket_of(k4, S.t4.nbuckets) : 0;
+  const Bucket q2 = load_bucket(S.t2, b2);
+  const Bucket q3 = has3 ? load_bucket(S.t3, b3) : Bucket{};
+  const Bucket q4 = has4 ? load_bucket(S.t4, b4) : Bucket{};
+  const Unigram u = S.uni[w];
+  *lines += 1u + (has3 ? 1u : 0u) + (has4 ? 1u : 0u);
+  uint32_t s2 = kNone, s3 = kNone, s4 = kNone;
+  float p2 = 0.f, bb2 = 0.f, p3 = 0.f, bb3 = 0.f, p4 = 0.f, bb4 = 0.f;
+  const bool f2 = resolve(S.t2, k2, b2, q2, &s2, &p2, &bb2, lines);
+  const bool f3 = has3 && resolve(S.t3, k3, b3, q3, &s3, &p3, &bb3, lines);
+  const bool f4 = has4 && resolve(S.t4, k4, b4, q4, &s4, &p4, &bb4, lines);
+  // log10 P(w | context) by backoff, innermost order first
+  double lp;
+  if (f4) {
+    lp = static_cast<double>(p4);
+  } else {
+    double l3;
+    if (f3) {
+      l3 = static_cast<double>(p3);
     } else {
-      double l3;
-      if (f3) {
-        l3 = static_cast<double>(p3);
-      } else {
-        const double l2 = f2 ? static_cast<double>(p2) : static_cast<double>(ctx.bo1) + static_cast<double>(u.logp);
-        l3 = static_cast<double>(ctx.bo2) + l2;
-      }
-      lp = static_cast<double>(ctx.bo3) + l3;
+      const double l2 = f2 ? static_cast<double>(p2) : static_cast<double>(ctx.bo1) + static_cast<double>(u.logp);
+      l3 = static_cast<double>(ctx.bo2) + l2;
     }
-    S.qL[q] = Lw + P.comega * lp;
-    QState st;
-    st.c2 = f2 ? s2 : kNone;
-    st.c3 = f3 ? s3 : kNone;
-    st.bo2 = f2 ? bb2 : 0.0f;
-    st.bo3 = f3 ? bb3 : 0.0f;
-    S.qS[q] = st;
+    lp = static_cast<double>(ctx.bo3) + l3;
   }
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) lines += __shfl_xor(lines, o, 64);
-  if ((threadIdx.x & 63) == 0 && lines) {
-    const uint32_t slot = ((blockIdx.x * blockDim.x + threadIdx.x) >> 6) & (kSpread - 1);
-    atomicAdd(&S.lines[slot * kSpreadStride], static_cast<unsigned long long>(lines));
-  }
+  LmResult r;
+  r.lp = lp;
+  r.st.c2 = f2 ? s2 : kNone;
+  r.st.c3 = f3 ? s3 : kNone;
+  r.st.bo2 = f2 ? bb2 : 0.0f;
+  r.st.bo3 = f3 ? bb3 : 0.0f;
+  return r;
 }
 
-// Homophone top-o (Eq. (1), App. E.3): one wavefront per completed word ranks
-// its queries by (score desc, (sub-beam, homophone) index asc), keeps o, drops
-// those more than lambda below the best, and appends word-history nodes.
-__global__ __launch_bounds__(256) void k_lmselect(const DevParams P, const DevState S, int32_t tau) {
-  const uint32_t nev = static_cast<uint32_t>(S.evq[tau & 1] >> 32);
-  const int lane = threadIdx.x & 63;
-  const uint32_t wave = (blockIdx.x * blockDim.x + threadIdx.x) >> 6;
-  const uint32_t nwaves = (gridDim.x * blockDim.x) >> 6;
+// Identity of an n-gram query group: the context of a history node (its 3-word
+// context slot if the LM has that trigram, else its 2-word context slot, else
+// its last word; the backoff weights are functions of these) and the trie
+// node of the completed word (by its first word offset, < 2^30).
+__device__ __forceinline__ unsigned long long group_key(const HistNode& ctx, uint32_t woff) {
+  const uint64_t tag = ctx.c3 != kNone ? 2u : (ctx.c2 != kNone ? 1u : 0u);
+  const uint64_t id = ctx.c3 != kNone ? ctx.c3 : (ctx.c2 != kNone ? ctx.c2 : static_cast<uint32_t>(ctx.word));
+  return (tag << 62) | (id << 30) | woff;
+}
+
+// ------------------------------------------------------------------ decoding loop
+
+// A stream's hypotheses in LDS (structure of arrays); the fields of each
+// hypothesis' trie node travel with it.
+template <int KMAX>
+struct BeamLds {
+  uint64_t key[KMAX];
+  uint64_t pkey[KMAX];
+  uint64_t tmask[KMAX];  // trie child mask, separator bit, word count << 48
+  double ab[KMAX];
+  double anb[KMAX];
+  double pt[KMAX];  // log-sum-exp(ab, anb)
+  double Lw[KMAX * kMaxSub];
+  uint32_t hist[KMAX * kMaxSub];
+  uint32_t node[KMAX];
+  uint32_t meta[KMAX];   // last symbol | number of sub-beams << 8
+  uint32_t first[KMAX];  // the trie node's first child
+  uint32_t woff[KMAX];   // the trie node's first word in trie_words
+};
+
+// Frames [tau0, min(tau1, length)) of Alg. 1 for every stream: one workgroup
+// per stream, which keeps the stream's beam in LDS from frame to frame.  Each
+// frame:
+//   * fan-out of every hypothesis by blank, repeat and each lexicon-valid
+//     symbol (trie child mask), token / word bonuses, recombination of equal
+//     prefixes by log-sum-exp, theta pruning, top-K selection (score bins,
+//     exact rank inside the boundary bin), beam update, trie-state advance;
+//     hypothesis i is owned by LPB consecutive lanes: lane s of it handles the
+//     extensions v = 1+s, 1+s+LPB, ... and lane 0 also the merged stay;
+//   * Eq. (1) for the hypotheses that completed a word: every (sub-beam,
+//     homophone) pair is scored with the 4-gram backoff LM, the pairs spread
+//     over all threads; the top-o survive lambda pruning and receive
+//     word-history nodes;
+//   * Eq. (2) with the synthetic scorer on fusion frames.
+template <int KMAX, int LPB>
+__global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const DevState S,
+                                                       const float* __restrict__ logits,
+                                                       const int32_t* __restrict__ lengths, int32_t Tc,
+                                                       int32_t tau0, int32_t tau1) {
+  constexpr int BLOCK = KMAX * LPB;
+  constexpr int HS = 2 * KMAX;  // LDS hash slots for the current prefix keys
+  constexpr int NW = BLOCK / 64;
+  constexpr int NC = (kSep + LPB - 1) / LPB;  // extension slots per lane
+  constexpr int NPM = KMAX * kMaxSub;  // (completed word, sub-beam) pairs per frame, at most
+  constexpr int SEL_BYTES = kBins * 4 + kBoundaryCap * 16;
+  constexpr int LM_BYTES = 32 * NPM + 16;
+  constexpr int UNI_BYTES = SEL_BYTES > LM_BYTES ? SEL_BYTES : LM_BYTES;
+  static_assert(20 * KMAX <= SEL_BYTES, "fusion sort scratch");
+  const int b = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int len = lengths[b];
+  const int tend = len < tau1 ? len : tau1;
+  if (tau0 >= tend) return;
+
+  __shared__ BeamLds<KMAX> sBeam[2];
+  __shared__ double sD[48];  // classes 0..40; 41..47 are zero (slots past the separator)
+  __shared__ double sAb2[KMAX], sAnb2[KMAX], sPt2[KMAX], sStay[KMAX];
+  __shared__ uint64_t sMask[KMAX];
+  __shared__ unsigned long long sHKey[HS];
+  __shared__ int32_t sHIdx[HS];
+  // top-K selection scratch; the LM step and the fusion sort reuse it
+  __shared__ __align__(16) unsigned char sSel[UNI_BYTES];
+  __shared__ double sLvHi[kMaxLevels], sLvInv[kMaxLevels];
+  __shared__ int32_t sLvBeta[kMaxLevels], sLvShift[kMaxLevels];
+  __shared__ uint32_t sSelSrc[KMAX];
+  // hypotheses that completed a word this frame
+  __shared__ uint32_t sEvBeam[KMAX], sEvSrc[KMAX], sEvWoff[KMAX], sEvH[KMAX];
+  __shared__ int32_t sNG;
+  __shared__ double sRed[2 * NW];
+  __shared__ int32_t sScan[NW];
+  __shared__ int32_t sBucket, sAbove, sBucketCnt, sBCount;
+  __shared__ unsigned long long sCnt[3];  // probed lines, completed words, LM queries
+
+  uint32_t* const sHisto = reinterpret_cast<uint32_t*>(sSel);
+  double* const sBScore = reinterpret_cast<double*>(sSel + kBins * 4);
+  uint64_t* const sBKey = reinterpret_cast<uint64_t*>(sSel + kBins * 4 + kBoundaryCap * 8);
+
+  const size_t gb = static_cast<size_t>(b) * P.K;
+  const int O = P.O;
   const bool synth = P.fusion_source == 1;
-  for (uint32_t e = wave; e < nev; e += nwaves) {
-    const Event ev = S.events[e];
-    const size_t bi = static_cast<size_t>(ev.stream) * P.K + ev.beam;
-    const int nq = static_cast<int>(ev.nsub * ev.H);
-    double tL[kMaxSub];
-    int tq[kMaxSub];
-#pragma unroll
-    for (int k = 0; k < kMaxSub; ++k) {
-      tL[k] = kNegInf;
-      tq[k] = 0x7FFFFFFF;
+  const bool fuse_frames = synth && P.fusion_interval > 0;
+  const int64_t t0 = S.t0[b];
+  const uint32_t arena0 = 1u + static_cast<uint32_t>(static_cast<uint64_t>(b) * S.arena_cap);
+
+  // ---- the stream's beam into LDS
+  int n = S.nbeam[b];
+  if (tid < n) {
+    BeamLds<KMAX>& B0 = sBeam[0];
+    const size_t g = gb + tid;
+    B0.key[tid] = S.key[g];
+    B0.pkey[tid] = S.pkey[g];
+    B0.ab[tid] = S.ab[g];
+    B0.anb[tid] = S.anb[g];
+    B0.pt[tid] = S.pt[g];
+    const uint32_t node = S.node[g];
+    const uint32_t meta = S.meta[g];
+    B0.node[tid] = node;
+    B0.meta[tid] = meta;
+    const int nsub = (meta >> 8) & 0xFF;
+    for (int j = 0; j < nsub; ++j) {
+      B0.Lw[tid * kMaxSub + j] = S.Lw[g * O + j];
+      B0.hist[tid * kMaxSub + j] = S.hist[g * O + j];
     }
-    auto insert = [&](double L, int qq) {
-#pragma unroll
-      for (int k = 0; k < kMaxSub; ++k) {
-        if (k < P.O && (L > tL[k] || (L == tL[k] && qq < tq[k]))) {
-          const double t = tL[k];
-          const int u = tq[k];
-          tL[k] = L;
-          tq[k] = qq;
-          L = t;
-          qq = u;
+    const TrieNode tn = S.trie[node];
+    B0.tmask[tid] = tn.mask;
+    B0.first[tid] = tn.first_child;
+    B0.woff[tid] = tn.word_off;
+  }
+  if (tid < 3) sCnt[tid] = 0;
+  uint32_t arena_n = S.arena_n[b];
+  uint32_t lines = 0, c_words = 0;  // per thread
+  uint64_t c_queries = 0;
+  uint64_t c_exp = 0, c_fused = 0;                  // uniform
+  double* const scrL = S.scrL + static_cast<size_t>(b) * S.scap;
+  QState* const scrS = S.scrS + static_cast<size_t>(b) * S.scap;
+  int cur = 0;
+  float dnext = tid < kClasses ? logits[(static_cast<size_t>(b) * Tc + tau0) * kClasses + tid] : 0.0f;
+  __syncthreads();
+
+  for (int tau = tau0; tau < tend; ++tau) {
+    // the thread index is made opaque to the optimizer in every frame so that
+    // values derived from it are not hoisted out of the loop (they would stay
+    // live in registers across all frames)
+    int tid = threadIdx.x;
+    asm volatile("" : "+v"(tid));
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    BeamLds<KMAX>& C = sBeam[cur];
+    BeamLds<KMAX>& N = sBeam[cur ^ 1];
+
+    // ---- the frame's scaled log-probs (the next frame's row is loaded meanwhile)
+    if (tid < kClasses) {
+      sD[tid] = P.alpha * static_cast<double>(dnext);
+      if (tau + 1 < tend) dnext = logits[(static_cast<size_t>(b) * Tc + tau + 1) * kClasses + tid];
+    } else if (tid < 48) {
+      sD[tid] = 0.0;
+    }
+    for (int s = tid; s < HS; s += BLOCK) sHKey[s] = kEmptyKey;
+    uint64_t my_key = 0, my_pkey = kNoParent;
+    double my_anb = kNegInf;
+    uint32_t my_meta = 0;
+    if (tid < n) {
+      my_key = C.key[tid];
+      my_pkey = C.pkey[tid];
+      my_anb = C.anb[tid];
+      my_meta = C.meta[tid];
+      sMask[tid] = C.tmask[tid];
+    }
+    __syncthreads();
+
+    // ---- prefix keys into an LDS hash table
+    if (tid < n) {
+      uint32_t s = static_cast<uint32_t>(my_key) & (HS - 1);
+      for (;;) {
+        const unsigned long long prev = atomicCAS(&sHKey[s], kEmptyKey, my_key);
+        if (prev == kEmptyKey) {
+          sHIdx[s] = tid;
+          break;
         }
+        s = (s + 1) & (HS - 1);
+      }
+    }
+    __syncthreads();
+
+    // ---- recombination: a hypothesis whose parent prefix is also live receives
+    // the parent's extension by its last symbol; that extension is removed from
+    // the parent's fan-out.
+    int par = -1;
+    if (tid < n && my_pkey != kNoParent) {
+      uint32_t s = static_cast<uint32_t>(my_pkey) & (HS - 1);
+      for (int probes = 0; probes < HS; ++probes) {
+        const unsigned long long k = sHKey[s];
+        if (k == kEmptyKey) break;
+        if (k == my_pkey) {
+          par = sHIdx[s];
+          break;
+        }
+        s = (s + 1) & (HS - 1);
+      }
+      if (par >= 0) atomicAnd(reinterpret_cast<unsigned long long*>(&sMask[par]), ~(1ull << (my_meta & 0xFF)));
+    }
+    __syncthreads();
+
+    // ---- stay candidates (blank-stay, repeat-stay, merged parent extension)
+    if (tid < n) {
+      const int last = my_meta & 0xFF;
+      const double ab2 = C.pt[tid] + sD[0];
+      const double rep = last ? my_anb + sD[last] : kNegInf;
+      double ext = kNegInf;
+      if (par >= 0) {
+        const double base = (last == static_cast<int>(C.meta[par] & 0xFF)) ? C.ab[par] : C.pt[par];
+        ext = (base + sD[last]) + (last == kSep ? P.gamma : P.beta);
+      }
+      // anb2 = lse(rep, ext), then pt2 = lse(ab2, anb2)
+      double x = rep, y = ext, anb2 = 0.0;
+#pragma unroll 1
+      for (int pass = 0; pass < 2; ++pass) {
+        const double l = lse2(x, y);
+        if (pass == 0) {
+          anb2 = l;
+          x = ab2;
+          y = l;
+        } else {
+          y = l;
+        }
+      }
+      const double pt2 = y;
+      sAb2[tid] = ab2;
+      sAnb2[tid] = anb2;
+      sPt2[tid] = pt2;
+      sStay[tid] = pt2 + C.Lw[tid * kMaxSub];
+    }
+    __syncthreads();
+
+    // ---- this lane's candidates: slot k is the extension by v = 1 + ln + LPB*k,
+    // plus the merged stay on lane 0; scores are recomputed in every pass (same
+    // operations, same result)
+    const int hi_ = tid / LPB;
+    const int ln = tid - hi_ * LPB;
+    const bool live = hi_ < n;
+    uint64_t c_key = 0, c_rel = 0;
+    double c_stay = kNegInf, c_ab = 0.0, c_p = 0.0, c_L = 0.0;
+    int c_rep = -1;
+    if (live) {
+      c_ab = C.ab[hi_];
+      c_p = C.pt[hi_];
+      c_L = C.Lw[hi_ * kMaxSub];
+      // slot k <-> symbol 1 + ln + LPB*k: bit LPB*k of c_rel is its mask bit
+      // (mask bits 41..47 are zero, so slots past the separator are invalid)
+      c_rel = sMask[hi_] >> (1 + ln);
+      c_rep = static_cast<int>(C.meta[hi_] & 0xFF) - 1 - ln;  // LPB*k of the repeat symbol
+      c_key = C.key[hi_];
+      if (ln == 0) c_stay = sStay[hi_];
+    }
+    // the slot of the separator on this lane (-1: none)
+    const int c_sep = ((kSep - 1 - ln) % LPB) == 0 ? (kSep - 1 - ln) / LPB : -1;
+    auto score_now = [&](int k) -> double {
+      const bool valid = (c_rel >> (LPB * k)) & 1ull;
+      const double base = (c_rep == LPB * k) ? c_ab : c_p;
+      const double sc = ((base + sD[1 + ln + LPB * k]) + (k == c_sep ? P.gamma : P.beta)) + c_L;
+      return valid ? sc : kNegInf;
+    };
+    auto key_of = [&](int v) -> uint64_t { return v == 0 ? c_key : prefix_step(c_key, v); };
+
+    double mx = c_stay, mn = c_stay != kNegInf ? c_stay : HUGE_VAL;
+#pragma unroll
+    for (int k = 0; k < NC; ++k) {
+      const double sc = score_now(k);
+      mx = fmax(mx, sc);
+      mn = fmin(mn, sc != kNegInf ? sc : HUGE_VAL);
+    }
+    double best, lowest;
+    block_minmax<BLOCK>(mx, mn, sRed, &best, &lowest);
+    const double thr = best - P.theta;
+
+    // ---- top-K.  Level 0 bins (best - score) over [max(thr, lowest), best] into
+    // kBins; the map is monotone, so bins above the one holding the K-th
+    // candidate are taken whole.  That bin is resolved exactly by rank on
+    // (score desc, key asc) when it holds at most kBoundaryCap candidates;
+    // otherwise it is re-binned over its own score range (deeper levels), and
+    // when its scores are all equal, by the bits of the key (smaller key first).
+    const double lo0 = fmax(thr, lowest);
+    const double inv0 = best > lo0 ? static_cast<double>(kBins) / (best - lo0) : 0.0;
+    const int shift0 = best > lo0 ? -1 : 64 - 10;
+    auto bin_score = [&](double hi, double inv, double s) -> int {
+      const double x = (hi - s) * inv;
+      return x >= static_cast<double>(kBins - 1) ? kBins - 1 : static_cast<int>(x);
+    };
+    auto bin0 = [&](int v, double s) -> int {
+      return shift0 < 0 ? bin_score(best, inv0, s) : static_cast<int>((key_of(v) >> shift0) & (kBins - 1));
+    };
+    // deeper levels (rare): parameters in LDS
+    auto bin_at = [&](int l, int v, double s) -> int {
+      const int sh = sLvShift[l];
+      if (sh >= 0) return static_cast<int>((key_of(v) >> sh) & (kBins - 1));
+      return bin_score(sLvHi[l], sLvInv[l], s);
+    };
+    // candidates in the boundary bin of levels 0..L-1
+    auto member = [&](int L, int v, double s) -> bool {
+      if (s < thr || bin0(v, s) != sLvBeta[0]) return false;
+      for (int l = 1; l < L; ++l)
+        if (bin_at(l, v, s) != sLvBeta[l]) return false;
+      return true;
+    };
+    // the lane's candidates with scores recomputed (no register array): for the rare levels
+    auto for_cands_rt = [&](auto&& f) {
+      if (c_stay != kNegInf) f(0, c_stay);
+#pragma unroll 1
+      for (int k = 0; k < NC; ++k) {
+        const double s = score_now(k);
+        if (s != kNegInf) f(1 + ln + LPB * k, s);
       }
     };
-    // four independent loads in flight per lane, then the insertions
-    const double* ql = S.qL + ev.qoff;
-    int q = lane;
-    for (; q + 192 < nq; q += 256) {
-      const double a0 = ql[q], a1 = ql[q + 64], a2 = ql[q + 128], a3 = ql[q + 192];
-      insert(a0, q);
-      insert(a1, q + 64);
-      insert(a2, q + 128);
-      insert(a3, q + 192);
-    }
-    for (; q < nq; q += 64) insert(ql[q], q);
-    uint32_t abase = 0;
-    if (lane == 0) abase = atomicAdd(&S.arena_n[ev.stream], static_cast<uint32_t>(P.O));
-    abase = __shfl(abase, 0, 64);
-    const bool room = static_cast<uint64_t>(abase) + P.O <= S.arena_cap;
-    if (!room && lane == 0) atomicOr(S.flags, kFlagArena);
-    const uint32_t node0 = 1u + static_cast<uint32_t>(static_cast<uint64_t>(ev.stream) * S.arena_cap) + abase;
-    double bestL = kNegInf;
-    int kept = 0;
+    // finds the bin holding the need-th candidate of sHisto; returns via sBucket/sAbove/sBucketCnt
+    auto find_bin = [&](int need_in) -> int {
+      constexpr int PER = (kBins + BLOCK - 1) / BLOCK;
+      int local = 0;
 #pragma unroll
-    for (int k = 0; k < kMaxSub; ++k) {
-      if (k >= P.O) break;
-      double bL = tL[0];
-      int bq = tq[0];
-      int bl = lane;
-#pragma unroll
-      for (int o = 32; o > 0; o >>= 1) {
-        const double oL = __shfl_xor(bL, o, 64);
-        const int oq = __shfl_xor(bq, o, 64);
-        const int ol = __shfl_xor(bl, o, 64);
-        if (oL > bL || (oL == bL && (oq < bq || (oq == bq && ol < bl)))) {
-          bL = oL;
-          bq = oq;
-          bl = ol;
-        }
+      for (int q = 0; q < PER; ++q) {
+        const int d = tid * PER + q;
+        local += d < kBins ? static_cast<int>(sHisto[d]) : 0;
       }
-      if (bL == kNegInf) break;
-      if (k == 0) bestL = bL;
-      if (bL < bestL - P.lam) break;
-      if (lane == bl) {
-        if (room) {
-          const uint32_t j = static_cast<uint32_t>(bq) / ev.H;
-          const uint32_t h = static_cast<uint32_t>(bq) - j * ev.H;
-          const int w = S.trie_words[ev.woff + h];
-          const uint32_t ph = hist_of(ev, j);
-          const QState st = S.qS[ev.qoff + bq];
-          HistNode hn;
-          hn.parent = ph;
-          hn.word = w;
-          hn.c2 = st.c2;
-          hn.c3 = st.c3;
-          hn.bo1 = S.uni[w].bo;
-          hn.bo2 = st.bo2;
-          hn.bo3 = st.bo3;
-          hn.pad = 0;
-          if (synth) {
-            const HistNode ctx = S.arena[ph];
-            hn.sfus = ctx.sfus + bigram_score(P, ctx.word, w);
-          } else {
-            hn.sfus = 0.0;
+      int tot = 0;
+      const int before = block_scan<BLOCK>(local, sScan, &tot);
+      if (need_in > 0 && before < need_in && before + local >= need_in) {
+        int acc = before;
+        for (int q = 0; q < PER; ++q) {
+          const int d = tid * PER + q;
+          const int h = static_cast<int>(sHisto[d]);
+          if (acc + h >= need_in) {
+            sBucket = d;
+            sAbove = acc;
+            sBucketCnt = h;
+            break;
           }
-          S.arena[node0 + k] = hn;
-          S.Lw[bi * P.O + k] = bL;
-          S.hist[bi * P.O + k] = node0 + k;
+          acc += h;
+        }
+      }
+      __syncthreads();
+      return tot;
+    };
+
+    // level-0 bin of each of the lane's candidates, kept packed 16 bits per slot
+    // (0xFFFF: no candidate); exact scores are recomputed only inside the boundary bin
+    uint32_t binp[(NC + 1) / 2];
+    uint32_t bin_stay = 0xFFFFu;
+    for (int d = tid; d < kBins; d += BLOCK) sHisto[d] = 0;
+    __syncthreads();
+    if (c_stay != kNegInf && c_stay >= thr) {
+      bin_stay = static_cast<uint32_t>(bin0(0, c_stay));
+      atomicAdd(&sHisto[bin_stay], 1u);
+    }
+    if (shift0 < 0) {
+#pragma unroll
+      for (int k = 0; k < NC; ++k) {
+        const double sc = score_now(k);
+        const bool in = sc >= thr;  // -inf (no candidate) is below any threshold
+        const uint32_t bn = in ? static_cast<uint32_t>(bin_score(best, inv0, sc)) : 0xFFFFu;
+        if (in) atomicAdd(&sHisto[bn], 1u);
+        if (k & 1)
+          binp[k >> 1] |= bn << 16;
+        else
+          binp[k >> 1] = bn;
+      }
+    } else {
+      // every candidate in range has the same score: bins by key bits
+#pragma unroll
+      for (int k = 0; k < NC; ++k) {
+        const double sc = score_now(k);
+        const bool in = sc >= thr;
+        const uint32_t bn = in ? static_cast<uint32_t>(bin0(1 + ln + LPB * k, sc)) : 0xFFFFu;
+        if (in) atomicAdd(&sHisto[bn], 1u);
+        if (k & 1)
+          binp[k >> 1] |= bn << 16;
+        else
+          binp[k >> 1] = bn;
+      }
+    }
+    __syncthreads();
+    const int nvalid = find_bin(P.K);
+    const bool select_all = nvalid <= P.K;
+    int beta0 = kBins, nlev = 1, need = P.K, nbc = 0;
+    bool all_bin = false;
+    if (!select_all) {
+      beta0 = sBucket;
+      need -= sAbove;
+      int cntb = sBucketCnt;
+      if (tid == 0) {
+        sLvBeta[0] = beta0;
+        sLvShift[0] = shift0;
+      }
+      __syncthreads();
+      int key_shift = shift0 >= 0 ? shift0 - 10 : 64 - 10;
+      bool key_level = shift0 >= 0;
+      while (cntb != need && cntb > kBoundaryCap && !(key_level && sLvShift[nlev - 1] == 0) && nlev < kMaxLevels) {
+        // refine: score range of the boundary bin's members, or key bits when it is flat
+        const int L = nlev;
+        double bmx = kNegInf, bmn = HUGE_VAL;
+        for_cands_rt([&](int v, double s) {
+          if (member(L, v, s)) {
+            bmx = fmax(bmx, s);
+            bmn = fmin(bmn, s);
+          }
+        });
+        double lv_hi, lv_lo;
+        block_minmax<BLOCK>(bmx, bmn, sRed, &lv_hi, &lv_lo);
+        if (tid == 0) {
+          sLvHi[L] = lv_hi;
+          sLvInv[L] = lv_hi > lv_lo ? static_cast<double>(kBins) / (lv_hi - lv_lo) : 0.0;
+          sLvShift[L] = lv_hi > lv_lo ? -1 : (key_shift > 0 ? key_shift : 0);
+        }
+        for (int d = tid; d < kBins; d += BLOCK) sHisto[d] = 0;
+        __syncthreads();
+        key_level = sLvShift[L] >= 0;
+        if (key_level) key_shift -= 10;
+        for_cands_rt([&](int v, double s) {
+          if (member(L, v, s)) atomicAdd(&sHisto[bin_at(L, v, s)], 1u);
+        });
+        __syncthreads();
+        (void)find_bin(need);
+        if (tid == 0) sLvBeta[L] = sBucket;
+        need -= sAbove;
+        cntb = sBucketCnt;
+        nlev = L + 1;
+        __syncthreads();
+      }
+      if (cntb == need) {
+        all_bin = true;
+      } else {
+        // exact rank inside the boundary bin (a flat key level of shift 0 holds one key)
+        if (tid == 0) sBCount = 0;
+        __syncthreads();
+        const int L = nlev;
+        for_cands_rt([&](int v, double s) {
+          if (!member(L, v, s)) return;
+          const int slot = atomicAdd(&sBCount, 1);
+          if (slot < kBoundaryCap) {
+            sBScore[slot] = s;
+            sBKey[slot] = key_of(v);
+          }
+        });
+        __syncthreads();
+        nbc = sBCount < kBoundaryCap ? sBCount : kBoundaryCap;
+        if (sBCount > kBoundaryCap && tid == 0) atomicOr(S.flags, kFlagSelect);
+      }
+    }
+    // selection: a candidate whose level-0 bin is above the boundary bin is
+    // taken, below it dropped; candidates inside the boundary bin (bit k of
+    // bnd: slot k, bit NC: the stay) are resolved by the deeper levels and the
+    // exact rank on (score desc, key asc)
+    uint64_t sel_bits = 0;  // bit 0: the stay, bit k+1: slot k
+    uint32_t bnd = 0;
+    auto classify = [&](uint32_t bn, int bit, int bbit) {
+      if (bn == 0xFFFFu) return;
+      if (select_all || static_cast<int>(bn) < beta0)
+        sel_bits |= 1ull << bit;
+      else if (static_cast<int>(bn) == beta0)
+        bnd |= 1u << bbit;
+    };
+    classify(bin_stay, 0, NC);
+#pragma unroll
+    for (int k = 0; k < NC; ++k) classify((binp[k >> 1] >> ((k & 1) * 16)) & 0xFFFFu, k + 1, k);
+#pragma unroll 1
+    for (uint32_t m = bnd; m; m &= m - 1) {
+      const int k = __ffs(m) - 1;
+      const int v = k == NC ? 0 : 1 + ln + LPB * k;
+      const double sc = k == NC ? c_stay : score_now(k);
+      bool take = true;
+      bool decided = false;
+      for (int l = 1; l < nlev && !decided; ++l) {
+        const int bl = bin_at(l, v, sc);
+        if (bl != sLvBeta[l]) {
+          take = bl < sLvBeta[l];
+          decided = true;
+        }
+      }
+      if (!decided && !all_bin) {
+        const uint64_t key = key_of(v);
+        int rank = 0;
+        for (int u = 0; u < nbc; ++u) rank += ranks_before(sBScore[u], sBKey[u], sc, key);
+        take = rank < need;
+      }
+      if (take) sel_bits |= 1ull << (k == NC ? 0 : k + 1);
+    }
+    int nsel = 0;
+    int wpos = block_scan<BLOCK>(__popcll(sel_bits), sScan, &nsel);
+    if (nsel > P.K) {  // cannot happen when the selection is exact; never write past K entries
+      nsel = P.K;
+      if (tid == 0) atomicOr(S.flags, kFlagSelect);
+    }
+#pragma unroll 1
+    for (uint64_t m = sel_bits; m && wpos < nsel; m &= m - 1) {
+      const int bit = __ffsll(static_cast<unsigned long long>(m)) - 1;
+      const uint32_t v = bit == 0 ? 0u : static_cast<uint32_t>(1 + ln + LPB * (bit - 1));
+      sSelSrc[wpos++] = static_cast<uint32_t>(hi_) | (v << 16);
+    }
+    __syncthreads();
+
+    // ---- the new hypotheses; an extension's trie node is fetched now and
+    // stored after the LM step
+    const int r = tid;
+    int is_event = 0;
+    uint32_t ev_src = 0, ev_woff = 0, ev_H = 0;
+    bool tn_load = false;
+    TrieNode tn{};
+    if (r < nsel) {
+      const uint32_t src = sSelSrc[r];
+      const int i = src & 0xFFFF;
+      const int v = src >> 16;
+      const uint32_t meta_i = C.meta[i];
+      const int nsub = (meta_i >> 8) & 0xFF;
+      if (v == 0) {
+        N.key[r] = C.key[i];
+        N.pkey[r] = C.pkey[i];
+        N.ab[r] = sAb2[i];
+        N.anb[r] = sAnb2[i];
+        N.pt[r] = sPt2[i];
+        N.node[r] = C.node[i];
+        N.meta[r] = meta_i;
+        N.tmask[r] = C.tmask[i];
+        N.first[r] = C.first[i];
+        N.woff[r] = C.woff[i];
+      } else {
+        const int last = meta_i & 0xFF;
+        const double base = (v == last) ? C.ab[i] : C.pt[i];
+        const double anb = (base + sD[v]) + (v == kSep ? P.gamma : P.beta);
+        const uint64_t tm = C.tmask[i];
+        N.key[r] = prefix_step(C.key[i], v);
+        N.pkey[r] = C.key[i];
+        N.ab[r] = kNegInf;
+        N.anb[r] = anb;
+        N.pt[r] = anb;  // log-sum-exp(-inf, anb)
+        uint32_t child = kRootNode;
+        if (v != kSep) child = C.first[i] + __popcll(tm & ((1ull << v) - 1ull));
+        N.node[r] = child;
+        N.meta[r] = static_cast<uint32_t>(v) | (meta_i & 0xFF00u);
+        tn = S.trie[child];
+        tn_load = true;
+        if (v == kSep) {
+          is_event = 1;
+          ev_src = static_cast<uint32_t>(i);
+          ev_woff = C.woff[i];
+          ev_H = static_cast<uint32_t>(tm >> kWordCountShift);
+        }
+      }
+      for (int j = 0; j < nsub; ++j) {
+        N.Lw[r * kMaxSub + j] = C.Lw[i * kMaxSub + j];
+        N.hist[r * kMaxSub + j] = C.hist[i * kMaxSub + j];
+      }
+    }
+    int nev = 0;
+    const int erank = block_scan<BLOCK>(is_event, sScan, &nev);
+    if (is_event) {
+      sEvBeam[erank] = static_cast<uint32_t>(r);
+      sEvSrc[erank] = ev_src;
+      sEvWoff[erank] = ev_woff;
+      sEvH[erank] = ev_H;
+    }
+
+    // ---- Eq. (1).  The queries (sub-beam j, homophone h) of the completed
+    // words are scored once per distinct group (n-gram context, completed-word
+    // node): the pairs (word e, sub-beam j) are grouped in an LDS hash table,
+    // the groups' lookups spread over all threads into the stream's scratch,
+    // and each completed word ranks its queries from there.
+    unsigned long long* const sGKey = reinterpret_cast<unsigned long long*>(sSel);
+    int32_t* const sGId = reinterpret_cast<int32_t*>(sSel + 8 * NPM);
+    int32_t* const sPairG = sGId + NPM;  // pair -> hash slot, then -> group
+    uint32_t* const sGph = reinterpret_cast<uint32_t*>(sPairG + NPM);
+    uint32_t* const sGwoff = sGph + NPM;
+    uint32_t* const sGH = sGwoff + NPM;
+    int32_t* const sGoff = reinterpret_cast<int32_t*>(sGH + NPM);  // NPM + 1 entries
+    for (int q = tid; q < NPM; q += BLOCK) sGKey[q] = kEmptyKey;
+    if (tid == 0) sNG = 0;
+    __syncthreads();
+    for (int pr = tid; pr < nev * kMaxSub; pr += BLOCK) {
+      const int e = pr / kMaxSub;
+      const int j = pr - e * kMaxSub;
+      const uint32_t i = sEvSrc[e];
+      int slot = -1;
+      if (j < static_cast<int>((C.meta[i] >> 8) & 0xFF)) {
+        const uint32_t ph = C.hist[i * kMaxSub + j];
+        const HistNode ctx = S.arena[ph];
+        const unsigned long long key = group_key(ctx, sEvWoff[e]);
+        uint32_t q = static_cast<uint32_t>(splitmix64(key)) & (NPM - 1);
+        for (;;) {
+          const unsigned long long prev = atomicCAS(&sGKey[q], kEmptyKey, key);
+          if (prev == kEmptyKey) {
+            const int g = atomicAdd(&sNG, 1);
+            sGId[q] = g;
+            sGph[g] = ph;
+            sGwoff[g] = sEvWoff[e];
+            sGH[g] = sEvH[e];
+            break;
+          }
+          if (prev == key) break;
+          q = (q + 1) & (NPM - 1);
+        }
+        slot = static_cast<int>(q);
+      }
+      sPairG[pr] = slot;
+    }
+    __syncthreads();
+    const int NG = sNG;
+    for (int pr = tid; pr < nev * kMaxSub; pr += BLOCK) {
+      const int q = sPairG[pr];
+      if (q >= 0) sPairG[pr] = sGId[q];
+    }
+    // lookup offsets of the groups
+    int U = 0;
+    {
+      constexpr int PG = (NPM + BLOCK - 1) / BLOCK;
+      int loc = 0;
+#pragma unroll
+      for (int q = 0; q < PG; ++q) {
+        const int g = tid * PG + q;
+        loc += g < NG ? static_cast<int>(sGH[g]) : 0;
+      }
+      int pre = block_scan<BLOCK>(loc, sScan, &U);
+#pragma unroll
+      for (int q = 0; q < PG; ++q) {
+        const int g = tid * PG + q;
+        if (g < NG) {
+          sGoff[g] = pre;
+          pre += static_cast<int>(sGH[g]);
+        }
+      }
+      if (tid == 0) sGoff[NG] = U;
+    }
+    if (static_cast<uint64_t>(U) > S.scap) {  // cannot happen: U <= K * O * (largest homophone set)
+      if (tid == 0) atomicOr(S.flags, kFlagSelect);
+      U = 0;
+    }
+    __syncthreads();
+    for (int u = tid; u < U; u += BLOCK) {
+      int lo = 0, hi = NG - 1;
+      while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (sGoff[mid] <= u) lo = mid; else hi = mid - 1;
+      }
+      const uint32_t h = static_cast<uint32_t>(u - sGoff[lo]);
+      const int32_t w = S.trie_words[sGwoff[lo] + h];
+      const HistNode ctx = S.arena[sGph[lo]];
+      const LmResult res = lm_lookup(S, w, ctx, &lines);
+      scrL[u] = res.lp;
+      scrS[u] = res.st;
+    }
+    __syncthreads();
+    // each completed word (one wavefront): its top-o by (score desc, j*H + h
+    // asc), lambda pruning, word-history nodes (o reserved per word, in order)
+    for (int e = wave; e < nev; e += NW) {
+      const uint32_t rr = sEvBeam[e];
+      const uint32_t i = sEvSrc[e];
+      const uint32_t H = sEvH[e];
+      const int nsub = (C.meta[i] >> 8) & 0xFF;
+      const int nq = nsub * static_cast<int>(H);
+      double tL[kMaxSub];
+      int tq[kMaxSub];
+#pragma unroll
+      for (int k = 0; k < kMaxSub; ++k) {
+        tL[k] = kNegInf;
+        tq[k] = 0x7FFFFFFF;
+      }
+      for (int q = lane; q < nq; q += 64) {
+        const uint32_t j = static_cast<uint32_t>(q) / H;
+        const uint32_t h = static_cast<uint32_t>(q) - j * H;
+        double L = C.Lw[i * kMaxSub + j] + P.comega * scrL[sGoff[sPairG[e * kMaxSub + j]] + h];
+        int qq = q;
+#pragma unroll
+        for (int k = 0; k < kMaxSub; ++k) {
+          if (k < O && (L > tL[k] || (L == tL[k] && qq < tq[k]))) {
+            const double t = tL[k];
+            const int u = tq[k];
+            tL[k] = L;
+            tq[k] = qq;
+            L = t;
+            qq = u;
+          }
+        }
+      }
+      // O rounds of wavefront arg-max; lane k keeps the k-th winner
+      double myL = kNegInf, bestL = kNegInf;
+      int myq = 0, kept = 0;
+#pragma unroll 1
+      for (int k = 0; k < O; ++k) {
+        double bL = tL[0];
+        int bq = tq[0];
+        int bl = lane;
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) {
+          const double oL = __shfl_xor(bL, o, 64);
+          const int oq = __shfl_xor(bq, o, 64);
+          const int ol = __shfl_xor(bl, o, 64);
+          if (oL > bL || (oL == bL && (oq < bq || (oq == bq && ol < bl)))) {
+            bL = oL;
+            bq = oq;
+            bl = ol;
+          }
+        }
+        if (bL == kNegInf) break;
+        if (k == 0) bestL = bL;
+        if (bL < bestL - P.lam) break;
+        if (lane == k) {
+          myL = bL;
+          myq = bq;
+        }
+        if (lane == bl) {
+#pragma unroll
+          for (int m = 0; m + 1 < kMaxSub; ++m) {
+            tL[m] = tL[m + 1];
+            tq[m] = tq[m + 1];
+          }
+          tL[kMaxSub - 1] = kNegInf;
+          tq[kMaxSub - 1] = 0x7FFFFFFF;
+        }
+        kept = k + 1;
+      }
+      const uint32_t abase = arena_n + static_cast<uint32_t>(e * O);
+      const bool room = static_cast<uint64_t>(abase) + O <= S.arena_cap;
+      if (lane < kept && room) {
+        const uint32_t j = static_cast<uint32_t>(myq) / H;
+        const uint32_t h = static_cast<uint32_t>(myq) - j * H;
+        const uint32_t ph = C.hist[i * kMaxSub + j];
+        const QState st = scrS[sGoff[sPairG[e * kMaxSub + j]] + h];
+        const int32_t w = S.trie_words[sEvWoff[e] + h];
+        HistNode hn;
+        hn.parent = ph;
+        hn.word = w;
+        hn.c2 = st.c2;
+        hn.c3 = st.c3;
+        hn.bo1 = S.uni[w].bo;
+        hn.bo2 = st.bo2;
+        hn.bo3 = st.bo3;
+        hn.pad = 0;
+        hn.sfus = 0.0;
+        if (synth) {
+          const HistNode ctx = S.arena[ph];
+          hn.sfus = ctx.sfus + bigram_score(P, ctx.word, w);
+        }
+        const uint32_t node = arena0 + abase + static_cast<uint32_t>(lane);
+        S.arena[node] = hn;
+        N.Lw[rr * kMaxSub + lane] = myL;
+        N.hist[rr * kMaxSub + lane] = node;
+      }
+      if (lane == 0) {
+        if (room)
+          N.meta[rr] = (N.meta[rr] & 0xFFu) | (static_cast<uint32_t>(kept) << 8);
+        else
+          atomicOr(S.flags, kFlagArena);
+        c_words += 1;
+        c_queries += static_cast<uint64_t>(nq);
+      }
+    }
+    arena_n += static_cast<uint32_t>(nev * O);
+    c_exp += static_cast<uint64_t>(n) * kClasses;
+    n = nsel;
+    __syncthreads();
+    if (tn_load) {
+      N.tmask[r] = tn.mask;
+      N.first[r] = tn.first_child;
+      N.woff[r] = tn.word_off;
+    }
+
+    // ---- Eq. (2) on fusion frames: the top-F hypotheses by (total desc, key
+    // asc); each sub-beam's score becomes phi * its synthetic fusion score and
+    // the sub-beams are re-ranked (stable)
+    const int64_t t = t0 + tau;
+    if (fuse_frames && t > 0 && t % P.fusion_interval == 0) {
+      double* sc = reinterpret_cast<double*>(sSel);
+      uint64_t* ky = reinterpret_cast<uint64_t*>(sSel + 8 * KMAX);
+      uint32_t* ix = reinterpret_cast<uint32_t*>(sSel + 16 * KMAX);
+      const int F = (P.fusion_top_f <= 0 || P.fusion_top_f >= n) ? n : P.fusion_top_f;
+      if (F < n) {
+        if (tid < KMAX) {
+          sc[tid] = tid < n ? N.pt[tid] + N.Lw[tid * kMaxSub] : kNegInf;
+          ky[tid] = tid < n ? N.key[tid] : ~0ull;
+          ix[tid] = tid < n ? static_cast<uint32_t>(tid) : 0u;
+        }
+        __syncthreads();
+        bitonic_sort<KMAX>(sc, ky, ix);
+      }
+      if (tid < F) {
+        const int i = F < n ? static_cast<int>(ix[tid]) : tid;
+        const int nsub = (N.meta[i] >> 8) & 0xFF;
+        double L[kMaxSub];
+        uint32_t h[kMaxSub];
+#pragma unroll
+        for (int j = 0; j < kMaxSub; ++j) {
+          if (j < nsub) {
+            h[j] = N.hist[i * kMaxSub + j];
+            L[j] = P.phi * S.arena[h[j]].sfus;
+          } else {
+            L[j] = kNegInf;
+            h[j] = 0;
+          }
+        }
+        // stable bubble sort, descending
+#pragma unroll
+        for (int pass = 0; pass < kMaxSub - 1; ++pass) {
+#pragma unroll
+          for (int j = 0; j + 1 < kMaxSub; ++j) {
+            if (j + 1 < nsub && L[j] < L[j + 1]) {
+              const double tL = L[j];
+              L[j] = L[j + 1];
+              L[j + 1] = tL;
+              const uint32_t th = h[j];
+              h[j] = h[j + 1];
+              h[j + 1] = th;
+            }
+          }
         }
 #pragma unroll
-        for (int m = 0; m + 1 < kMaxSub; ++m) {
-          tL[m] = tL[m + 1];
-          tq[m] = tq[m + 1];
+        for (int j = 0; j < kMaxSub; ++j) {
+          if (j < nsub) {
+            N.Lw[i * kMaxSub + j] = L[j];
+            N.hist[i * kMaxSub + j] = h[j];
+          }
         }
-        tL[kMaxSub - 1] = kNegInf;
-        tq[kMaxSub - 1] = 0x7FFFFFFF;
       }
-      kept = k + 1;
+      c_fused += static_cast<uint64_t>(F);
     }
-    if (lane == 0) {
-      if (room) S.meta[bi] = (S.meta[bi] & 0xFFu) | (static_cast<uint32_t>(kept) << 8);
-      unsigned long long* cn = S.counters + static_cast<size_t>(ev.stream) * kNumCounters;
-      atomicAdd(&cn[kCntWordEvents], 1ull);
-      atomicAdd(&cn[kCntLmQueries], static_cast<unsigned long long>(nq));
+    __syncthreads();
+    cur ^= 1;
+  }
+
+  // ---- the beam back to HBM
+  {
+    const BeamLds<KMAX>& E = sBeam[cur];
+    if (tid < n) {
+      const size_t g = gb + tid;
+      S.key[g] = E.key[tid];
+      S.pkey[g] = E.pkey[tid];
+      S.ab[g] = E.ab[tid];
+      S.anb[g] = E.anb[tid];
+      S.pt[g] = E.pt[tid];
+      S.node[g] = E.node[tid];
+      const uint32_t meta = E.meta[tid];
+      S.meta[g] = meta;
+      const int nsub = (meta >> 8) & 0xFF;
+      for (int j = 0; j < nsub; ++j) {
+        S.Lw[g * O + j] = E.Lw[tid * kMaxSub + j];
+        S.hist[g * O + j] = E.hist[tid * kMaxSub + j];
+      }
     }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    lines += __shfl_xor(lines, o, 64);
+    c_words += __shfl_xor(c_words, o, 64);
+    c_queries += __shfl_xor(c_queries, o, 64);
+  }
+  if (lane == 0) {
+    atomicAdd(&sCnt[0], static_cast<unsigned long long>(lines));
+    atomicAdd(&sCnt[1], static_cast<unsigned long long>(c_words));
+    atomicAdd(&sCnt[2], static_cast<unsigned long long>(c_queries));
+  }
+  __syncthreads();
+  if (tid == 0) {
+    S.nbeam[b] = n;
+    S.arena_n[b] = arena_n;
+    unsigned long long* cn = S.counters + static_cast<size_t>(b) * kNumCounters;
+    cn[kCntExpansions] += c_exp;
+    cn[kCntFrames] += static_cast<unsigned long long>(tend - tau0);
+    cn[kCntWordEvents] += sCnt[1];
+    cn[kCntLmQueries] += sCnt[2];
+    cn[kCntFused] += c_fused;
+    cn[kCntProbeLines] += sCnt[0];
   }
 }
 
@@ -1048,20 +1282,6 @@ __device__ void apply_fused(const DevParams& P, const DevState& S, int b, const 
   __syncthreads();
 }
 
-template <int BLOCK>
-__global__ __launch_bounds__(BLOCK) void k_fusion(const DevParams P, const DevState S,
-                                                  const int32_t* __restrict__ lengths, int32_t tau) {
-  const int b = blockIdx.x;
-  if (tau >= lengths[b]) return;
-  const int64_t t = S.t0[b] + tau;
-  if (t == 0 || t % P.fusion_interval != 0) return;
-  __shared__ double sc[BLOCK];
-  __shared__ uint64_t ky[BLOCK];
-  __shared__ uint32_t ix[BLOCK];
-  select_fused<BLOCK>(P, S, b, P.fusion_top_f, sc, ky, ix);
-  apply_fused<BLOCK>(P, S, b, nullptr);
-}
-
 // External scorer, step 1: per stream, the hypotheses to fuse (flag 1: a
 // fusion frame, top-F; flag 2: end of utterance, all; 0: none).
 template <int BLOCK>
@@ -1134,10 +1354,6 @@ __global__ __launch_bounds__(BLOCK) void k_output(const DevParams P, const DevSt
   __shared__ uint64_t ky[BLOCK];
   __shared__ uint32_t ix[BLOCK];
   __shared__ int32_t sScan[BLOCK / 64];
-  if (b == 0 && tid == 0) {
-    S.evq[0] = 0;
-    S.evq[1] = 0;
-  }
   if (fin && P.fusion_source == 1 && P.fusion_interval > 0) {
     select_fused<BLOCK>(P, S, b, 0, sc, ky, ix);
     apply_fused<BLOCK>(P, S, b, nullptr);
@@ -1184,6 +1400,25 @@ __global__ __launch_bounds__(BLOCK) void k_output(const DevParams P, const DevSt
 
 // ------------------------------------------------------------------ launchers
 
+// Optional start/stop events for the next decode-kernel launch.  They go into
+// the kernel's own dispatch (hipExtLaunchKernel), so their elapsed time is the
+// kernel's execution without the gaps around it.
+namespace {
+thread_local hipEvent_t g_ev_start = nullptr;
+thread_local hipEvent_t g_ev_stop = nullptr;
+}  // namespace
+
+void set_launch_events(hipEvent_t start, hipEvent_t stop) {
+  g_ev_start = start;
+  g_ev_stop = stop;
+}
+
+#define LB_LAUNCH(KERNEL, GRID, BLOCK, ST, ...)                                                  \
+  do {                                                                                         \
+    hipExtLaunchKernelGGL(KERNEL, GRID, BLOCK, 0, ST, g_ev_start, g_ev_stop, 0, __VA_ARGS__);  \
+    g_ev_start = g_ev_stop = nullptr;                                                          \
+  } while (0)
+
 hipError_t launch_build_order(int order, const int32_t* ids, const float* lp, const float* bo, int64_t count,
                               int32_t vocab, NgramTable t2, NgramTable t3, NgramTable dst, uint32_t* flags,
                               hipStream_t st) {
@@ -1203,44 +1438,26 @@ hipError_t launch_begin(const DevParams& P, const DevState& S, int32_t B, hipStr
 #define LB_DISPATCH_BLOCK(BLK, KERNEL, GRID, ...)                                           \
   do {                                                                                      \
     if ((BLK) == 64)                                                                        \
-      hipLaunchKernelGGL(KERNEL<64>, dim3(GRID), dim3(64), 0, st, __VA_ARGS__);             \
+      LB_LAUNCH(KERNEL<64>, dim3(GRID), dim3(64), st, __VA_ARGS__);                         \
     else if ((BLK) == 128)                                                                  \
-      hipLaunchKernelGGL(KERNEL<128>, dim3(GRID), dim3(128), 0, st, __VA_ARGS__);           \
+      LB_LAUNCH(KERNEL<128>, dim3(GRID), dim3(128), st, __VA_ARGS__);                       \
     else                                                                                    \
-      hipLaunchKernelGGL(KERNEL<256>, dim3(GRID), dim3(256), 0, st, __VA_ARGS__);           \
+      LB_LAUNCH(KERNEL<256>, dim3(GRID), dim3(256), st, __VA_ARGS__);                       \
   } while (0)
 
-// Frame-kernel shapes: (hypotheses per workgroup, lanes per hypothesis).
-hipError_t launch_frame(int K, const DevParams& P, const DevState& S, const float* logits,
-                        const int32_t* lengths, int32_t B, int32_t Tc, int32_t tau, hipStream_t st) {
+// Decode-kernel shapes: (hypotheses per workgroup, lanes per hypothesis).
+hipError_t launch_decode(int K, const DevParams& P, const DevState& S, const float* logits,
+                         const int32_t* lengths, int32_t B, int32_t Tc, int32_t tau0, int32_t tau1, hipStream_t st) {
   if (K <= 16)
-    hipLaunchKernelGGL((k_frame<16, 4>), dim3(B), dim3(64), 0, st, P, S, logits, lengths, Tc, tau);
+    LB_LAUNCH((k_decode<16, 4>), dim3(B), dim3(64), st, P, S, logits, lengths, Tc, tau0, tau1);
   else if (K <= 32)
-    hipLaunchKernelGGL((k_frame<32, 4>), dim3(B), dim3(128), 0, st, P, S, logits, lengths, Tc, tau);
+    LB_LAUNCH((k_decode<32, 4>), dim3(B), dim3(128), st, P, S, logits, lengths, Tc, tau0, tau1);
   else if (K <= 64)
-    hipLaunchKernelGGL((k_frame<64, 4>), dim3(B), dim3(256), 0, st, P, S, logits, lengths, Tc, tau);
+    LB_LAUNCH((k_decode<64, 4>), dim3(B), dim3(256), st, P, S, logits, lengths, Tc, tau0, tau1);
   else if (K <= 128)
-    hipLaunchKernelGGL((k_frame<128, LB_LPB_LARGE>), dim3(B), dim3(128 * LB_LPB_LARGE), 0, st, P, S, logits, lengths,
-                       Tc, tau);
+    LB_LAUNCH((k_decode<128, 4>), dim3(B), dim3(512), st, P, S, logits, lengths, Tc, tau0, tau1);
   else
-    hipLaunchKernelGGL((k_frame<256, LB_LPB_LARGE>), dim3(B), dim3(256 * LB_LPB_LARGE), 0, st, P, S, logits, lengths,
-                       Tc, tau);
-  return hipGetLastError();
-}
-
-hipError_t launch_lmquery(int grid, const DevParams& P, const DevState& S, int32_t tau, hipStream_t st) {
-  hipLaunchKernelGGL(k_lmquery, dim3(grid), dim3(256), 0, st, P, S, tau);
-  return hipGetLastError();
-}
-
-hipError_t launch_lmselect(int grid, const DevParams& P, const DevState& S, int32_t tau, hipStream_t st) {
-  hipLaunchKernelGGL(k_lmselect, dim3(grid), dim3(256), 0, st, P, S, tau);
-  return hipGetLastError();
-}
-
-hipError_t launch_fusion(int block, const DevParams& P, const DevState& S, const int32_t* lengths, int32_t B,
-                         int32_t tau, hipStream_t st) {
-  LB_DISPATCH_BLOCK(block, k_fusion, B, P, S, lengths, tau);
+    LB_LAUNCH((k_decode<256, 2>), dim3(B), dim3(512), st, P, S, logits, lengths, Tc, tau0, tau1);
   return hipGetLastError();
 }
 

@@ -7,16 +7,16 @@
 
 namespace lb {
 
+// Events recorded at the start and end of the next decode-kernel launch on this
+// host thread (null: none).
+void set_launch_events(hipEvent_t start, hipEvent_t stop);
+
 hipError_t launch_build_order(int order, const int32_t* ids, const float* lp, const float* bo, int64_t count,
                               int32_t vocab, NgramTable t2, NgramTable t3, NgramTable dst, uint32_t* flags,
                               hipStream_t st);
 hipError_t launch_begin(const DevParams& P, const DevState& S, int32_t B, hipStream_t st);
-hipError_t launch_frame(int K, const DevParams& P, const DevState& S, const float* logits,
-                        const int32_t* lengths, int32_t B, int32_t Tc, int32_t tau, hipStream_t st);
-hipError_t launch_lmquery(int grid, const DevParams& P, const DevState& S, int32_t tau, hipStream_t st);
-hipError_t launch_lmselect(int grid, const DevParams& P, const DevState& S, int32_t tau, hipStream_t st);
-hipError_t launch_fusion(int block, const DevParams& P, const DevState& S, const int32_t* lengths, int32_t B,
-                         int32_t tau, hipStream_t st);
+hipError_t launch_decode(int K, const DevParams& P, const DevState& S, const float* logits,
+                         const int32_t* lengths, int32_t B, int32_t Tc, int32_t tau0, int32_t tau1, hipStream_t st);
 hipError_t launch_fuse_select(int block, const DevParams& P, const DevState& S, const int32_t* flag, int32_t B,
                               hipStream_t st);
 hipError_t launch_fuse_export(int block, const DevParams& P, const DevState& S, int32_t* words, int32_t* n_words,
