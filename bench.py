@@ -40,7 +40,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="c4")
     ap.add_argument("--cpu-sample", type=int, default=0,
-                    help="utterances decoded by the CPU oracle (0 = one per host thread, max 16)")
+                    help="utterances decoded by the CPU oracle (0 = four per host thread, at most 16 threads)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true", help="skip per-kernel event timing")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -68,13 +68,47 @@ def copy_calibration(mib: int) -> None:
                       "ms": ms, "GBps_read_plus_write": 2 * n * 4 / (ms * 1e-3) / 1e9}), flush=True)
 
 
+def kernel_source_hash() -> str:
+    """sha256 over the device sources; a traffic figure is valid only for the
+    kernel it was measured on."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("lb_kernels.hip", "lb_device.h"):
+        with open(os.path.join(ROOT, "paper_2603_14002_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per k_decode launch from the committed rocprofv3 summary
+    (FETCH_SIZE and WRITE_SIZE, each scaled by what the counter reads for a
+    plain copy), or None when there is none for this workload or the kernel
+    sources changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", f"k_decode_{workload}.md")
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    with open(path) as fh:
+        for line in fh:
+            if line.startswith("- ") and ": " in line:
+                k, v = line[2:].split(": ", 1)
+                vals[k.strip("` ")] = v.strip().strip("`")
+    if vals.get("kernel_source_sha256") != kernel_source_hash():
+        return None
+    try:
+        return float(vals["traffic_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
 def algorithmic_bytes(s, B, T, p, lp):
     """Bytes the method itself moves in the counted work (all launches of the
     pass): the logits once, a 16-B trie node per 41 expansions, the beam state
     read and written once per call, per n-gram query the probed 64-B bucket
-    lines plus the unigram entry (8 B), the word id (4 B) and the parent's
-    32-B history node, and a 32-B history node written per kept word (at most
-    o per completed word)."""
+    lines plus the unigram entry (8 B), the word id (4 B) and the context's
+    40-B history node, counted per lookup (the queries of a stream-frame that
+    share context and word are looked up once), and a 40-B history node
+    written per kept word (at most o per completed word)."""
     state = 48 + 12 * p.subbeams          # key, pkey, a_b, a_nb, total, node, meta + o x (L, hist)
     calls = max(1, int(s.launches[0]))
     parts = {
@@ -82,8 +116,8 @@ def algorithmic_bytes(s, B, T, p, lp):
         "trie": float(s.expansions) * 16.0 / 41.0,
         "state": 2.0 * calls * B * p.beam * state,
         "ngram_lines": float(s.probe_lines) * LINE_BYTES,
-        "ngram_other": float(s.lm_queries) * (8 + 4 + 32),
-        "history_nodes": float(s.word_events) * p.subbeams * 32.0,
+        "ngram_other": float(s.lm_lookups) * (8 + 4 + 40),
+        "history_nodes": float(s.word_events) * p.subbeams * 40.0,
     }
     parts["total"] = sum(parts.values())
     return parts
@@ -221,7 +255,7 @@ def main():
         avg_us = 1000.0 * sp.kernel_ms[i] / max(1, sp.timed[i])
         alg = {k: v / nl for k, v in algorithmic_bytes(sp, B, T, p, lp).items()}
         roof = dict(kernel="k_decode", bound="hbm", achieved=alg["total"] / (avg_us * 1e-6) / 1e9,
-                    peak=HBM_PEAK_GBS, unit="GB/s", frac=None, traffic=None,
+                    peak=HBM_PEAK_GBS, unit="GB/s", frac=None, traffic=measured_traffic(wl.name),
                     bytes_per_launch=alg, avg_launch_us=avg_us, launches=nl,
                     timing="start/stop events carried by each k_decode dispatch (hipExtLaunchKernel), "
                            "a second pass of the same steps",
@@ -249,13 +283,14 @@ def main():
         else (ms / 1000.0) / len(chunks) / (chunk * FRAME_SECONDS),
         "counters": {"expansions_per_step": exp_per_step, "word_events_per_step": s.word_events / args.steps,
                      "lm_queries_per_step": s.lm_queries / args.steps, "fused_per_step": s.fused / args.steps,
+                     "lm_lookups_per_step": s.lm_lookups / args.steps,
                      "probe_lines_per_step": s.probe_lines / args.steps},
         "kernels": kern,
         "roofline": roof,
     }
     if not args.no_cpu_baseline:
         threads = min(os.cpu_count() or 1, 16)
-        n = args.cpu_sample or threads
+        n = args.cpu_sample or 4 * threads
         out["cpu_baseline"] = cpu_baseline(d, min(n, B), threads)
     dec.close()
     print(json.dumps(out), flush=True)

@@ -65,7 +65,7 @@ class lb_params(ctypes.Structure):
 class lb_stats(ctypes.Structure):
     _fields_ = [("expansions", ctypes.c_int64), ("word_events", ctypes.c_int64),
                 ("lm_queries", ctypes.c_int64), ("fused", ctypes.c_int64), ("frames", ctypes.c_int64),
-                ("probe_lines", ctypes.c_int64),
+                ("probe_lines", ctypes.c_int64), ("lm_lookups", ctypes.c_int64),
                 ("launches", ctypes.c_int64 * 8), ("kernel_ms", ctypes.c_double * 8),
                 ("timed", ctypes.c_int64 * 8)]
 

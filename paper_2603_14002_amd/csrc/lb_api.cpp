@@ -16,6 +16,11 @@
 
 using namespace lb;
 
+static_assert(sizeof(lb_params) == 128, "lb_params layout");
+static_assert(sizeof(lb_ngram_desc) == 144, "lb_ngram_desc layout");
+static_assert(sizeof(lb_lexicon_desc) == 24, "lb_lexicon_desc layout");
+static_assert(sizeof(lb_stats) == 248, "lb_stats layout");
+
 namespace {
 
 thread_local std::string g_err;
@@ -601,6 +606,7 @@ lb_status lb_get_stats(lb_decoder* d, lb_stats* out) {
     out->fused += static_cast<int64_t>(x[kCntFused]);
     out->frames += static_cast<int64_t>(x[kCntFrames]);
     out->probe_lines += static_cast<int64_t>(x[kCntProbeLines]);
+    out->lm_lookups += static_cast<int64_t>(x[kCntLookups]);
   }
   d->harvest();
   for (int k = 0; k < kKinds; ++k) {

@@ -48,7 +48,7 @@ constexpr uint32_t kFlagBuildFull = 64u;
 
 // per-stream counters (DevState::counters, [max_batch][kNumCounters])
 enum { kCntExpansions = 0, kCntWordEvents = 1, kCntLmQueries = 2, kCntFused = 3, kCntFrames = 4,
-       kCntProbeLines = 5, kNumCounters = 6 };
+       kCntProbeLines = 5, kCntLookups = 6, kNumCounters = 7 };
 
 struct TrieNode {
   uint64_t mask;

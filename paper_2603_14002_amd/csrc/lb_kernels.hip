@@ -25,16 +25,26 @@ constexpr int kMaxLevels = 16;      // refinement levels of the top-K selection
 
 // ------------------------------------------------------------------ block helpers
 
+// Workgroup barrier that orders LDS only: it waits for the wave's LDS
+// operations, not for its outstanding global loads and stores (those are
+// waited for where their registers are used, and by a full __syncthreads
+// where global memory is handed between threads).
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 template <int BLOCK>
 __device__ inline double block_max(double v, double* red) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v = fmax(v, __shfl_xor(v, o, 64));
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
-  __syncthreads();
+  lds_barrier();
   double r = red[0];
 #pragma unroll
   for (int k = 1; k < BLOCK / 64; ++k) r = fmax(r, red[k]);
-  __syncthreads();
+  lds_barrier();
   return r;
 }
 
@@ -51,14 +61,14 @@ __device__ inline void block_minmax(double mx, double mn, double* red, double* o
     red[threadIdx.x >> 6] = mx;
     red[NW + (threadIdx.x >> 6)] = mn;
   }
-  __syncthreads();
+  lds_barrier();
   double a = red[0], c = red[NW];
 #pragma unroll
   for (int k = 1; k < NW; ++k) {
     a = fmax(a, red[k]);
     c = fmin(c, red[NW + k]);
   }
-  __syncthreads();
+  lds_barrier();
   *out_max = a;
   *out_min = c;
 }
@@ -75,7 +85,7 @@ __device__ inline int block_scan(int v, int* red, int* total) {
     if (lane >= o) x += y;
   }
   if (lane == 63) red[w] = x;
-  __syncthreads();
+  lds_barrier();
   int base = 0, tot = 0;
 #pragma unroll
   for (int k = 0; k < BLOCK / 64; ++k) {
@@ -83,7 +93,7 @@ __device__ inline int block_scan(int v, int* red, int* total) {
     base += (k < w) ? t : 0;
     tot += t;
   }
-  __syncthreads();
+  lds_barrier();
   *total = tot;
   return base + x - v;
 }
@@ -117,7 +127,7 @@ __device__ inline void bitonic_sort(double* sc, uint64_t* ky, uint32_t* val) {
           val[ixj] = vv;
         }
       }
-      __syncthreads();
+      lds_barrier();
     }
   }
 }
@@ -460,12 +470,12 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
   uint32_t arena_n = S.arena_n[b];
   uint32_t lines = 0, c_words = 0;  // per thread
   uint64_t c_queries = 0;
-  uint64_t c_exp = 0, c_fused = 0;                  // uniform
+  uint64_t c_exp = 0, c_fused = 0, c_lookups = 0;  // uniform
   double* const scrL = S.scrL + static_cast<size_t>(b) * S.scap;
   QState* const scrS = S.scrS + static_cast<size_t>(b) * S.scap;
   int cur = 0;
   float dnext = tid < kClasses ? logits[(static_cast<size_t>(b) * Tc + tau0) * kClasses + tid] : 0.0f;
-  __syncthreads();
+  lds_barrier();
 
   for (int tau = tau0; tau < tend; ++tau) {
     // the thread index is made opaque to the optimizer in every frame so that
@@ -496,7 +506,7 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
       my_meta = C.meta[tid];
       sMask[tid] = C.tmask[tid];
     }
-    __syncthreads();
+    lds_barrier();
 
     // ---- prefix keys into an LDS hash table
     if (tid < n) {
@@ -510,7 +520,7 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
         s = (s + 1) & (HS - 1);
       }
     }
-    __syncthreads();
+    lds_barrier();
 
     // ---- recombination: a hypothesis whose parent prefix is also live receives
     // the parent's extension by its last symbol; that extension is removed from
@@ -529,7 +539,7 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
       }
       if (par >= 0) atomicAnd(reinterpret_cast<unsigned long long*>(&sMask[par]), ~(1ull << (my_meta & 0xFF)));
     }
-    __syncthreads();
+    lds_barrier();
 
     // ---- stay candidates (blank-stay, repeat-stay, merged parent extension)
     if (tid < n) {
@@ -560,7 +570,7 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
       sPt2[tid] = pt2;
       sStay[tid] = pt2 + C.Lw[tid * kMaxSub];
     }
-    __syncthreads();
+    lds_barrier();
 
     // ---- this lane's candidates: slot k is the extension by v = 1 + ln + LPB*k,
     // plus the merged stay on lane 0; scores are recomputed in every pass (same
@@ -666,7 +676,7 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
           acc += h;
         }
       }
-      __syncthreads();
+      lds_barrier();
       return tot;
     };
 
@@ -675,7 +685,7 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
     uint32_t binp[(NC + 1) / 2];
     uint32_t bin_stay = 0xFFFFu;
     for (int d = tid; d < kBins; d += BLOCK) sHisto[d] = 0;
-    __syncthreads();
+    lds_barrier();
     if (c_stay != kNegInf && c_stay >= thr) {
       bin_stay = static_cast<uint32_t>(bin0(0, c_stay));
       atomicAdd(&sHisto[bin_stay], 1u);
@@ -706,7 +716,7 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
           binp[k >> 1] = bn;
       }
     }
-    __syncthreads();
+    lds_barrier();
     const int nvalid = find_bin(P.K);
     const bool select_all = nvalid <= P.K;
     int beta0 = kBins, nlev = 1, need = P.K, nbc = 0;
@@ -719,7 +729,7 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
         sLvBeta[0] = beta0;
         sLvShift[0] = shift0;
       }
-      __syncthreads();
+      lds_barrier();
       int key_shift = shift0 >= 0 ? shift0 - 10 : 64 - 10;
       bool key_level = shift0 >= 0;
       while (cntb != need && cntb > kBoundaryCap && !(key_level && sLvShift[nlev - 1] == 0) && nlev < kMaxLevels) {
@@ -740,26 +750,26 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
           sLvShift[L] = lv_hi > lv_lo ? -1 : (key_shift > 0 ? key_shift : 0);
         }
         for (int d = tid; d < kBins; d += BLOCK) sHisto[d] = 0;
-        __syncthreads();
+        lds_barrier();
         key_level = sLvShift[L] >= 0;
         if (key_level) key_shift -= 10;
         for_cands_rt([&](int v, double s) {
           if (member(L, v, s)) atomicAdd(&sHisto[bin_at(L, v, s)], 1u);
         });
-        __syncthreads();
+        lds_barrier();
         (void)find_bin(need);
         if (tid == 0) sLvBeta[L] = sBucket;
         need -= sAbove;
         cntb = sBucketCnt;
         nlev = L + 1;
-        __syncthreads();
+        lds_barrier();
       }
       if (cntb == need) {
         all_bin = true;
       } else {
         // exact rank inside the boundary bin (a flat key level of shift 0 holds one key)
         if (tid == 0) sBCount = 0;
-        __syncthreads();
+        lds_barrier();
         const int L = nlev;
         for_cands_rt([&](int v, double s) {
           if (!member(L, v, s)) return;
@@ -769,7 +779,7 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
             sBKey[slot] = key_of(v);
           }
         });
-        __syncthreads();
+        lds_barrier();
         nbc = sBCount < kBoundaryCap ? sBCount : kBoundaryCap;
         if (sBCount > kBoundaryCap && tid == 0) atomicOr(S.flags, kFlagSelect);
       }
@@ -824,7 +834,7 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
       const uint32_t v = bit == 0 ? 0u : static_cast<uint32_t>(1 + ln + LPB * (bit - 1));
       sSelSrc[wpos++] = static_cast<uint32_t>(hi_) | (v << 16);
     }
-    __syncthreads();
+    lds_barrier();
 
     // ---- the new hypotheses; an extension's trie node is fetched now and
     // stored after the LM step
@@ -901,7 +911,7 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
     int32_t* const sGoff = reinterpret_cast<int32_t*>(sGH + NPM);  // NPM + 1 entries
     for (int q = tid; q < NPM; q += BLOCK) sGKey[q] = kEmptyKey;
     if (tid == 0) sNG = 0;
-    __syncthreads();
+    lds_barrier();
     for (int pr = tid; pr < nev * kMaxSub; pr += BLOCK) {
       const int e = pr / kMaxSub;
       const int j = pr - e * kMaxSub;
@@ -929,7 +939,7 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
       }
       sPairG[pr] = slot;
     }
-    __syncthreads();
+    lds_barrier();
     const int NG = sNG;
     for (int pr = tid; pr < nev * kMaxSub; pr += BLOCK) {
       const int q = sPairG[pr];
@@ -960,7 +970,8 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
       if (tid == 0) atomicOr(S.flags, kFlagSelect);
       U = 0;
     }
-    __syncthreads();
+    c_lookups += static_cast<uint64_t>(U);
+    lds_barrier();
     for (int u = tid; u < U; u += BLOCK) {
       int lo = 0, hi = NG - 1;
       while (lo < hi) {
@@ -974,7 +985,7 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
       scrL[u] = res.lp;
       scrS[u] = res.st;
     }
-    __syncthreads();
+    __syncthreads();  // the lookup results (global memory) are read by other threads
     // each completed word (one wavefront): its top-o by (score desc, j*H + h
     // asc), lambda pruning, word-history nodes (o reserved per word, in order)
     for (int e = wave; e < nev; e += NW) {
@@ -990,11 +1001,7 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
         tL[k] = kNegInf;
         tq[k] = 0x7FFFFFFF;
       }
-      for (int q = lane; q < nq; q += 64) {
-        const uint32_t j = static_cast<uint32_t>(q) / H;
-        const uint32_t h = static_cast<uint32_t>(q) - j * H;
-        double L = C.Lw[i * kMaxSub + j] + P.comega * scrL[sGoff[sPairG[e * kMaxSub + j]] + h];
-        int qq = q;
+      auto insert = [&](double L, int qq) {
 #pragma unroll
         for (int k = 0; k < kMaxSub; ++k) {
           if (k < O && (L > tL[k] || (L == tL[k] && qq < tq[k]))) {
@@ -1006,6 +1013,22 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
             qq = u;
           }
         }
+      };
+      // sub-beam by sub-beam; a group's results are contiguous in the scratch
+#pragma unroll 1
+      for (int j = 0; j < nsub; ++j) {
+        const double Lw = C.Lw[i * kMaxSub + j];
+        const double* lp = scrL + sGoff[sPairG[e * kMaxSub + j]];
+        const int q0 = j * static_cast<int>(H);
+        int h = lane;
+        for (; h + 192 < static_cast<int>(H); h += 256) {
+          const double a0 = lp[h], a1 = lp[h + 64], a2 = lp[h + 128], a3 = lp[h + 192];
+          insert(Lw + P.comega * a0, q0 + h);
+          insert(Lw + P.comega * a1, q0 + h + 64);
+          insert(Lw + P.comega * a2, q0 + h + 128);
+          insert(Lw + P.comega * a3, q0 + h + 192);
+        }
+        for (; h < static_cast<int>(H); h += 64) insert(Lw + P.comega * lp[h], q0 + h);
       }
       // O rounds of wavefront arg-max; lane k keeps the k-th winner
       double myL = kNegInf, bestL = kNegInf;
@@ -1083,7 +1106,7 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
     arena_n += static_cast<uint32_t>(nev * O);
     c_exp += static_cast<uint64_t>(n) * kClasses;
     n = nsel;
-    __syncthreads();
+    __syncthreads();  // history nodes (global memory) are read by the fusion and the next frame
     if (tn_load) {
       N.tmask[r] = tn.mask;
       N.first[r] = tn.first_child;
@@ -1105,7 +1128,7 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
           ky[tid] = tid < n ? N.key[tid] : ~0ull;
           ix[tid] = tid < n ? static_cast<uint32_t>(tid) : 0u;
         }
-        __syncthreads();
+        lds_barrier();
         bitonic_sort<KMAX>(sc, ky, ix);
       }
       if (tid < F) {
@@ -1148,7 +1171,7 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
       }
       c_fused += static_cast<uint64_t>(F);
     }
-    __syncthreads();
+    lds_barrier();
     cur ^= 1;
   }
 
@@ -1194,6 +1217,7 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
     cn[kCntLmQueries] += sCnt[2];
     cn[kCntFused] += c_fused;
     cn[kCntProbeLines] += sCnt[0];
+    cn[kCntLookups] += c_lookups;
   }
 }
 

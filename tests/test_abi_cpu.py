@@ -34,7 +34,7 @@ def test_struct_sizes_match_header_layout():
     assert ctypes.sizeof(lbm.lb_params) == 128
     assert ctypes.sizeof(lbm.lb_ngram_desc) == 144
     assert ctypes.sizeof(lbm.lb_lexicon_desc) == 24
-    assert ctypes.sizeof(lbm.lb_stats) == 240
+    assert ctypes.sizeof(lbm.lb_stats) == 248
 
 
 def _descs():
