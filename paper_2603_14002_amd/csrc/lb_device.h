@@ -86,10 +86,13 @@ struct HistNode {
   double sfus;
 };
 
-// n-gram state after a queried word: slots of its 2- and 3-word contexts and their backoffs.
+// n-gram state after a queried word: slots of its 2- and 3-word contexts and
+// their backoffs, the word and its unigram backoff.
 struct QState {
   uint32_t c2, c3;
   float bo2, bo3;
+  int32_t w;
+  float bo1;
 };
 
 struct DevParams {

@@ -343,6 +343,8 @@ __device__ __forceinline__ LmResult lm_lookup(const DevState& S, int32_t w, cons
   r.st.c3 = f3 ? s3 : kNone;
   r.st.bo2 = f2 ? bb2 : 0.0f;
   r.st.bo3 = f3 ? bb3 : 0.0f;
+  r.st.w = w;
+  r.st.bo1 = u.bo;
   return r;
 }
 
@@ -635,22 +637,6 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
       if (sh >= 0) return static_cast<int>((key_of(v) >> sh) & (kBins - 1));
       return bin_score(sLvHi[l], sLvInv[l], s);
     };
-    // candidates in the boundary bin of levels 0..L-1
-    auto member = [&](int L, int v, double s) -> bool {
-      if (s < thr || bin0(v, s) != sLvBeta[0]) return false;
-      for (int l = 1; l < L; ++l)
-        if (bin_at(l, v, s) != sLvBeta[l]) return false;
-      return true;
-    };
-    // the lane's candidates with scores recomputed (no register array): for the rare levels
-    auto for_cands_rt = [&](auto&& f) {
-      if (c_stay != kNegInf) f(0, c_stay);
-#pragma unroll 1
-      for (int k = 0; k < NC; ++k) {
-        const double s = score_now(k);
-        if (s != kNegInf) f(1 + ln + LPB * k, s);
-      }
-    };
     // finds the bin holding the need-th candidate of sHisto; returns via sBucket/sAbove/sBucketCnt
     auto find_bin = [&](int need_in) -> int {
       constexpr int PER = (kBins + BLOCK - 1) / BLOCK;
@@ -719,10 +705,37 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
     lds_barrier();
     const int nvalid = find_bin(P.K);
     const bool select_all = nvalid <= P.K;
-    int beta0 = kBins, nlev = 1, need = P.K, nbc = 0;
+    int beta0 = select_all ? kBins : sBucket, nlev = 1, need = P.K, nbc = 0;
     bool all_bin = false;
+    // level 0 decides every candidate outside the boundary bin: above it taken,
+    // below it dropped; bnd marks this lane's candidates inside it (bit k: slot
+    // k, bit NC: the stay)
+    uint64_t sel_bits = 0;  // bit 0: the stay, bit k+1: slot k
+    uint32_t bnd = 0;
+    auto classify = [&](uint32_t bn, int bit, int bbit) {
+      if (bn == 0xFFFFu) return;
+      if (static_cast<int>(bn) < beta0)
+        sel_bits |= 1ull << bit;
+      else if (static_cast<int>(bn) == beta0)
+        bnd |= 1u << bbit;
+    };
+    classify(bin_stay, 0, NC);
+#pragma unroll
+    for (int k = 0; k < NC; ++k) classify((binp[k >> 1] >> ((k & 1) * 16)) & 0xFFFFu, k + 1, k);
+    // the lane's boundary-bin candidates (v, exact score) that also lie in the
+    // boundary bins of levels 1..L-1
+    auto for_bnd = [&](int L, auto&& f) {
+#pragma unroll 1
+      for (uint32_t m = bnd; m; m &= m - 1) {
+        const int k = __ffs(m) - 1;
+        const int v = k == NC ? 0 : 1 + ln + LPB * k;
+        const double sc = k == NC ? c_stay : score_now(k);
+        bool in = true;
+        for (int l = 1; l < L && in; ++l) in = bin_at(l, v, sc) == sLvBeta[l];
+        if (in) f(k, v, sc);
+      }
+    };
     if (!select_all) {
-      beta0 = sBucket;
       need -= sAbove;
       int cntb = sBucketCnt;
       if (tid == 0) {
@@ -736,11 +749,9 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
         // refine: score range of the boundary bin's members, or key bits when it is flat
         const int L = nlev;
         double bmx = kNegInf, bmn = HUGE_VAL;
-        for_cands_rt([&](int v, double s) {
-          if (member(L, v, s)) {
-            bmx = fmax(bmx, s);
-            bmn = fmin(bmn, s);
-          }
+        for_bnd(L, [&](int, int, double sc) {
+          bmx = fmax(bmx, sc);
+          bmn = fmin(bmn, sc);
         });
         double lv_hi, lv_lo;
         block_minmax<BLOCK>(bmx, bmn, sRed, &lv_hi, &lv_lo);
@@ -753,9 +764,7 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
         lds_barrier();
         key_level = sLvShift[L] >= 0;
         if (key_level) key_shift -= 10;
-        for_cands_rt([&](int v, double s) {
-          if (member(L, v, s)) atomicAdd(&sHisto[bin_at(L, v, s)], 1u);
-        });
+        for_bnd(L, [&](int, int v, double sc) { atomicAdd(&sHisto[bin_at(L, v, sc)], 1u); });
         lds_barrier();
         (void)find_bin(need);
         if (tid == 0) sLvBeta[L] = sBucket;
@@ -770,12 +779,10 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
         // exact rank inside the boundary bin (a flat key level of shift 0 holds one key)
         if (tid == 0) sBCount = 0;
         lds_barrier();
-        const int L = nlev;
-        for_cands_rt([&](int v, double s) {
-          if (!member(L, v, s)) return;
+        for_bnd(nlev, [&](int, int v, double sc) {
           const int slot = atomicAdd(&sBCount, 1);
           if (slot < kBoundaryCap) {
-            sBScore[slot] = s;
+            sBScore[slot] = sc;
             sBKey[slot] = key_of(v);
           }
         });
@@ -784,22 +791,8 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
         if (sBCount > kBoundaryCap && tid == 0) atomicOr(S.flags, kFlagSelect);
       }
     }
-    // selection: a candidate whose level-0 bin is above the boundary bin is
-    // taken, below it dropped; candidates inside the boundary bin (bit k of
-    // bnd: slot k, bit NC: the stay) are resolved by the deeper levels and the
-    // exact rank on (score desc, key asc)
-    uint64_t sel_bits = 0;  // bit 0: the stay, bit k+1: slot k
-    uint32_t bnd = 0;
-    auto classify = [&](uint32_t bn, int bit, int bbit) {
-      if (bn == 0xFFFFu) return;
-      if (select_all || static_cast<int>(bn) < beta0)
-        sel_bits |= 1ull << bit;
-      else if (static_cast<int>(bn) == beta0)
-        bnd |= 1u << bbit;
-    };
-    classify(bin_stay, 0, NC);
-#pragma unroll
-    for (int k = 0; k < NC; ++k) classify((binp[k >> 1] >> ((k & 1) * 16)) & 0xFFFFu, k + 1, k);
+    // the boundary bin's candidates: the deeper levels, then the exact rank on
+    // (score desc, key asc)
 #pragma unroll 1
     for (uint32_t m = bnd; m; m &= m - 1) {
       const int k = __ffs(m) - 1;
@@ -1014,21 +1007,23 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
           }
         }
       };
-      // sub-beam by sub-beam; a group's results are contiguous in the scratch
-#pragma unroll 1
-      for (int j = 0; j < nsub; ++j) {
-        const double Lw = C.Lw[i * kMaxSub + j];
-        const double* lp = scrL + sGoff[sPairG[e * kMaxSub + j]];
-        const int q0 = j * static_cast<int>(H);
-        int h = lane;
-        for (; h + 192 < static_cast<int>(H); h += 256) {
-          const double a0 = lp[h], a1 = lp[h + 64], a2 = lp[h + 128], a3 = lp[h + 192];
-          insert(Lw + P.comega * a0, q0 + h);
-          insert(Lw + P.comega * a1, q0 + h + 64);
-          insert(Lw + P.comega * a2, q0 + h + 128);
-          insert(Lw + P.comega * a3, q0 + h + 192);
-        }
-        for (; h < static_cast<int>(H); h += 64) insert(Lw + P.comega * lp[h], q0 + h);
+      // the sub-beams' scores and result offsets (a group's results are
+      // contiguous in the scratch); lane h reads homophone h of every sub-beam
+      double Lw[kMaxSub];
+      const double* lp[kMaxSub];
+#pragma unroll
+      for (int j = 0; j < kMaxSub; ++j) {
+        const int jj = j < nsub ? j : 0;
+        Lw[j] = C.Lw[i * kMaxSub + jj];
+        lp[j] = scrL + sGoff[sPairG[e * kMaxSub + jj]];
+      }
+      for (int h = lane; h < static_cast<int>(H); h += 64) {
+        double a[kMaxSub];
+#pragma unroll
+        for (int j = 0; j < kMaxSub; ++j) a[j] = j < nsub ? lp[j][h] : 0.0;
+#pragma unroll
+        for (int j = 0; j < kMaxSub; ++j)
+          if (j < nsub) insert(Lw[j] + P.comega * a[j], j * static_cast<int>(H) + h);
       }
       // O rounds of wavefront arg-max; lane k keeps the k-th winner
       double myL = kNegInf, bestL = kNegInf;
@@ -1074,13 +1069,13 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
         const uint32_t h = static_cast<uint32_t>(myq) - j * H;
         const uint32_t ph = C.hist[i * kMaxSub + j];
         const QState st = scrS[sGoff[sPairG[e * kMaxSub + j]] + h];
-        const int32_t w = S.trie_words[sEvWoff[e] + h];
+        const int32_t w = st.w;
         HistNode hn;
         hn.parent = ph;
         hn.word = w;
         hn.c2 = st.c2;
         hn.c3 = st.c3;
-        hn.bo1 = S.uni[w].bo;
+        hn.bo1 = st.bo1;
         hn.bo2 = st.bo2;
         hn.bo3 = st.bo3;
         hn.pad = 0;
