@@ -35,6 +35,77 @@ __device__ __forceinline__ void lds_barrier() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
+// Cross-lane moves inside rows of 16 lanes (DPP): lane i reads lane i^1
+// (quad_perm [1,0,3,2]), lane i^2 (quad_perm [2,3,0,1]), the mirror lane in
+// its half-row (7-i) and in its row (15-i).  Applying an associative,
+// commutative operation after each of the four leaves every lane with the
+// result over its row; the four rows are then combined through readlane.  A
+// lane whose source lane is inactive receives `ident` (the operation's
+// identity).
+constexpr int kDppXor1 = 0xB1, kDppXor2 = 0x4E, kDppHalfMirror = 0x141, kDppMirror = 0x140;
+
+template <int CTRL>
+__device__ __forceinline__ int dpp_i32(int x, int ident) {
+  return __builtin_amdgcn_update_dpp(ident, x, CTRL, 0xF, 0xF, false);
+}
+
+template <int CTRL>
+__device__ __forceinline__ double dpp_f64(double x, double ident) {
+  return __hiloint2double(dpp_i32<CTRL>(__double2hiint(x), __double2hiint(ident)),
+                          dpp_i32<CTRL>(__double2loint(x), __double2loint(ident)));
+}
+
+__device__ __forceinline__ double readlane_f64(double x, int lane) {
+  return __hiloint2double(__builtin_amdgcn_readlane(__double2hiint(x), lane),
+                          __builtin_amdgcn_readlane(__double2loint(x), lane));
+}
+
+// Wavefront maximum of *mx and minimum of *mn, in every lane.
+__device__ __forceinline__ void wave_minmax(double* mx, double* mn) {
+  double a = *mx, c = *mn;
+#define LB_MM_STEP(C)                    \
+  a = fmax(a, dpp_f64<C>(a, -HUGE_VAL)); \
+  c = fmin(c, dpp_f64<C>(c, HUGE_VAL));
+  LB_MM_STEP(kDppXor1)
+  LB_MM_STEP(kDppXor2)
+  LB_MM_STEP(kDppHalfMirror)
+  LB_MM_STEP(kDppMirror)
+#undef LB_MM_STEP
+  *mx = fmax(fmax(readlane_f64(a, 0), readlane_f64(a, 16)), fmax(readlane_f64(a, 32), readlane_f64(a, 48)));
+  *mn = fmin(fmin(readlane_f64(c, 0), readlane_f64(c, 16)), fmin(readlane_f64(c, 32), readlane_f64(c, 48)));
+}
+
+// One DPP step of the wavefront arg-max of (L desc, q asc).
+template <int CTRL>
+__device__ __forceinline__ void argmax_step(double* L, int* q) {
+  const double oL = dpp_f64<CTRL>(*L, -HUGE_VAL);
+  const int oq = dpp_i32<CTRL>(*q, 0x7FFFFFFF);
+  const bool take = oL > *L || (oL == *L && oq < *q);
+  *L = take ? oL : *L;
+  *q = take ? oq : *q;
+}
+
+// Wavefront arg-max of (L desc, q asc), in every lane.
+__device__ __forceinline__ void wave_argmax(double* L, int* q) {
+  argmax_step<kDppXor1>(L, q);
+  argmax_step<kDppXor2>(L, q);
+  argmax_step<kDppHalfMirror>(L, q);
+  argmax_step<kDppMirror>(L, q);
+  double bL = readlane_f64(*L, 0);
+  int bq = __builtin_amdgcn_readlane(*q, 0);
+#pragma unroll
+  for (int r = 16; r < 64; r += 16) {
+    const double oL = readlane_f64(*L, r);
+    const int oq = __builtin_amdgcn_readlane(*q, r);
+    if (oL > bL || (oL == bL && oq < bq)) {
+      bL = oL;
+      bq = oq;
+    }
+  }
+  *L = bL;
+  *q = bq;
+}
+
 template <int BLOCK>
 __device__ inline double block_max(double v, double* red) {
 #pragma unroll
@@ -48,14 +119,11 @@ __device__ inline double block_max(double v, double* red) {
   return r;
 }
 
-// Block-wide maximum of `mx` and minimum of `mn` in one reduction.
-template <int BLOCK>
+// Block-wide maximum of `mx` and minimum of `mn` in one reduction (SYNC as in
+// block_scan).
+template <int BLOCK, bool SYNC = true>
 __device__ inline void block_minmax(double mx, double mn, double* red, double* out_max, double* out_min) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    mx = fmax(mx, __shfl_xor(mx, o, 64));
-    mn = fmin(mn, __shfl_xor(mn, o, 64));
-  }
+  wave_minmax(&mx, &mn);
   constexpr int NW = BLOCK / 64;
   if ((threadIdx.x & 63) == 0) {
     red[threadIdx.x >> 6] = mx;
@@ -68,13 +136,15 @@ __device__ inline void block_minmax(double mx, double mn, double* red, double* o
     a = fmax(a, red[k]);
     c = fmin(c, red[NW + k]);
   }
-  lds_barrier();
+  if (SYNC) lds_barrier();
   *out_max = a;
   *out_min = c;
 }
 
-// Exclusive prefix sum over the block; *total receives the block sum.
-template <int BLOCK>
+// Exclusive prefix sum over the block; *total receives the block sum.  With
+// SYNC = false the trailing barrier is left out: `red` must then not be
+// written again before the next barrier.
+template <int BLOCK, bool SYNC = true>
 __device__ inline int block_scan(int v, int* red, int* total) {
   const int lane = threadIdx.x & 63;
   const int w = threadIdx.x >> 6;
@@ -93,7 +163,7 @@ __device__ inline int block_scan(int v, int* red, int* total) {
     base += (k < w) ? t : 0;
     tot += t;
   }
-  lds_barrier();
+  if (SYNC) lds_barrier();
   *total = tot;
   return base + x - v;
 }
@@ -304,7 +374,26 @@ struct LmResult {
   QState st;
 };
 
-__device__ __forceinline__ LmResult lm_lookup(const DevState& S, int32_t w, const HistNode& ctx, uint32_t* lines) {
+// The n-gram context of a history node: its last word, the slots of its 2- and
+// 3-word contexts and the three backoffs.
+struct Ctx {
+  int32_t word;
+  uint32_t c2, c3;
+  float bo1, bo2, bo3;
+};
+
+__device__ __forceinline__ Ctx ctx_of(const HistNode& h) {
+  Ctx c;
+  c.word = h.word;
+  c.c2 = h.c2;
+  c.c3 = h.c3;
+  c.bo1 = h.bo1;
+  c.bo2 = h.bo2;
+  c.bo3 = h.bo3;
+  return c;
+}
+
+__device__ __forceinline__ LmResult lm_lookup(const DevState& S, int32_t w, const Ctx& ctx, uint32_t* lines) {
   const uint64_t k2 = (static_cast<uint64_t>(static_cast<uint32_t>(ctx.word)) << 32) | static_cast<uint32_t>(w);
   const uint64_t k3 = (static_cast<uint64_t>(ctx.c2) << 32) | static_cast<uint32_t>(w);
   const uint64_t k4 = (static_cast<uint64_t>(ctx.c3) << 32) | static_cast<uint32_t>(w);
@@ -352,7 +441,7 @@ __device__ __forceinline__ LmResult lm_lookup(const DevState& S, int32_t w, cons
 // context slot if the LM has that trigram, else its 2-word context slot, else
 // its last word; the backoff weights are functions of these) and the trie
 // node of the completed word (by its first word offset, < 2^30).
-__device__ __forceinline__ unsigned long long group_key(const HistNode& ctx, uint32_t woff) {
+__device__ __forceinline__ unsigned long long group_key(const Ctx& ctx, uint32_t woff) {
   const uint64_t tag = ctx.c3 != kNone ? 2u : (ctx.c2 != kNone ? 1u : 0u);
   const uint64_t id = ctx.c3 != kNone ? ctx.c3 : (ctx.c2 != kNone ? ctx.c2 : static_cast<uint32_t>(ctx.word));
   return (tag << 62) | (id << 30) | woff;
@@ -403,7 +492,7 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
   constexpr int NC = (kSep + LPB - 1) / LPB;  // extension slots per lane
   constexpr int NPM = KMAX * kMaxSub;  // (completed word, sub-beam) pairs per frame, at most
   constexpr int SEL_BYTES = kBins * 4 + kBoundaryCap * 16;
-  constexpr int LM_BYTES = 32 * NPM + 16;
+  constexpr int LM_BYTES = 52 * NPM + 16;
   constexpr int UNI_BYTES = SEL_BYTES > LM_BYTES ? SEL_BYTES : LM_BYTES;
   static_assert(20 * KMAX <= SEL_BYTES, "fusion sort scratch");
   const int b = blockIdx.x;
@@ -428,8 +517,8 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
   // hypotheses that completed a word this frame
   __shared__ uint32_t sEvBeam[KMAX], sEvSrc[KMAX], sEvWoff[KMAX], sEvH[KMAX];
   __shared__ int32_t sNG;
-  __shared__ double sRed[2 * NW];
-  __shared__ int32_t sScan[NW];
+  __shared__ double sRed[2 * NW], sRedB[2 * NW];
+  __shared__ int32_t sScan[NW], sScanB[NW], sScanC[NW], sScanD[NW];
   __shared__ int32_t sBucket, sAbove, sBucketCnt, sBCount;
   __shared__ unsigned long long sCnt[3];  // probed lines, completed words, LM queries
 
@@ -498,6 +587,8 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
       sD[tid] = 0.0;
     }
     for (int s = tid; s < HS; s += BLOCK) sHKey[s] = kEmptyKey;
+    for (int d = tid; d < kBins; d += BLOCK) sHisto[d] = 0;
+    if (tid == 0) sBCount = 0;
     uint64_t my_key = 0, my_pkey = kNoParent;
     double my_anb = kNegInf;
     uint32_t my_meta = 0;
@@ -612,7 +703,7 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
       mn = fmin(mn, sc != kNegInf ? sc : HUGE_VAL);
     }
     double best, lowest;
-    block_minmax<BLOCK>(mx, mn, sRed, &best, &lowest);
+    block_minmax<BLOCK, false>(mx, mn, sRed, &best, &lowest);
     const double thr = best - P.theta;
 
     // ---- top-K.  Level 0 bins (best - score) over [max(thr, lowest), best] into
@@ -647,7 +738,7 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
         local += d < kBins ? static_cast<int>(sHisto[d]) : 0;
       }
       int tot = 0;
-      const int before = block_scan<BLOCK>(local, sScan, &tot);
+      const int before = block_scan<BLOCK, false>(local, sScan, &tot);
       if (need_in > 0 && before < need_in && before + local >= need_in) {
         int acc = before;
         for (int q = 0; q < PER; ++q) {
@@ -670,8 +761,6 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
     // (0xFFFF: no candidate); exact scores are recomputed only inside the boundary bin
     uint32_t binp[(NC + 1) / 2];
     uint32_t bin_stay = 0xFFFFu;
-    for (int d = tid; d < kBins; d += BLOCK) sHisto[d] = 0;
-    lds_barrier();
     if (c_stay != kNegInf && c_stay >= thr) {
       bin_stay = static_cast<uint32_t>(bin0(0, c_stay));
       atomicAdd(&sHisto[bin_stay], 1u);
@@ -738,14 +827,10 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
     if (!select_all) {
       need -= sAbove;
       int cntb = sBucketCnt;
-      if (tid == 0) {
-        sLvBeta[0] = beta0;
-        sLvShift[0] = shift0;
-      }
-      lds_barrier();
       int key_shift = shift0 >= 0 ? shift0 - 10 : 64 - 10;
       bool key_level = shift0 >= 0;
-      while (cntb != need && cntb > kBoundaryCap && !(key_level && sLvShift[nlev - 1] == 0) && nlev < kMaxLevels) {
+      int last_shift = shift0;  // shift of the deepest level (-1: score bins)
+      while (cntb != need && cntb > kBoundaryCap && !(key_level && last_shift == 0) && nlev < kMaxLevels) {
         // refine: score range of the boundary bin's members, or key bits when it is flat
         const int L = nlev;
         double bmx = kNegInf, bmn = HUGE_VAL;
@@ -754,7 +839,7 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
           bmn = fmin(bmn, sc);
         });
         double lv_hi, lv_lo;
-        block_minmax<BLOCK>(bmx, bmn, sRed, &lv_hi, &lv_lo);
+        block_minmax<BLOCK>(bmx, bmn, sRedB, &lv_hi, &lv_lo);
         if (tid == 0) {
           sLvHi[L] = lv_hi;
           sLvInv[L] = lv_hi > lv_lo ? static_cast<double>(kBins) / (lv_hi - lv_lo) : 0.0;
@@ -762,7 +847,8 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
         }
         for (int d = tid; d < kBins; d += BLOCK) sHisto[d] = 0;
         lds_barrier();
-        key_level = sLvShift[L] >= 0;
+        last_shift = sLvShift[L];
+        key_level = last_shift >= 0;
         if (key_level) key_shift -= 10;
         for_bnd(L, [&](int, int v, double sc) { atomicAdd(&sHisto[bin_at(L, v, sc)], 1u); });
         lds_barrier();
@@ -776,9 +862,8 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
       if (cntb == need) {
         all_bin = true;
       } else {
-        // exact rank inside the boundary bin (a flat key level of shift 0 holds one key)
-        if (tid == 0) sBCount = 0;
-        lds_barrier();
+        // exact rank inside the boundary bin (a flat key level of shift 0 holds one
+        // key); sBCount was cleared at the start of the frame
         for_bnd(nlev, [&](int, int v, double sc) {
           const int slot = atomicAdd(&sBCount, 1);
           if (slot < kBoundaryCap) {
@@ -816,7 +901,7 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
       if (take) sel_bits |= 1ull << (k == NC ? 0 : k + 1);
     }
     int nsel = 0;
-    int wpos = block_scan<BLOCK>(__popcll(sel_bits), sScan, &nsel);
+    int wpos = block_scan<BLOCK, false>(__popcll(sel_bits), sScanB, &nsel);
     if (nsel > P.K) {  // cannot happen when the selection is exact; never write past K entries
       nsel = P.K;
       if (tid == 0) atomicOr(S.flags, kFlagSelect);
@@ -830,7 +915,13 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
     lds_barrier();
 
     // ---- the new hypotheses; an extension's trie node is fetched now and
-    // stored after the LM step
+    // stored after the LM step.  (The n-gram grouping table is cleared here:
+    // the top-K scratch it shares is no longer read.)
+    {
+      unsigned long long* const gk = reinterpret_cast<unsigned long long*>(sSel);
+      for (int q = tid; q < NPM; q += BLOCK) gk[q] = kEmptyKey;
+      if (tid == 0) sNG = 0;
+    }
     const int r = tid;
     int is_event = 0;
     uint32_t ev_src = 0, ev_woff = 0, ev_H = 0;
@@ -882,7 +973,7 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
       }
     }
     int nev = 0;
-    const int erank = block_scan<BLOCK>(is_event, sScan, &nev);
+    const int erank = block_scan<BLOCK, false>(is_event, sScanC, &nev);
     if (is_event) {
       sEvBeam[erank] = static_cast<uint32_t>(r);
       sEvSrc[erank] = ev_src;
@@ -898,12 +989,10 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
     unsigned long long* const sGKey = reinterpret_cast<unsigned long long*>(sSel);
     int32_t* const sGId = reinterpret_cast<int32_t*>(sSel + 8 * NPM);
     int32_t* const sPairG = sGId + NPM;  // pair -> hash slot, then -> group
-    uint32_t* const sGph = reinterpret_cast<uint32_t*>(sPairG + NPM);
-    uint32_t* const sGwoff = sGph + NPM;
+    uint32_t* const sGwoff = reinterpret_cast<uint32_t*>(sPairG + NPM);
     uint32_t* const sGH = sGwoff + NPM;
-    int32_t* const sGoff = reinterpret_cast<int32_t*>(sGH + NPM);  // NPM + 1 entries
-    for (int q = tid; q < NPM; q += BLOCK) sGKey[q] = kEmptyKey;
-    if (tid == 0) sNG = 0;
+    Ctx* const sGctx = reinterpret_cast<Ctx*>(sGH + NPM);             // 24 B each
+    int32_t* const sGoff = reinterpret_cast<int32_t*>(sGctx + NPM);  // NPM + 1 entries
     lds_barrier();
     for (int pr = tid; pr < nev * kMaxSub; pr += BLOCK) {
       const int e = pr / kMaxSub;
@@ -912,7 +1001,7 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
       int slot = -1;
       if (j < static_cast<int>((C.meta[i] >> 8) & 0xFF)) {
         const uint32_t ph = C.hist[i * kMaxSub + j];
-        const HistNode ctx = S.arena[ph];
+        const Ctx ctx = ctx_of(S.arena[ph]);
         const unsigned long long key = group_key(ctx, sEvWoff[e]);
         uint32_t q = static_cast<uint32_t>(splitmix64(key)) & (NPM - 1);
         for (;;) {
@@ -920,9 +1009,9 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
           if (prev == kEmptyKey) {
             const int g = atomicAdd(&sNG, 1);
             sGId[q] = g;
-            sGph[g] = ph;
             sGwoff[g] = sEvWoff[e];
             sGH[g] = sEvH[e];
+            sGctx[g] = ctx;
             break;
           }
           if (prev == key) break;
@@ -948,7 +1037,7 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
         const int g = tid * PG + q;
         loc += g < NG ? static_cast<int>(sGH[g]) : 0;
       }
-      int pre = block_scan<BLOCK>(loc, sScan, &U);
+      int pre = block_scan<BLOCK, false>(loc, sScanD, &U);
 #pragma unroll
       for (int q = 0; q < PG; ++q) {
         const int g = tid * PG + q;
@@ -973,8 +1062,7 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
       }
       const uint32_t h = static_cast<uint32_t>(u - sGoff[lo]);
       const int32_t w = S.trie_words[sGwoff[lo] + h];
-      const HistNode ctx = S.arena[sGph[lo]];
-      const LmResult res = lm_lookup(S, w, ctx, &lines);
+      const LmResult res = lm_lookup(S, w, sGctx[lo], &lines);
       scrL[u] = res.lp;
       scrS[u] = res.st;
     }
@@ -1032,18 +1120,7 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
       for (int k = 0; k < O; ++k) {
         double bL = tL[0];
         int bq = tq[0];
-        int bl = lane;
-#pragma unroll
-        for (int o = 32; o > 0; o >>= 1) {
-          const double oL = __shfl_xor(bL, o, 64);
-          const int oq = __shfl_xor(bq, o, 64);
-          const int ol = __shfl_xor(bl, o, 64);
-          if (oL > bL || (oL == bL && (oq < bq || (oq == bq && ol < bl)))) {
-            bL = oL;
-            bq = oq;
-            bl = ol;
-          }
-        }
+        wave_argmax(&bL, &bq);
         if (bL == kNegInf) break;
         if (k == 0) bestL = bL;
         if (bL < bestL - P.lam) break;
@@ -1051,7 +1128,7 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
           myL = bL;
           myq = bq;
         }
-        if (lane == bl) {
+        if (tL[0] == bL && tq[0] == bq) {  // the lane holding the winner (queries are distinct)
 #pragma unroll
           for (int m = 0; m + 1 < kMaxSub; ++m) {
             tL[m] = tL[m + 1];
@@ -1476,7 +1553,7 @@ hipError_t launch_decode(int K, const DevParams& P, const DevState& S, const flo
   else if (K <= 128)
     LB_LAUNCH((k_decode<128, 4>), dim3(B), dim3(512), st, P, S, logits, lengths, Tc, tau0, tau1);
   else
-    LB_LAUNCH((k_decode<256, 2>), dim3(B), dim3(512), st, P, S, logits, lengths, Tc, tau0, tau1);
+    LB_LAUNCH((k_decode<256, 4>), dim3(B), dim3(1024), st, P, S, logits, lengths, Tc, tau0, tau1);
   return hipGetLastError();
 }
 
