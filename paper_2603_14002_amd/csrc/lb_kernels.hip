@@ -148,12 +148,16 @@ template <int BLOCK, bool SYNC = true>
 __device__ inline int block_scan(int v, int* red, int* total) {
   const int lane = threadIdx.x & 63;
   const int w = threadIdx.x >> 6;
+  // inclusive wavefront scan: shifts by 1, 2, 4, 8 inside each row of 16 lanes
+  // (lanes shifted in from outside the row add 0), then rows 1 and 3 add the
+  // last lane of the row before them, and rows 2 and 3 add lane 31
   int x = v;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const int y = __shfl_up(x, o, 64);
-    if (lane >= o) x += y;
-  }
+  x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xF, 0xF, true);
+  x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xF, 0xF, true);
+  x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xF, 0xF, true);
+  x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xF, 0xF, true);
+  x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xA, 0xF, false);
+  x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xC, 0xF, false);
   if (lane == 63) red[w] = x;
   lds_barrier();
   int base = 0, tot = 0;
@@ -565,7 +569,10 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
   double* const scrL = S.scrL + static_cast<size_t>(b) * S.scap;
   QState* const scrS = S.scrS + static_cast<size_t>(b) * S.scap;
   int cur = 0;
-  float dnext = tid < kClasses ? logits[(static_cast<size_t>(b) * Tc + tau0) * kClasses + tid] : 0.0f;
+  // the scaled log-probs of the first frame; each frame's row of the next frame
+  // is loaded early and written to sD after the frame's last global wait
+  if (tid < 48) sD[tid] = tid < kClasses ? P.alpha * static_cast<double>(logits[(static_cast<size_t>(b) * Tc + tau0) * kClasses + tid]) : 0.0;
+  float dnext = 0.0f;
   lds_barrier();
 
   for (int tau = tau0; tau < tend; ++tau) {
@@ -579,13 +586,8 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
     BeamLds<KMAX>& C = sBeam[cur];
     BeamLds<KMAX>& N = sBeam[cur ^ 1];
 
-    // ---- the frame's scaled log-probs (the next frame's row is loaded meanwhile)
-    if (tid < kClasses) {
-      sD[tid] = P.alpha * static_cast<double>(dnext);
-      if (tau + 1 < tend) dnext = logits[(static_cast<size_t>(b) * Tc + tau + 1) * kClasses + tid];
-    } else if (tid < 48) {
-      sD[tid] = 0.0;
-    }
+    // the next frame's log-probs are loaded meanwhile
+    if (tid < kClasses && tau + 1 < tend) dnext = logits[(static_cast<size_t>(b) * Tc + tau + 1) * kClasses + tid];
     for (int s = tid; s < HS; s += BLOCK) sHKey[s] = kEmptyKey;
     for (int d = tid; d < kBins; d += BLOCK) sHisto[d] = 0;
     if (tid == 0) sBCount = 0;
@@ -1184,6 +1186,7 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
       N.first[r] = tn.first_child;
       N.woff[r] = tn.word_off;
     }
+    if (tid < kClasses && tau + 1 < tend) sD[tid] = P.alpha * static_cast<double>(dnext);  // this frame's are no longer read
 
     // ---- Eq. (2) on fusion frames: the top-F hypotheses by (total desc, key
     // asc); each sub-beam's score becomes phi * its synthetic fusion score and
