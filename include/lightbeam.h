@@ -51,6 +51,18 @@ enum { LB_MAX_BEAM = 256, LB_MAX_SUBBEAMS = 4 };
 /* lb_decode_batch flags */
 enum { LB_BEGIN = 1u, LB_END = 2u };
 
+/* recombination of the paths that reach one prefix (lb_params.merge) */
+enum {
+  LB_MERGE_LOGSUMEXP = 0,  /* sum over alignments (classical CTC prefix search)      */
+  LB_MERGE_MAX = 1         /* best alignment only (the recombination of App. E.1)    */
+};
+
+/* what lb_decode_batch's per-frame scores are (lb_params.input) */
+enum {
+  LB_INPUT_LOGPROBS = 0,   /* log-probabilities (log-softmax already applied)        */
+  LB_INPUT_LOGITS = 1      /* raw scores: log-softmax over the 41 classes per frame  */
+};
+
 /* fusion scorer */
 enum {
   LB_FUSION_NONE = 0,          /* no delayed fusion                                     */
@@ -108,6 +120,8 @@ typedef struct lb_params {
   double fusion_hi;        /*   S_fus(w1..wn) = sum_i Bg(w_{i-1}, w_i), w0 = <s>  */
   double lm_load_factor;   /* n-gram hash-table load factor (0 = 0.5), <= 0.9     */
   int64_t arena_nodes_per_stream; /* word-history capacity (0 = beam*subbeams*max_frames) */
+  int32_t merge;           /* LB_MERGE_*                                          */
+  int32_t input;           /* LB_INPUT_*                                          */
 } lb_params;
 
 typedef struct lb_decoder lb_decoder;

@@ -47,6 +47,7 @@ class _Params(ctypes.Structure):
                 ("lam", ctypes.c_double),
                 ("fusion_interval", ctypes.c_int32), ("fusion_top_f", ctypes.c_int32),
                 ("fusion_mode", ctypes.c_int32), ("finalize", ctypes.c_int32),
+                ("merge_max", ctypes.c_int32), ("raw_logits", ctypes.c_int32),
                 ("fusion_seed", ctypes.c_uint64),
                 ("fusion_lo", ctypes.c_double), ("fusion_hi", ctypes.c_double)]
 
@@ -106,7 +107,7 @@ def params_from(p, fusion_seed: int = 0, fusion_mode: int = 0, **overrides) -> _
     d = dict(beam=p.beam, subbeams=p.subbeams, alpha=p.alpha, beta=p.beta, gamma=p.gamma,
              omega=p.omega, phi=p.phi, theta=p.theta, lam=p.lam,
              fusion_interval=p.fusion_interval, fusion_top_f=p.fusion_top_f,
-             fusion_mode=fusion_mode, finalize=1, fusion_seed=fusion_seed,
+             fusion_mode=fusion_mode, finalize=1, merge_max=0, raw_logits=0, fusion_seed=fusion_seed,
              fusion_lo=p.fusion_lo, fusion_hi=p.fusion_hi)
     d.update(overrides)
     return _Params(**d)

@@ -66,6 +66,17 @@ double lse_list(const std::vector<double>& v) {
   return acc;
 }
 
+// The combination of two path scores that reach the same prefix: their
+// log-sum-exp (all alignments), or their maximum (the best alignment, the
+// recombination of App. E.1).
+double comb2(bool use_max, double x, double y) { return use_max ? std::max(x, y) : lse2(x, y); }
+
+double comb_list(bool use_max, const std::vector<double>& v) {
+  double acc = kNegInf;
+  for (double x : v) acc = comb2(use_max, acc, x);
+  return acc;
+}
+
 // SplitMix64 output function for state x (Steele, Lea & Flood, OOPSLA 2014):
 // advance by the golden-ratio increment, then the variant-13 finaliser.
 uint64_t splitmix64(uint64_t x) {
@@ -91,6 +102,8 @@ struct Params {
   int fusion_top_f;     // 0 = all entries
   int fusion_mode;      // 0 = synthetic bigram scorer, 1 = the n-gram LM's own score (pin)
   int finalize;         // 1 = end of utterance (final fusion, drop mid-word); 0 = rank the live beam
+  int merge_max;        // 0 = contributions to a prefix combine by log-sum-exp; 1 = by max (App. E.1)
+  int raw_logits;       // 0 = inputs are log-probabilities; 1 = raw scores, log-softmax per frame first
   uint64_t fusion_seed;
   double fusion_lo, fusion_hi;
 };
@@ -189,7 +202,9 @@ std::vector<int> partial_word(const std::vector<int>& y) {
   return std::vector<int>(y.begin() + i, y.end());
 }
 
-double acoustic(const Hyp& h) { return lse2(h.a_b, h.a_nb); }
+// Set once per decode: how a_b and a_nb combine into a prefix's acoustic score.
+thread_local bool g_merge_max = false;
+double acoustic(const Hyp& h) { return comb2(g_merge_max, h.a_b, h.a_nb); }
 double total(const Hyp& h) { return acoustic(h) + h.subs[0].Lw; }
 
 // Is symbol v (1..40) a lexicon-valid extension of a prefix whose current
@@ -328,9 +343,22 @@ Output decode(const Model& M, const Params& p, const float* logits, int T, bool 
   beam[0].a_nb = kNegInf;
   beam[0].subs = {Sub{0.0, {}}};
 
+  g_merge_max = p.merge_max != 0;
+  const bool mx = g_merge_max;
   for (int t = 0; t < T; ++t) {
     double D[kClasses];
-    for (int v = 0; v < kClasses; ++v) D[v] = p.alpha * static_cast<double>(logits[t * kClasses + v]);
+    double lp[kClasses];
+    for (int v = 0; v < kClasses; ++v) lp[v] = static_cast<double>(logits[t * kClasses + v]);
+    if (p.raw_logits) {
+      // log-softmax over the frame's classes
+      double m = kNegInf;
+      for (int v = 0; v < kClasses; ++v) m = std::max(m, lp[v]);
+      double s = 0.0;
+      for (int v = 0; v < kClasses; ++v) s += std::exp(lp[v] - m);
+      const double ls = std::log(s);
+      for (int v = 0; v < kClasses; ++v) lp[v] = (lp[v] - m) - ls;
+    }
+    for (int v = 0; v < kClasses; ++v) D[v] = p.alpha * lp[v];
     out.st.expansions += static_cast<int64_t>(beam.size()) * kClasses;
 
     // Fan-out (Alg. 1): every entry stays (blank / repeated last symbol) or
@@ -344,7 +372,7 @@ Output decode(const Model& M, const Params& p, const float* logits, int T, bool 
     };
     std::map<std::vector<int>, Cand> C;
     for (const Hyp& h : beam) {
-      const double pr = lse2(h.a_b, h.a_nb);
+      const double pr = comb2(mx, h.a_b, h.a_nb);
       const int last = last_symbol(h.y);
       Cand& cs = C[h.y];
       cs.b.push_back(pr + D[kBlank]);
@@ -376,10 +404,10 @@ Output decode(const Model& M, const Params& p, const float* logits, int T, bool 
       Merged m;
       m.y = &kv.first;
       m.c = &kv.second;
-      m.a_b = lse_list(kv.second.b);
-      m.a_nb = lse_list(kv.second.nb);
+      m.a_b = comb_list(mx, kv.second.b);
+      m.a_nb = comb_list(mx, kv.second.nb);
       const Hyp* src = kv.second.stay ? kv.second.stay : kv.second.ext;
-      m.total = lse2(m.a_b, m.a_nb) + src->subs[0].Lw;
+      m.total = comb2(mx, m.a_b, m.a_nb) + src->subs[0].Lw;
       m.key = prefix_key(kv.first);
       if (m.total == kNegInf) continue;
       ms.push_back(m);
@@ -422,7 +450,7 @@ Output decode(const Model& M, const Params& p, const float* logits, int T, bool 
 
     if (want_frame_lse) {
       double acc = kNegInf;
-      for (const Hyp& h : beam) acc = lse2(acc, acoustic(h));
+      for (const Hyp& h : beam) acc = lse2(acc, lse2(h.a_b, h.a_nb));
       out.frame_lse.push_back(acc);
     }
   }
@@ -455,6 +483,8 @@ struct orc_params {
   int32_t fusion_top_f;
   int32_t fusion_mode;
   int32_t finalize;
+  int32_t merge_max;
+  int32_t raw_logits;
   uint64_t fusion_seed;
   double fusion_lo, fusion_hi;
 };
@@ -523,6 +553,8 @@ static Params to_params(const orc_params* q) {
   p.fusion_top_f = q->fusion_top_f;
   p.fusion_mode = q->fusion_mode;
   p.finalize = q->finalize;
+  p.merge_max = q->merge_max;
+  p.raw_logits = q->raw_logits;
   p.fusion_seed = q->fusion_seed;
   p.fusion_lo = q->fusion_lo;
   p.fusion_hi = q->fusion_hi;

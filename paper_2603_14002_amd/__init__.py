@@ -59,7 +59,8 @@ class lb_params(ctypes.Structure):
                 ("max_frames", ctypes.c_int32), ("max_words_out", ctypes.c_int32),
                 ("fusion_seed", ctypes.c_uint64), ("fusion_lo", ctypes.c_double),
                 ("fusion_hi", ctypes.c_double), ("lm_load_factor", ctypes.c_double),
-                ("arena_nodes_per_stream", ctypes.c_int64)]
+                ("arena_nodes_per_stream", ctypes.c_int64),
+                ("merge", ctypes.c_int32), ("input", ctypes.c_int32)]
 
 
 class lb_stats(ctypes.Structure):
@@ -183,6 +184,8 @@ def lb_reset_stats(dec: int) -> None:
 # kernel kinds (index of lb_stats.launches / kernel_ms)
 KIND_DECODE, KIND_OUTPUT, KIND_FUSE_SELECT, KIND_FUSE_EXPORT, KIND_FUSE_APPLY, KIND_BEGIN = 0, 1, 2, 3, 4, 5
 KIND_NAMES = ("decode", "output", "fuse_select", "fuse_export", "fuse_apply", "begin")
+LB_MERGE_LOGSUMEXP, LB_MERGE_MAX = 0, 1
+LB_INPUT_LOGPROBS, LB_INPUT_LOGITS = 0, 1
 LB_PROFILE_ALL = 0xFF
 
 
@@ -247,7 +250,7 @@ def make_params(p, *, max_batch: int, max_frames: int, fusion_source: Optional[i
              fusion_top_f=p.fusion_top_f, max_batch=max_batch, max_frames=max_frames,
              max_words_out=p.max_words_out, fusion_seed=fusion_seed & (2**64 - 1),
              fusion_lo=p.fusion_lo, fusion_hi=p.fusion_hi, lm_load_factor=load_factor,
-             arena_nodes_per_stream=arena_nodes_per_stream)
+             arena_nodes_per_stream=arena_nodes_per_stream, merge=LB_MERGE_LOGSUMEXP, input=LB_INPUT_LOGPROBS)
     d.update(overrides)
     return lb_params(**d)
 

@@ -16,7 +16,7 @@
 
 using namespace lb;
 
-static_assert(sizeof(lb_params) == 128, "lb_params layout");
+static_assert(sizeof(lb_params) == 136, "lb_params layout");
 static_assert(sizeof(lb_ngram_desc) == 144, "lb_ngram_desc layout");
 static_assert(sizeof(lb_lexicon_desc) == 24, "lb_lexicon_desc layout");
 static_assert(sizeof(lb_stats) == 248, "lb_stats layout");
@@ -232,6 +232,10 @@ lb_status validate(const lb_lexicon_desc* lex, const lb_ngram_desc* lm, const lb
     return fail(LB_ERR_INVALID_ARG, "unknown fusion_source");
   if (p->fusion_source != LB_FUSION_NONE && p->fusion_interval < 1)
     return fail(LB_ERR_INVALID_ARG, "fusion needs fusion_interval >= 1");
+  if (p->merge != LB_MERGE_LOGSUMEXP && p->merge != LB_MERGE_MAX)
+    return fail(LB_ERR_INVALID_ARG, "merge must be LB_MERGE_LOGSUMEXP or LB_MERGE_MAX");
+  if (p->input != LB_INPUT_LOGPROBS && p->input != LB_INPUT_LOGITS)
+    return fail(LB_ERR_INVALID_ARG, "input must be LB_INPUT_LOGPROBS or LB_INPUT_LOGITS");
   if (p->fusion_top_f < 0) return fail(LB_ERR_INVALID_ARG, "fusion_top_f < 0");
   const double lf = p->lm_load_factor == 0.0 ? 0.5 : p->lm_load_factor;
   if (!(lf > 0.0 && lf <= 0.9)) return fail(LB_ERR_INVALID_ARG, "lm_load_factor must be in (0, 0.9]");
@@ -443,6 +447,8 @@ lb_status lb_create(const lb_lexicon_desc* lex, const lb_ngram_desc* lm, const l
   P.fusion_interval = p.fusion_interval;
   P.fusion_top_f = p.fusion_top_f;
   P.bos = lm->bos_id;
+  P.merge_max = p.merge == LB_MERGE_MAX ? 1 : 0;
+  P.raw_input = p.input == LB_INPUT_LOGITS ? 1 : 0;
   P.alpha = p.alpha;
   P.beta = p.beta;
   P.gamma = p.gamma;

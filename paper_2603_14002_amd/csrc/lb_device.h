@@ -99,6 +99,8 @@ struct DevParams {
   int32_t K, O, W;
   int32_t fusion_source, fusion_interval, fusion_top_f;
   int32_t bos;
+  int32_t merge_max;  // 1: paths into one prefix combine by max, 0: by log-sum-exp
+  int32_t raw_input;  // 1: per-frame scores are raw, log-softmax them first
   int32_t pad;
   double alpha, beta, gamma, comega, phi, theta, lam;
   uint64_t seed;

@@ -75,6 +75,15 @@ __device__ __forceinline__ void wave_minmax(double* mx, double* mn) {
   *mn = fmin(fmin(readlane_f64(c, 0), readlane_f64(c, 16)), fmin(readlane_f64(c, 32), readlane_f64(c, 48)));
 }
 
+// Wavefront sum of x, in every lane.
+__device__ __forceinline__ double wave_sum(double x) {
+  x += dpp_f64<kDppXor1>(x, 0.0);
+  x += dpp_f64<kDppXor2>(x, 0.0);
+  x += dpp_f64<kDppHalfMirror>(x, 0.0);
+  x += dpp_f64<kDppMirror>(x, 0.0);
+  return (readlane_f64(x, 0) + readlane_f64(x, 16)) + (readlane_f64(x, 32) + readlane_f64(x, 48));
+}
+
 // One DPP step of the wavefront arg-max of (L desc, q asc).
 template <int CTRL>
 __device__ __forceinline__ void argmax_step(double* L, int* q) {
@@ -569,9 +578,22 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
   double* const scrL = S.scrL + static_cast<size_t>(b) * S.scap;
   QState* const scrS = S.scrS + static_cast<size_t>(b) * S.scap;
   int cur = 0;
-  // the scaled log-probs of the first frame; each frame's row of the next frame
-  // is loaded early and written to sD after the frame's last global wait
-  if (tid < 48) sD[tid] = tid < kClasses ? P.alpha * static_cast<double>(logits[(static_cast<size_t>(b) * Tc + tau0) * kClasses + tid]) : 0.0;
+  // D = alpha * log-probs of a frame into sD, by wavefront 0 (every lane):
+  // raw scores are first normalised by a log-softmax over the 41 classes
+  auto set_row = [&](const DevParams& Pr, float xin) {
+    double x = lane < kClasses ? static_cast<double>(xin) : kNegInf;
+    if (Pr.raw_input) {
+      double m = x, unused = x;
+      wave_minmax(&m, &unused);
+      const double sum = wave_sum(lane < kClasses ? exp(x - m) : 0.0);
+      x = (x - m) - log(sum);
+    }
+    if (lane < 48) sD[lane] = lane < kClasses ? Pr.alpha * x : 0.0;
+  };
+  // the first frame's row now; each frame loads the next frame's row early and
+  // writes it to sD after the frame's last global wait
+  if (wave == 0)
+    set_row(P, lane < kClasses ? logits[(static_cast<size_t>(b) * Tc + tau0) * kClasses + lane] : 0.0f);
   float dnext = 0.0f;
   lds_barrier();
 
@@ -646,11 +668,12 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
         const double base = (last == static_cast<int>(C.meta[par] & 0xFF)) ? C.ab[par] : C.pt[par];
         ext = (base + sD[last]) + (last == kSep ? P.gamma : P.beta);
       }
-      // anb2 = lse(rep, ext), then pt2 = lse(ab2, anb2)
+      // anb2 = merge(rep, ext), then pt2 = merge(ab2, anb2); merge is
+      // log-sum-exp, or max for the best-alignment recombination
       double x = rep, y = ext, anb2 = 0.0;
 #pragma unroll 1
       for (int pass = 0; pass < 2; ++pass) {
-        const double l = lse2(x, y);
+        const double l = P.merge_max ? fmax(x, y) : lse2(x, y);
         if (pass == 0) {
           anb2 = l;
           x = ab2;
@@ -1186,7 +1209,7 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
       N.first[r] = tn.first_child;
       N.woff[r] = tn.word_off;
     }
-    if (tid < kClasses && tau + 1 < tend) sD[tid] = P.alpha * static_cast<double>(dnext);  // this frame's are no longer read
+    if (wave == 0 && tau + 1 < tend) set_row(P, dnext);  // this frame's row is no longer read
 
     // ---- Eq. (2) on fusion frames: the top-F hypotheses by (total desc, key
     // asc); each sub-beam's score becomes phi * its synthetic fusion score and

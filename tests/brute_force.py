@@ -4,8 +4,9 @@ Every alignment a in C^T over a small class subset C is scored as
 sum_t D[t, a_t], collapsed (merge repeats, drop blanks) and grouped by the
 collapsed symbol sequence; alignments with symbols outside the lexicon are
 discarded.  A complete hypothesis (empty, or ending in the separator) then
-scores LSE over its alignments, plus the token / word bonuses, plus the best
-word-level reading over its homophones.  No beam, no pruning, no prefix
+scores LSE over its alignments (or the best alignment alone, for the max
+recombination), plus the token / word bonuses, plus the best word-level
+reading over its homophones.  No beam, no pruning, no prefix
 search: the definition of the search target written out.
 """
 
@@ -30,8 +31,9 @@ def collapse(a: Sequence[int]) -> Tuple[int, ...]:
     return tuple(out)
 
 
-def alignment_lse(D: np.ndarray, classes: Sequence[int]) -> Dict[Tuple[int, ...], float]:
-    """log-sum-exp over alignments of D (float64 [T, 41]) per collapsed sequence."""
+def alignment_lse(D: np.ndarray, classes: Sequence[int], reduce: str = "lse") -> Dict[Tuple[int, ...], float]:
+    """log-sum-exp (reduce="lse") or maximum (reduce="max") over alignments of D
+    (float64 [T, 41]) per collapsed sequence."""
     T = D.shape[0]
     C = np.asarray(classes)
     grid = np.array(list(itertools.product(range(len(C)), repeat=T)), dtype=np.int64)
@@ -40,7 +42,8 @@ def alignment_lse(D: np.ndarray, classes: Sequence[int]) -> Dict[Tuple[int, ...]
     acc: Dict[Tuple[int, ...], float] = {}
     for row, sc in zip(A, scores):
         y = collapse(row)
-        acc[y] = float(np.logaddexp(acc.get(y, -math.inf), sc))
+        prev = acc.get(y, -math.inf)
+        acc[y] = float(np.logaddexp(prev, sc)) if reduce == "lse" else float(max(prev, sc))
     return acc
 
 
@@ -58,13 +61,13 @@ def segments(y: Tuple[int, ...]):
 
 def complete_hypotheses(D: np.ndarray, classes: Sequence[int], lex_words: List[Tuple[int, ...]],
                         beta: float, gamma: float,
-                        reading_score: Callable[[List[int]], float]):
+                        reading_score: Callable[[List[int]], float], reduce: str = "lse"):
     """{y: (total, best reading)} over every lexicon-valid complete hypothesis."""
     homs: Dict[Tuple[int, ...], List[int]] = {}
     for w, ph in enumerate(lex_words):
         homs.setdefault(tuple(ph), []).append(w)
     out = {}
-    for y, lse in alignment_lse(D, classes).items():
+    for y, lse in alignment_lse(D, classes, reduce).items():
         words, partial = segments(y)
         if partial:
             continue

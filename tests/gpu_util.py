@@ -26,7 +26,7 @@ def say(msg: str) -> None:
 
 def gpu_decode(d, params=None, chunk: int = 0, batch: Optional[int] = None, fusion_source=None,
                profiling=False, max_words: Optional[int] = None, arena_nodes_per_stream: int = 0,
-               return_decoder=False, finalize=True):
+               return_decoder=False, finalize=True, logits: Optional[np.ndarray] = None, lb_overrides=None):
     """Decodes the first `batch` utterances of workload data `d` on cuda:0.
 
     Returns a list of (words list per rank, scores float32 array) per utterance."""
@@ -35,14 +35,16 @@ def gpu_decode(d, params=None, chunk: int = 0, batch: Optional[int] = None, fusi
     B = d.logits.shape[0] if batch is None else batch
     T = d.logits.shape[1]
     lp = lbm.make_params(p, max_batch=B, max_frames=T, fusion_seed=d.fusion_seed,
-                         fusion_source=fusion_source, arena_nodes_per_stream=arena_nodes_per_stream)
+                         fusion_source=fusion_source, arena_nodes_per_stream=arena_nodes_per_stream,
+                         **(lb_overrides or {}))
     if max_words is not None:
         lp.max_words_out = max_words
     dec = lbm.Decoder(d.lexicon, d.lm, lp)
     if profiling:
         lbm.lb_set_profiling(dec.handle, lbm.LB_PROFILE_ALL)
     dev = torch.device("cuda:0")
-    logits = torch.from_numpy(np.ascontiguousarray(d.logits[:B])).to(dev)
+    src = d.logits if logits is None else logits
+    logits = torch.from_numpy(np.ascontiguousarray(src[:B])).to(dev)
     lengths = np.ascontiguousarray(d.lengths[:B]).astype(np.int32)
     K, W = lp.beam, lp.max_words_out
     hyps = torch.empty((B, K, W), dtype=torch.int32, device=dev)
@@ -128,14 +130,17 @@ def oracle_for(d):
     return oracle.Oracle(d.lexicon, d.lm)
 
 
-def check_parity(d, gpu_out, utts, params=None, orc=None, name="", max_mismatch=0, finalize=True):
+def check_parity(d, gpu_out, utts, params=None, orc=None, name="", max_mismatch=0, finalize=True,
+                 logits: Optional[np.ndarray] = None, oracle_overrides=None):
     p = params or d.workload.params
     orc = orc or oracle_for(d)
-    op = oracle.params_from(p, fusion_seed=d.fusion_seed, finalize=1 if finalize else 0)
+    op = oracle.params_from(p, fusion_seed=d.fusion_seed, finalize=1 if finalize else 0,
+                            **(oracle_overrides or {}))
+    src = d.logits if logits is None else logits
     par = Parity()
     t0 = time.time()
     for b in utts:
-        res = orc.decode(d.logits[b, :d.lengths[b]], op)
+        res = orc.decode(src[b, :d.lengths[b]], op)
         compare(par, b, gpu_out[b], res, p.beam)
     say(par.report(name) + f" oracle {time.time() - t0:.1f}s")
     assert len(par.mismatch) <= max_mismatch, "\n".join(par.mismatch[:5])

@@ -212,3 +212,37 @@ def test_external_fusion_round_trip(name):
         say(f"[case] external fusion {name} finalize={fin}: {events} events")
         check_parity(d, out, range(B), orc=orc, name=f"external/{name}", finalize=fin)
         dec.close()
+
+
+# ---------------------------------------------------------------- recombination by max, raw scores in
+
+
+@pytest.mark.parametrize("name", ["t-c1k", "t-c20k", "t-k256"])
+def test_max_recombination(name):
+    """merge = max (App. E.1): the GPU against the oracle with the same rule."""
+    d = load_workload(name, batch=12 if name != "t-k256" else 4)
+    B = d.logits.shape[0]
+    say(f"[case] max recombination {name}: B={B} K={d.workload.params.beam}")
+    for fin in (True, False):
+        out = gpu_decode(d, finalize=fin, lb_overrides=dict(merge=lbm.LB_MERGE_MAX))
+        check_parity(d, out, range(B), name=f"{name}/max/{'end' if fin else 'live'}", finalize=fin,
+                     oracle_overrides=dict(merge_max=1))
+    # the rule matters: scores differ from log-sum-exp somewhere
+    lse = gpu_decode(d, finalize=False)
+    mx = gpu_decode(d, finalize=False, lb_overrides=dict(merge=lbm.LB_MERGE_MAX))
+    assert any(len(a[1]) and len(b[1]) and abs(float(a[1][0]) - float(b[1][0])) > 1e-3 for a, b in zip(lse, mx))
+
+
+@pytest.mark.parametrize("name", ["t-c1k", "t-c125k"])
+def test_raw_logits_log_softmax(name):
+    """input = raw scores: each frame is log-softmax-normalised in the kernel.
+    The raw rows are the log-probs plus a seeded per-frame shift."""
+    d = load_workload(name, batch=12)
+    B, T = d.logits.shape[:2]
+    rng = np.random.default_rng(2603)
+    raw = (d.logits.astype(np.float64) + rng.uniform(-20, 20, size=(B, T, 1))).astype(np.float32)
+    say(f"[case] raw logits {name}: B={B}")
+    for fin in (True, False):
+        out = gpu_decode(d, finalize=fin, logits=raw, lb_overrides=dict(input=lbm.LB_INPUT_LOGITS))
+        check_parity(d, out, range(B), name=f"{name}/raw/{'end' if fin else 'live'}", finalize=fin,
+                     logits=raw, oracle_overrides=dict(raw_logits=1))

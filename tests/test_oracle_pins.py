@@ -82,6 +82,54 @@ def test_brute_force_no_pruning(tiny, seed, omega):
     check_against_brute(res, expect)
 
 
+@pytest.mark.parametrize("seed", [0, 1, 2])
+@pytest.mark.parametrize("omega", [0.0, 0.5])
+def test_brute_force_max_recombination(tiny, seed, omega):
+    """merge = max (App. E.1): every complete hypothesis scores its single best
+    alignment (Viterbi) plus bonuses plus its best reading."""
+    lex, lm, orc = tiny
+    T = 7
+    lg = tiny_logits(T, seed)
+    p = DecodeParams(omega=omega, fusion_interval=0)
+    params = oracle.params_from(p, merge_max=1, **BIG)
+    res = orc.decode(lg, params)
+    D = p.alpha * lg.astype(np.float64)
+    expect = bf.complete_hypotheses(D, TINY_CLASSES, TINY_WORDS, p.beta, p.gamma,
+                                    ngram_reading_score(orc, lm, omega), reduce="max")
+    assert len(expect) > 5
+    check_against_brute(res, expect)
+    # the max never exceeds the sum over alignments
+    lse = bf.complete_hypotheses(D, TINY_CLASSES, TINY_WORDS, p.beta, p.gamma,
+                                 ngram_reading_score(orc, lm, omega))
+    assert all(expect[y][0] <= lse[y][0] + 1e-12 for y in expect)
+    assert any(expect[y][0] < lse[y][0] - 1e-3 for y in expect)
+
+
+@pytest.mark.parametrize("seed", [0, 6])
+def test_raw_logits_brute_force(tiny, seed):
+    """Raw scores in: each frame is log-softmax-normalised (scipy's log_softmax
+    on the same fp32 inputs, in fp64) before the search; a per-frame constant
+    shift of the inputs changes nothing."""
+    from scipy.special import log_softmax
+    lex, lm, orc = tiny
+    T = 7
+    rng = np.random.default_rng(100 + seed)
+    raw = rng.standard_normal((T, 41)) * 2.0
+    raw[:, list(TINY_CLASSES)] += 3.0
+    raw = raw.astype(np.float32)
+    p = DecodeParams(omega=0.5, fusion_interval=0)
+    params = oracle.params_from(p, raw_logits=1, **BIG)
+    res = orc.decode(raw, params)
+    D = p.alpha * log_softmax(raw.astype(np.float64), axis=-1)
+    expect = bf.complete_hypotheses(D, TINY_CLASSES, TINY_WORDS, p.beta, p.gamma,
+                                    ngram_reading_score(orc, lm, 0.5))
+    check_against_brute(res, expect)
+    shifted = (raw + np.arange(T, dtype=np.float32)[:, None] * 8.0).astype(np.float32)
+    res2 = orc.decode(shifted, params)
+    assert [list(w) for w in res2.words] == [list(w) for w in res.words]
+    assert np.allclose(res2.total, res.total, atol=1e-5)
+
+
 @pytest.mark.parametrize("seed", [3, 4])
 def test_brute_force_with_fusion(tiny, seed):
     """Final fusion over all entries: total = acoustic + bonuses + max_reading phi*S_fus."""
