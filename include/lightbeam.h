@@ -74,9 +74,12 @@ enum {
  * each in 1..39, at least one per word.  Word ids double as LM vocabulary ids.
  * Words with equal spellings are homophones (Sec. 3.4.1). */
 typedef struct lb_lexicon_desc {
-  int32_t n_words;
-  const int32_t* offsets;  /* [n_words + 1], non-decreasing, offsets[0] == 0 */
-  const int32_t* phonemes; /* [offsets[n_words]] */
+  int32_t n_entries;         /* pronunciations                                      */
+  const int32_t* offsets;    /* [n_entries + 1], increasing, offsets[0] == 0        */
+  const int32_t* phonemes;   /* [offsets[n_entries]], values 1..39                  */
+  const int32_t* entry_word; /* [n_entries]: LM word id spelled by each entry, so a
+                                word may have several pronunciations (App. I);
+                                NULL: entry e spells word e                         */
 } lb_lexicon_desc;
 
 /* 4-gram backoff LM in ARPA form (host memory), queried per (context, word) as
@@ -122,6 +125,11 @@ typedef struct lb_params {
   int64_t arena_nodes_per_stream; /* word-history capacity (0 = beam*subbeams*max_frames) */
   int32_t merge;           /* LB_MERGE_*                                          */
   int32_t input;           /* LB_INPUT_*                                          */
+  int32_t eos_count;       /* end-of-sentence marks (0..3) tried at LB_END with the
+                              synthetic scorer: each sub-beam's sequence is scored
+                              with every mark appended, the best counts and is
+                              appended to the output words (first of equals wins) */
+  int32_t eos_ids[3];      /* the marks' LM word ids                              */
 } lb_params;
 
 typedef struct lb_decoder lb_decoder;

@@ -48,6 +48,7 @@ class _Params(ctypes.Structure):
                 ("fusion_interval", ctypes.c_int32), ("fusion_top_f", ctypes.c_int32),
                 ("fusion_mode", ctypes.c_int32), ("finalize", ctypes.c_int32),
                 ("merge_max", ctypes.c_int32), ("raw_logits", ctypes.c_int32),
+                ("eos_count", ctypes.c_int32), ("eos_ids", ctypes.c_int32 * 3),
                 ("fusion_seed", ctypes.c_uint64),
                 ("fusion_lo", ctypes.c_double), ("fusion_hi", ctypes.c_double)]
 
@@ -63,7 +64,7 @@ def _load():
         lib = ctypes.CDLL(_LIB)
         P = ctypes.c_void_p
         lib.orc_create.restype = P
-        lib.orc_create.argtypes = [ctypes.c_int32, P, P, ctypes.c_int32, ctypes.c_int32,
+        lib.orc_create.argtypes = [ctypes.c_int32, P, P, P, ctypes.c_int32, ctypes.c_int32,
                                    ctypes.c_int32, P] + [P] * 11
         lib.orc_destroy.argtypes = [P]
         lib.orc_last_error.restype = ctypes.c_char_p
@@ -125,7 +126,11 @@ class Oracle:
         ids = [np.ascontiguousarray(a, dtype=np.int32) for a in lm.ids]
         lp = [np.ascontiguousarray(a, dtype=np.float32) for a in lm.logp]
         bo = [np.ascontiguousarray(a, dtype=np.float32) for a in lm.bo[:3]]
-        self._h = lib.orc_create(int(lexicon.n_words), _ptr(offs), _ptr(phs), int(lm.vocab_size),
+        ew = getattr(lexicon, "entry_word", None)
+        ew = None if ew is None else np.ascontiguousarray(ew, dtype=np.int32)
+        self._ew = ew
+        self._h = lib.orc_create(int(lexicon.n_words), _ptr(offs), _ptr(phs), _ptr(ew) if ew is not None else None,
+                                 int(lm.vocab_size),
                                  int(lm.bos), int(lm.unk), _ptr(counts),
                                  _ptr(ids[0]), _ptr(lp[0]), _ptr(bo[0]),
                                  _ptr(ids[1]), _ptr(lp[1]), _ptr(bo[1]),

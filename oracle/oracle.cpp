@@ -104,6 +104,8 @@ struct Params {
   int finalize;         // 1 = end of utterance (final fusion, drop mid-word); 0 = rank the live beam
   int merge_max;        // 0 = contributions to a prefix combine by log-sum-exp; 1 = by max (App. E.1)
   int raw_logits;       // 0 = inputs are log-probabilities; 1 = raw scores, log-softmax per frame first
+  int eos_count;        // end-of-sentence marks tried at the final fusion (synthetic scorer), 0..3
+  int eos_ids[3];       // their word ids
   uint64_t fusion_seed;
   double fusion_lo, fusion_hi;
 };
@@ -184,6 +186,7 @@ struct Model {
 struct Sub {
   double Lw;               // cumulative word-level score (natural log, weighted)
   std::vector<int> words;  // word ids of this orthographic reading
+  int eos = -1;            // end-of-sentence mark chosen at the final fusion (-1: none)
 };
 
 struct Hyp {
@@ -273,14 +276,33 @@ std::vector<Ranked> rank(const std::vector<Hyp>& beam) {
 
 // Delayed fusion (Eq. (2), App. E.4): the fusion score replaces the word-level
 // score of every sub-beam of the selected entries; sub-beams are re-ranked.
+// At the end of the utterance (final = true) each sub-beam's sequence is also
+// tried with every end-of-sentence mark appended; the best mark's score is the
+// sub-beam's, and the mark is kept for the output (the first of equals wins).
 void apply_fusion(const Model& M, const Params& p, std::vector<Hyp>& beam, int top_f, Margins& mg,
-                  Stats& st) {
+                  Stats& st, bool final = false) {
   std::vector<Ranked> r = rank(beam);
   size_t nf = (top_f <= 0) ? r.size() : std::min<size_t>(top_f, r.size());
   if (nf < r.size()) mg.fusion = std::min(mg.fusion, r[nf - 1].total - r[nf].total);
+  const bool eos = final && p.eos_count > 0 && p.fusion_mode == 0;
   for (size_t i = 0; i < nf; ++i) {
     Hyp& h = beam[r[i].idx];
-    for (Sub& s : h.subs) s.Lw = p.phi * fusion_score(M, p, s.words);
+    for (Sub& s : h.subs) {
+      double f = fusion_score(M, p, s.words);
+      if (eos) {
+        const int last = s.words.empty() ? M.lm.bos : s.words.back();
+        double best = kNegInf;
+        for (int k = 0; k < p.eos_count; ++k) {
+          const double v = bigram_score(p, last, p.eos_ids[k]);
+          if (v > best) {
+            best = v;
+            s.eos = p.eos_ids[k];
+          }
+        }
+        f += best;
+      }
+      s.Lw = p.phi * f;
+    }
     std::stable_sort(h.subs.begin(), h.subs.end(),
                      [](const Sub& a, const Sub& b) { return a.Lw > b.Lw; });
     ++st.fusion_events;
@@ -458,7 +480,7 @@ Output decode(const Model& M, const Params& p, const float* logits, int T, bool 
   // End of the utterance: final fusion over every entry, drop entries that
   // stop inside a word, rank the rest.  Without finalisation the live beam is
   // ranked as it stands (the state a streaming decoder reports mid-stream).
-  if (p.finalize && p.fusion_interval > 0) apply_fusion(M, p, beam, 0, out.mg, out.st);
+  if (p.finalize && p.fusion_interval > 0) apply_fusion(M, p, beam, 0, out.mg, out.st, true);
   std::vector<Hyp> done;
   for (Hyp& h : beam)
     if (!p.finalize || partial_word(h.y).empty()) done.push_back(std::move(h));
@@ -485,6 +507,8 @@ struct orc_params {
   int32_t finalize;
   int32_t merge_max;
   int32_t raw_logits;
+  int32_t eos_count;
+  int32_t eos_ids[3];
   uint64_t fusion_seed;
   double fusion_lo, fusion_hi;
 };
@@ -493,22 +517,29 @@ const char* orc_last_error(void) { return g_err.c_str(); }
 
 // Builds the lexicon sets and copies the LM.  Each order's tuples must be
 // sorted lexicographically and unique (checked).  Returns NULL on error.
-void* orc_create(int32_t n_words, const int32_t* lex_offsets, const int32_t* lex_phonemes,
+// Lexicon: n_entries pronunciations (CSR lex_offsets / lex_phonemes); entry e
+// spells word entry_word[e] (entry_word NULL: word e).
+void* orc_create(int32_t n_entries, const int32_t* lex_offsets, const int32_t* lex_phonemes, const int32_t* entry_word,
                  int32_t vocab_size, int32_t bos_id, int32_t unk_id, const int64_t* counts,
                  const int32_t* ids1, const float* p1, const float* bo1,
                  const int32_t* ids2, const float* p2, const float* bo2,
                  const int32_t* ids3, const float* p3, const float* bo3,
                  const int32_t* ids4, const float* p4) {
   Model* M = new Model();
-  for (int32_t w = 0; w < n_words; ++w) {
-    std::vector<int> ph(lex_phonemes + lex_offsets[w], lex_phonemes + lex_offsets[w + 1]);
+  for (int32_t e = 0; e < n_entries; ++e) {
+    std::vector<int> ph(lex_phonemes + lex_offsets[e], lex_phonemes + lex_offsets[e + 1]);
     if (ph.empty()) {
       g_err = "empty word";
       delete M;
       return nullptr;
     }
     for (size_t k = 0; k <= ph.size(); ++k) M->lex.prefixes.insert(std::vector<int>(ph.begin(), ph.begin() + k));
-    M->lex.words[ph].push_back(w);  // ascending: w increases
+    M->lex.words[ph].push_back(entry_word ? entry_word[e] : e);
+  }
+  // homophones of a spelling: distinct word ids, ascending
+  for (auto& kv : M->lex.words) {
+    std::sort(kv.second.begin(), kv.second.end());
+    kv.second.erase(std::unique(kv.second.begin(), kv.second.end()), kv.second.end());
   }
   M->lm.vocab = vocab_size;
   M->lm.bos = bos_id;
@@ -555,6 +586,8 @@ static Params to_params(const orc_params* q) {
   p.finalize = q->finalize;
   p.merge_max = q->merge_max;
   p.raw_logits = q->raw_logits;
+  p.eos_count = q->eos_count;
+  for (int k = 0; k < 3; ++k) p.eos_ids[k] = q->eos_ids[k];
   p.fusion_seed = q->fusion_seed;
   p.fusion_lo = q->fusion_lo;
   p.fusion_hi = q->fusion_hi;
@@ -586,7 +619,8 @@ int32_t orc_decode(void* h, const orc_params* q, const float* logits, int32_t T,
   const int32_t n = static_cast<int32_t>(o.hyps.size());
   for (int32_t i = 0; i < n && i < max_hyps; ++i) {
     const Hyp& x = o.hyps[i];
-    const std::vector<int>& ws = x.subs[0].words;
+    std::vector<int> ws = x.subs[0].words;
+    if (x.subs[0].eos >= 0) ws.push_back(x.subs[0].eos);
     if (out_nwords) out_nwords[i] = static_cast<int32_t>(ws.size());
     if (out_words)
       for (int32_t k = 0; k < max_words; ++k)

@@ -39,7 +39,8 @@ class LBError(RuntimeError):
 
 
 class lb_lexicon_desc(ctypes.Structure):
-    _fields_ = [("n_words", ctypes.c_int32), ("offsets", ctypes.c_void_p), ("phonemes", ctypes.c_void_p)]
+    _fields_ = [("n_entries", ctypes.c_int32), ("offsets", ctypes.c_void_p), ("phonemes", ctypes.c_void_p),
+                ("entry_word", ctypes.c_void_p)]
 
 
 class lb_ngram_desc(ctypes.Structure):
@@ -60,7 +61,8 @@ class lb_params(ctypes.Structure):
                 ("fusion_seed", ctypes.c_uint64), ("fusion_lo", ctypes.c_double),
                 ("fusion_hi", ctypes.c_double), ("lm_load_factor", ctypes.c_double),
                 ("arena_nodes_per_stream", ctypes.c_int64),
-                ("merge", ctypes.c_int32), ("input", ctypes.c_int32)]
+                ("merge", ctypes.c_int32), ("input", ctypes.c_int32),
+                ("eos_count", ctypes.c_int32), ("eos_ids", ctypes.c_int32 * 3)]
 
 
 class lb_stats(ctypes.Structure):
@@ -207,8 +209,8 @@ class Descriptors:
 
 
 def make_descriptors(lexicon, ngram) -> Descriptors:
-    """Descriptors of a lexicon (n_words, offsets, phonemes) and a 4-gram LM
-    (vocab_size, bos, unk, ids[4], logp[4], bo[3])."""
+    """Descriptors of a lexicon (entries: offsets, phonemes, optional entry ->
+    word map) and a 4-gram LM (vocab_size, bos, unk, ids[4], logp[4], bo[3])."""
     keep = []
 
     def arr(a, dt):
@@ -218,7 +220,9 @@ def make_descriptors(lexicon, ngram) -> Descriptors:
 
     offs = arr(lexicon.offsets, np.int32)
     phs = arr(lexicon.phonemes, np.int32)
-    lex = lb_lexicon_desc(int(lexicon.n_words), offs.ctypes.data, phs.ctypes.data)
+    ew = getattr(lexicon, "entry_word", None)
+    ewp = arr(ew, np.int32).ctypes.data if ew is not None else None
+    lex = lb_lexicon_desc(int(lexicon.n_words), offs.ctypes.data, phs.ctypes.data, ewp)
     lm = lb_ngram_desc()
     lm.vocab_size = int(ngram.vocab_size)
     lm.bos_id = int(ngram.bos)

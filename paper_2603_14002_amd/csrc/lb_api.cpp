@@ -16,9 +16,9 @@
 
 using namespace lb;
 
-static_assert(sizeof(lb_params) == 136, "lb_params layout");
+static_assert(sizeof(lb_params) == 152, "lb_params layout");
 static_assert(sizeof(lb_ngram_desc) == 144, "lb_ngram_desc layout");
-static_assert(sizeof(lb_lexicon_desc) == 24, "lb_lexicon_desc layout");
+static_assert(sizeof(lb_lexicon_desc) == 32, "lb_lexicon_desc layout");
 static_assert(sizeof(lb_stats) == 248, "lb_stats layout");
 
 namespace {
@@ -52,7 +52,7 @@ HostTrie build_trie(const lb_lexicon_desc& lex) {
   std::vector<std::array<int32_t, 40>> ch(1);
   ch[0].fill(-1);
   std::vector<std::vector<int32_t>> at(1);
-  for (int32_t w = 0; w < lex.n_words; ++w) {
+  for (int32_t w = 0; w < lex.n_entries; ++w) {
     int32_t n = 0;
     for (int32_t k = lex.offsets[w]; k < lex.offsets[w + 1]; ++k) {
       const int p = lex.phonemes[k];
@@ -64,7 +64,12 @@ HostTrie build_trie(const lb_lexicon_desc& lex) {
       }
       n = ch[n][p];
     }
-    at[n].push_back(w);
+    at[n].push_back(lex.entry_word ? lex.entry_word[w] : w);
+  }
+  // a node's words: distinct ids, ascending (two entries of one word may share a spelling)
+  for (auto& v : at) {
+    std::sort(v.begin(), v.end());
+    v.erase(std::unique(v.begin(), v.end()), v.end());
   }
   const size_t N = ch.size();
   std::vector<int32_t> order;  // BFS order of old ids
@@ -207,16 +212,22 @@ namespace {
 
 lb_status validate(const lb_lexicon_desc* lex, const lb_ngram_desc* lm, const lb_params* p) {
   if (!lex || !lm || !p) return fail(LB_ERR_INVALID_ARG, "null descriptor");
-  if (lex->n_words < 1 || !lex->offsets || !lex->phonemes) return fail(LB_ERR_INVALID_ARG, "empty lexicon");
+  if (lex->n_entries < 1 || !lex->offsets || !lex->phonemes) return fail(LB_ERR_INVALID_ARG, "empty lexicon");
   if (lex->offsets[0] != 0) return fail(LB_ERR_INVALID_ARG, "lexicon offsets[0] != 0");
-  for (int32_t w = 0; w < lex->n_words; ++w) {
+  for (int32_t w = 0; w < lex->n_entries; ++w) {
     if (lex->offsets[w + 1] <= lex->offsets[w])
       return fail(LB_ERR_INVALID_ARG, "word " + std::to_string(w) + " has no phonemes");
     for (int32_t k = lex->offsets[w]; k < lex->offsets[w + 1]; ++k)
       if (lex->phonemes[k] < 1 || lex->phonemes[k] > 39)
         return fail(LB_ERR_INVALID_ARG, "phoneme out of 1..39 in word " + std::to_string(w));
   }
-  if (lm->vocab_size < lex->n_words + 1) return fail(LB_ERR_INVALID_ARG, "LM vocabulary smaller than the lexicon");
+  if (lex->entry_word) {
+    for (int32_t e = 0; e < lex->n_entries; ++e)
+      if (lex->entry_word[e] < 0 || lex->entry_word[e] >= lm->vocab_size)
+        return fail(LB_ERR_INVALID_ARG, "entry " + std::to_string(e) + ": word id outside the LM vocabulary");
+  } else if (lm->vocab_size < lex->n_entries + 1) {
+    return fail(LB_ERR_INVALID_ARG, "LM vocabulary smaller than the lexicon");
+  }
   if (lm->bos_id < 0 || lm->bos_id >= lm->vocab_size || lm->unk_id < 0 || lm->unk_id >= lm->vocab_size)
     return fail(LB_ERR_INVALID_ARG, "bos/unk id out of range");
   for (int n = 0; n < 4; ++n) {
@@ -237,6 +248,12 @@ lb_status validate(const lb_lexicon_desc* lex, const lb_ngram_desc* lm, const lb
   if (p->input != LB_INPUT_LOGPROBS && p->input != LB_INPUT_LOGITS)
     return fail(LB_ERR_INVALID_ARG, "input must be LB_INPUT_LOGPROBS or LB_INPUT_LOGITS");
   if (p->fusion_top_f < 0) return fail(LB_ERR_INVALID_ARG, "fusion_top_f < 0");
+  if (p->eos_count < 0 || p->eos_count > 3) return fail(LB_ERR_INVALID_ARG, "eos_count must be in 0..3");
+  if (p->eos_count > 0 && p->fusion_source != LB_FUSION_SYNTH_BIGRAM)
+    return fail(LB_ERR_INVALID_ARG, "end-of-sentence marks are scored by the synthetic fusion scorer only");
+  for (int k = 0; k < p->eos_count; ++k)
+    if (p->eos_ids[k] < 0 || p->eos_ids[k] >= lm->vocab_size)
+      return fail(LB_ERR_INVALID_ARG, "eos_ids outside the LM vocabulary");
   const double lf = p->lm_load_factor == 0.0 ? 0.5 : p->lm_load_factor;
   if (!(lf > 0.0 && lf <= 0.9)) return fail(LB_ERR_INVALID_ARG, "lm_load_factor must be in (0, 0.9]");
   for (double x : {p->alpha, p->beta, p->gamma, p->omega, p->phi, p->theta, p->lambda, p->fusion_lo, p->fusion_hi})
@@ -449,6 +466,8 @@ lb_status lb_create(const lb_lexicon_desc* lex, const lb_ngram_desc* lm, const l
   P.bos = lm->bos_id;
   P.merge_max = p.merge == LB_MERGE_MAX ? 1 : 0;
   P.raw_input = p.input == LB_INPUT_LOGITS ? 1 : 0;
+  P.eos_count = p.eos_count;
+  for (int k = 0; k < 3; ++k) P.eos_ids[k] = p.eos_ids[k];
   P.alpha = p.alpha;
   P.beta = p.beta;
   P.gamma = p.gamma;

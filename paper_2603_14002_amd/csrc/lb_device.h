@@ -101,7 +101,8 @@ struct DevParams {
   int32_t bos;
   int32_t merge_max;  // 1: paths into one prefix combine by max, 0: by log-sum-exp
   int32_t raw_input;  // 1: per-frame scores are raw, log-softmax them first
-  int32_t pad;
+  int32_t eos_count;  // end-of-sentence marks tried at the final synthetic fusion
+  int32_t eos_ids[3];
   double alpha, beta, gamma, comega, phi, theta, lam;
   uint64_t seed;
   double lo, hi;

@@ -1352,8 +1352,26 @@ __device__ void select_fused(const DevParams& P, const DevState& S, int b, int t
 // sub-beam's word-level score becomes phi * its fusion score -- the synthetic
 // score kept in its history node, or the caller's ext[b][rank][j] -- and the
 // sub-beams are re-ranked (stable).
+// The best end-of-sentence mark after `word` by the synthetic scorer (the
+// first of equal scores), or -1 without marks.
+__device__ inline int32_t best_eos(const DevParams& P, int32_t word, double* score) {
+  int32_t best = -1;
+  double bs = kNegInf;
+  for (int k = 0; k < P.eos_count; ++k) {
+    const double v = bigram_score(P, word, P.eos_ids[k]);
+    if (v > bs) {
+      bs = v;
+      best = P.eos_ids[k];
+    }
+  }
+  *score = bs;
+  return best;
+}
+
+// With `eos` (the final synthetic fusion) each sub-beam's fusion score also
+// takes its best end-of-sentence mark.
 template <int BLOCK>
-__device__ void apply_fused(const DevParams& P, const DevState& S, int b, const float* ext) {
+__device__ void apply_fused(const DevParams& P, const DevState& S, int b, const float* ext, bool eos = false) {
   const int tid = threadIdx.x;
   const size_t gb = static_cast<size_t>(b) * P.K;
   const int F = S.fsel_n[b];
@@ -1367,7 +1385,18 @@ __device__ void apply_fused(const DevParams& P, const DevState& S, int b, const 
     for (int j = 0; j < kMaxSub; ++j) {
       if (j < nsub) {
         h[j] = S.hist[bi * P.O + j];
-        const double f = ext ? static_cast<double>(ext[(gb + tid) * P.O + j]) : S.arena[h[j]].sfus;
+        double f;
+        if (ext) {
+          f = static_cast<double>(ext[(gb + tid) * P.O + j]);
+        } else {
+          const HistNode hn = S.arena[h[j]];
+          f = hn.sfus;
+          if (eos) {
+            double e;
+            (void)best_eos(P, hn.word, &e);
+            f += e;
+          }
+        }
         L[j] = P.phi * f;
       } else {
         L[j] = kNegInf;
@@ -1478,7 +1507,7 @@ __global__ __launch_bounds__(BLOCK) void k_output(const DevParams P, const DevSt
   __shared__ int32_t sScan[BLOCK / 64];
   if (fin && P.fusion_source == 1 && P.fusion_interval > 0) {
     select_fused<BLOCK>(P, S, b, 0, sc, ky, ix);
-    apply_fused<BLOCK>(P, S, b, nullptr);
+    apply_fused<BLOCK>(P, S, b, nullptr, P.eos_count > 0);
   }
   const int n = S.nbeam[b];
   const size_t gb = static_cast<size_t>(b) * P.K;
@@ -1506,11 +1535,19 @@ __global__ __launch_bounds__(BLOCK) void k_output(const DevParams P, const DevSt
       int len = 0;
       for (uint32_t x = h; x != kRootHist && static_cast<uint64_t>(len) <= S.arena_cap; x = S.arena[x].parent)
         ++len;
-      if (len > P.W) atomicOr(S.flags, kFlagWords);
+      // at the end of an utterance with end-of-sentence marks, the best mark follows the words
+      int32_t mark = -1;
+      if (fin && P.fusion_source == 1 && P.fusion_interval > 0 && P.eos_count > 0) {
+        double e;
+        mark = best_eos(P, S.arena[h].word, &e);
+      }
+      const int n = len + (mark >= 0 ? 1 : 0);
+      if (n > P.W) atomicOr(S.flags, kFlagWords);
       int k = len - 1;
       for (uint32_t x = h; x != kRootHist && k >= 0; x = S.arena[x].parent, --k)
         if (k < P.W) row[k] = S.arena[x].word;
-      for (int k2 = len; k2 < P.W; ++k2) row[k2] = -1;
+      if (mark >= 0 && len < P.W) row[len] = mark;
+      for (int k2 = n; k2 < P.W; ++k2) row[k2] = -1;
     } else {
       out_scores[static_cast<size_t>(b) * P.K + r] = kNegInf;
       for (int k2 = 0; k2 < P.W; ++k2) row[k2] = -1;

@@ -61,11 +61,19 @@ def segments(y: Tuple[int, ...]):
 
 def complete_hypotheses(D: np.ndarray, classes: Sequence[int], lex_words: List[Tuple[int, ...]],
                         beta: float, gamma: float,
-                        reading_score: Callable[[List[int]], float], reduce: str = "lse"):
-    """{y: (total, best reading)} over every lexicon-valid complete hypothesis."""
+                        reading_score: Callable[[List[int]], float], reduce: str = "lse",
+                        entry_word: Sequence[int] = None):
+    """{y: (total, best reading)} over every lexicon-valid complete hypothesis.
+
+    ``lex_words[e]`` spells word ``entry_word[e]`` (default: word e)."""
     homs: Dict[Tuple[int, ...], List[int]] = {}
-    for w, ph in enumerate(lex_words):
-        homs.setdefault(tuple(ph), []).append(w)
+    for e, ph in enumerate(lex_words):
+        w = e if entry_word is None else int(entry_word[e])
+        lst = homs.setdefault(tuple(ph), [])
+        if w not in lst:
+            lst.append(w)
+    for k in homs:
+        homs[k].sort()
     out = {}
     for y, lse in alignment_lse(D, classes, reduce).items():
         words, partial = segments(y)

@@ -31,9 +31,9 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_struct_sizes_match_header_layout():
-    assert ctypes.sizeof(lbm.lb_params) == 136
+    assert ctypes.sizeof(lbm.lb_params) == 152
     assert ctypes.sizeof(lbm.lb_ngram_desc) == 144
-    assert ctypes.sizeof(lbm.lb_lexicon_desc) == 24
+    assert ctypes.sizeof(lbm.lb_lexicon_desc) == 32
     assert ctypes.sizeof(lbm.lb_stats) == 248
 
 
@@ -53,6 +53,7 @@ def _create(d, params):
     ("beam", 0), ("beam", 257), ("subbeams", 0), ("subbeams", 5), ("max_batch", 0), ("max_frames", 0),
     ("max_words_out", 0), ("fusion_source", 7), ("fusion_top_f", -1), ("theta", -1.0), ("lambda_", float("nan")),
     ("lm_load_factor", 0.95), ("arena_nodes_per_stream", -5), ("merge", 2), ("merge", -1), ("input", 2),
+    ("eos_count", 4), ("eos_count", -1),
 ])
 def test_create_rejects_bad_params(field, value):
     d = _descs()

@@ -246,3 +246,32 @@ def test_raw_logits_log_softmax(name):
         out = gpu_decode(d, finalize=fin, logits=raw, lb_overrides=dict(input=lbm.LB_INPUT_LOGITS))
         check_parity(d, out, range(B), name=f"{name}/raw/{'end' if fin else 'live'}", finalize=fin,
                      logits=raw, oracle_overrides=dict(raw_logits=1))
+
+
+# ---------------------------------------------------------------- pronunciation variants, end-of-sentence marks
+
+
+def test_pronunciation_variants():
+    """A lexicon where a fifth of the words have a second spelling (App. I)."""
+    d = load_workload("t-variants")
+    B = d.logits.shape[0]
+    assert d.lexicon.entry_word is not None and d.lexicon.n_words > d.lm.vocab_size - 3
+    say(f"[case] variants: B={B} entries={d.lexicon.n_words}")
+    for fin in (True, False):
+        out = gpu_decode(d, finalize=fin)
+        check_parity(d, out, range(B), name=f"variants/{'end' if fin else 'live'}", finalize=fin)
+
+
+@pytest.mark.parametrize("name", ["t-c1k", "t-c20k"])
+def test_end_of_sentence_marks(name):
+    """At LB_END every sub-beam takes its best end-of-sentence mark under the
+    synthetic scorer; the mark is appended to the output words."""
+    import ctypes
+    d = load_workload(name)
+    B = d.logits.shape[0]
+    marks = (ctypes.c_int32 * 3)(d.lm.eos, d.lm.unk, 3)
+    say(f"[case] end-of-sentence marks {name}: B={B}")
+    out = gpu_decode(d, lb_overrides=dict(eos_count=3, eos_ids=marks))
+    check_parity(d, out, range(B), name=f"{name}/eos", oracle_overrides=dict(eos_count=3, eos_ids=marks))
+    ends = [ws[-1] for words, _ in out for ws in words if ws]
+    assert ends and all(w in (d.lm.eos, d.lm.unk, 3) for w in ends)

@@ -10,6 +10,7 @@
 * fusion identity: fusing with the n-gram LM's own score changes nothing.
 """
 
+import ctypes
 import math
 
 import numpy as np
@@ -144,6 +145,63 @@ def test_brute_force_with_fusion(tiny, seed):
                                     lambda ws: p.phi * orc.fusion_score(params, ws))
     check_against_brute(res, expect)
     assert res.stats["fused"] > 0
+
+
+def test_brute_force_end_of_sentence_marks(tiny):
+    """The final fusion with end-of-sentence marks: every reading's fusion
+    score takes its best mark (the first of equals), and the mark follows the
+    words of the output."""
+    lex, lm, orc = tiny
+    T = 7
+    lg = tiny_logits(T, 8)
+    marks = [lm.eos, lm.unk, 2]
+    p = DecodeParams(fusion_interval=3, fusion_top_f=0)
+    params = oracle.params_from(p, fusion_seed=99, eos_count=3, eos_ids=(ctypes.c_int32 * 3)(*marks), **BIG)
+    res = orc.decode(lg, params)
+    D = p.alpha * lg.astype(np.float64)
+
+    def best_mark(ws):
+        last = ws[-1] if ws else lm.bos
+        vals = [orc.fusion_score(params, [last, m]) - orc.fusion_score(params, [last]) for m in marks]
+        k = int(np.argmax(vals))  # first of equals
+        return vals[k], marks[k]
+
+    expect = bf.complete_hypotheses(D, TINY_CLASSES, TINY_WORDS, p.beta, p.gamma,
+                                    lambda ws: p.phi * (orc.fusion_score(params, ws) + best_mark(ws)[0]))
+    expect = {y: (t, r + [best_mark(r)[1]], a) for y, (t, r, a) in expect.items()}
+    check_against_brute(res, expect)
+
+
+@pytest.mark.parametrize("omega,fusion", [(0.5, 0), (0.0, 2)])
+def test_brute_force_pronunciation_variants(omega, fusion):
+    """Several entries per word (App. I): a word is reachable through each of
+    its spellings, and a spelling's homophones are distinct word ids."""
+    words = [(1,), (2, 2), (1, 2), (3, 1), (2,)]
+    entries = words + [(3,), (1, 2), (2, 1)]      # variants of words 0, 2 (same spelling again) and 4
+    entry_word = list(range(len(words))) + [0, 2, 4]
+    lex = lexicon_from(entries)
+    lex.entry_word = np.array(entry_word, dtype=np.int32)
+    lm = random_small_lm(len(words), 40)
+    orc = oracle.Oracle(lex, lm)
+    T = 7
+    lg = tiny_logits(T, 11)
+    p = DecodeParams(omega=omega, fusion_interval=fusion, fusion_top_f=0)
+    params = oracle.params_from(p, fusion_seed=7, **BIG)
+    res = orc.decode(lg, params)
+    D = p.alpha * lg.astype(np.float64)
+    if fusion:
+        score = lambda ws: p.phi * orc.fusion_score(params, ws)
+    else:
+        score = ngram_reading_score(orc, lm, omega)
+    expect = bf.complete_hypotheses(D, TINY_CLASSES, entries, p.beta, p.gamma, score, entry_word=entry_word)
+    # word 0 is reachable through its variant spelling (3,), which spells nothing else
+    via_variant = False
+    for y, (_, r, _) in expect.items():
+        ws, _ = bf.segments(y)
+        via_variant |= any(w == (3,) and r[i] == 0 for i, w in enumerate(ws))
+    assert via_variant
+    check_against_brute(res, expect)
+    orc.close()
 
 
 def ctc_forward(lg, alpha, labels):

@@ -27,6 +27,7 @@ class LexiconSpec:
     name: str
     n_words: int
     max_len: int          # word lengths ~ U{1..max_len} phonemes
+    variant_frac: float = 0.0  # share of words given a second pronunciation (one phoneme edited)
 
 
 @dataclass(frozen=True)
@@ -82,6 +83,9 @@ LM_200M = LMSpec("lm200m", LEX_125K, 200_000_000)
 # Reduced LMs over the same lexicons, for parity tests the oracle finishes quickly.
 LM_20K_SMALL = LMSpec("lm20k-200k", LEX_20K, 200_000)
 LM_125K_SMALL = LMSpec("lm125k-2m", LEX_125K, 2_000_000)
+# 20k words, a fifth of them with a second pronunciation (App. I's word(2) entries)
+LEX_20K_VAR = LexiconSpec("lex20k-var", 20_000, 8, variant_frac=0.2)
+LM_20K_VAR = LMSpec("lm20kvar-200k", LEX_20K_VAR, 200_000)
 
 _P = DecodeParams()
 
@@ -119,6 +123,9 @@ CONFIGS = {
     "t-k256": Workload(
         "t-k256", batch=2, frames=80, lm=LM_125K_SMALL, sigma=1.5,
         params=replace(_P, beam=256, fusion_interval=16, fusion_top_f=32)),
+    "t-variants": Workload(
+        "t-variants", batch=5, frames=120, lm=LM_20K_VAR, sigma=1.0, ragged=True,
+        params=replace(_P, beam=32, fusion_interval=20, fusion_top_f=0)),
     "t-stream": Workload(
         "t-stream", batch=4, frames=90, lm=LM_125K_SMALL, sigma=1.5, chunk=10, ragged=True,
         params=replace(_P, beam=64, fusion_interval=8, fusion_top_f=0)),

@@ -45,18 +45,32 @@ def _log(msg: str) -> None:
 
 @dataclass
 class Lexicon:
-    """Word -> phoneme-sequence dictionary in CSR form.
+    """Pronunciation dictionary in CSR form.
 
-    ``offsets[w] .. offsets[w+1]`` index ``phonemes`` (values 1..39).  Word ids
-    are 0..n_words-1; they are also the LM vocabulary ids of the words.
+    Entry e spells ``phonemes[offsets[e] .. offsets[e+1]]`` (values 1..39) and
+    stands for word ``entry_word[e]`` (None: word e).  Without variants there
+    is one entry per word and ``n_words`` is also the number of words; word ids
+    are the LM vocabulary ids of the words.
     """
 
-    n_words: int
+    n_words: int          # entries
     offsets: np.ndarray   # int32 [n_words + 1]
     phonemes: np.ndarray  # int32 [offsets[-1]]
+    entry_word: Optional[np.ndarray] = None  # int32 [n_words]
 
-    def word(self, w: int) -> np.ndarray:
-        return self.phonemes[self.offsets[w]:self.offsets[w + 1]]
+    def word(self, e: int) -> np.ndarray:
+        return self.phonemes[self.offsets[e]:self.offsets[e + 1]]
+
+    def pronunciations(self, w: int) -> List[int]:
+        """Entries spelling word w (its default entry w first)."""
+        if self.entry_word is None:
+            return [w]
+        if not hasattr(self, "_prons"):
+            prons: dict = {}
+            for e, x in enumerate(self.entry_word.tolist()):
+                prons.setdefault(x, []).append(e)
+            self._prons = prons
+        return self._prons.get(w, [w])
 
 
 def make_lexicon(spec: LexiconSpec) -> Lexicon:
@@ -65,7 +79,29 @@ def make_lexicon(spec: LexiconSpec) -> Lexicon:
     offsets = np.zeros(spec.n_words + 1, dtype=np.int32)
     np.cumsum(lens, out=offsets[1:])
     phonemes = rng.integers(1, N_PHONEMES + 1, size=int(offsets[-1])).astype(np.int32)
-    return Lexicon(spec.n_words, offsets, phonemes)
+    if spec.variant_frac <= 0:
+        return Lexicon(spec.n_words, offsets, phonemes)
+    # a second pronunciation for a share of the words: one phoneme substituted,
+    # inserted or deleted
+    n_var = int(round(spec.variant_frac * spec.n_words))
+    base = np.sort(rng.choice(spec.n_words, size=n_var, replace=False))
+    extra: List[np.ndarray] = []
+    for w in base.tolist():
+        ph = phonemes[offsets[w]:offsets[w + 1]].tolist()
+        op = int(rng.integers(0, 4))
+        k = int(rng.integers(0, len(ph)))
+        if op == 2:
+            ph.insert(k, int(rng.integers(1, N_PHONEMES + 1)))
+        elif op == 3 and len(ph) > 1:
+            del ph[k]
+        else:
+            ph[k] = 1 + (ph[k] - 1 + int(rng.integers(1, N_PHONEMES))) % N_PHONEMES
+        extra.append(np.array(ph, dtype=np.int32))
+    lens2 = np.array([len(x) for x in extra], dtype=np.int64)
+    offsets2 = np.concatenate([offsets, offsets[-1] + np.cumsum(lens2)]).astype(np.int32)
+    phonemes2 = np.concatenate([phonemes] + extra).astype(np.int32)
+    entry_word = np.concatenate([np.arange(spec.n_words), base]).astype(np.int32)
+    return Lexicon(spec.n_words + n_var, offsets2, phonemes2, entry_word)
 
 
 # --------------------------------------------------------------------------- n-gram LM
@@ -312,7 +348,9 @@ def make_targets(lex: Lexicon, sampler: _Sampler, frames: int, rng: np.random.Ge
         words = sampler.sentence(n, rng)
         stop = False
         for w in words:
-            syms = list(lex.word(w)) + [SEP]
+            prons = lex.pronunciations(w)
+            e = prons[int(rng.integers(0, len(prons)))] if len(prons) > 1 else prons[0]
+            syms = list(lex.word(e)) + [SEP]
             seg: List[int] = []
             p = prev
             for s in syms:
