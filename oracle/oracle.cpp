@@ -30,6 +30,13 @@
 //    entries inside a word are dropped and the rest are ranked.
 //  * Ties are broken by a 64-bit key of the prefix (splitmix64 chain), and
 //    sub-beam ties by (parent sub-beam index, word id).
+//  * Options: recombination by max instead of log-sum-exp (the best alignment,
+//    App. E.1); raw per-frame scores normalised by a log-softmax first;
+//    lexicon entries that spell a given word id (pronunciation variants,
+//    App. I; a spelling's homophones are its distinct word ids, ascending);
+//    end-of-sentence marks tried at the final fusion (each sub-beam takes its
+//    best mark under the synthetic scorer, the first of equals, and the mark
+//    follows the output words).
 
 #include <algorithm>
 #include <cmath>
