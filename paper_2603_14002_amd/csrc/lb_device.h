@@ -75,14 +75,15 @@ struct NgramTable {
 // Word-history node: the word sequence (parent chain) of an orthographic
 // sub-beam plus the n-gram state after its last word: the word itself (the
 // 1-word context), the slots of the 2- and 3-word contexts (kNone if absent)
-// and the three backoff weights, and the running synthetic fusion score.
+// and the three backoff weights, the number of words in the chain, and the
+// running synthetic fusion score.
 struct HistNode {
   uint32_t parent;
   int32_t word;
   uint32_t c2;
   uint32_t c3;
   float bo1, bo2, bo3;
-  uint32_t pad;
+  uint32_t depth;
   double sfus;
 };
 

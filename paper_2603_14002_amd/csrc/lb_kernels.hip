@@ -1180,12 +1180,9 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
         hn.bo1 = st.bo1;
         hn.bo2 = st.bo2;
         hn.bo3 = st.bo3;
-        hn.pad = 0;
-        hn.sfus = 0.0;
-        if (synth) {
-          const HistNode ctx = S.arena[ph];
-          hn.sfus = ctx.sfus + bigram_score(P, ctx.word, w);
-        }
+        const HistNode par = S.arena[ph];
+        hn.depth = par.depth + 1;
+        hn.sfus = synth ? par.sfus + bigram_score(P, par.word, w) : 0.0;
         const uint32_t node = arena0 + abase + static_cast<uint32_t>(lane);
         S.arena[node] = hn;
         N.Lw[rr * kMaxSub + lane] = myL;
@@ -1469,8 +1466,7 @@ __global__ __launch_bounds__(BLOCK) void k_fuse_export(const DevParams P, const 
       const int nsub = (S.meta[bi] >> 8) & 0xFF;
       if (j < nsub) {
         const uint32_t h = S.hist[bi * P.O + j];
-        len = 0;
-        for (uint32_t x = h; x != kRootHist && static_cast<uint64_t>(len) <= S.arena_cap; x = S.arena[x].parent) ++len;
+        len = static_cast<int>(S.arena[h].depth);
         if (len > P.W) atomicOr(S.flags, kFlagWords);
         int k = len - 1;
         for (uint32_t x = h; x != kRootHist && k >= 0; x = S.arena[x].parent, --k)
@@ -1531,15 +1527,14 @@ __global__ __launch_bounds__(BLOCK) void k_output(const DevParams P, const DevSt
     if (r < m) {
       const size_t bi = gb + ix[r];
       out_scores[static_cast<size_t>(b) * P.K + r] = static_cast<float>(sc[r]);
-      uint32_t h = S.hist[bi * P.O];
-      int len = 0;
-      for (uint32_t x = h; x != kRootHist && static_cast<uint64_t>(len) <= S.arena_cap; x = S.arena[x].parent)
-        ++len;
+      const uint32_t h = S.hist[bi * P.O];
+      const HistNode top = S.arena[h];
+      const int len = static_cast<int>(top.depth);
       // at the end of an utterance with end-of-sentence marks, the best mark follows the words
       int32_t mark = -1;
       if (fin && P.fusion_source == 1 && P.fusion_interval > 0 && P.eos_count > 0) {
         double e;
-        mark = best_eos(P, S.arena[h].word, &e);
+        mark = best_eos(P, top.word, &e);
       }
       const int n = len + (mark >= 0 ? 1 : 0);
       if (n > P.W) atomicOr(S.flags, kFlagWords);
