@@ -1,6 +1,6 @@
 """Throughput of the MI355X LightBeam decoding path on one GPU.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c4]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c4] [--fusion-scorer lm]
 
 One step decodes one whole batch of the workload (LB_BEGIN | LB_END over all
 frames; streaming workloads are fed chunk by chunk) with the inputs already in
@@ -8,6 +8,9 @@ HBM.  Prints ONE JSON line: beam-token expansions per second (value), decoded
 audio-seconds per wall-second, per-stream real-time factor, the HBM roofline of
 the dominant kernel (per-launch durations from HIP events recorded on the
 decode stream) and the CPU oracle timed on a bounded sample of the workload.
+With --fusion-scorer lm the fusion scores travel the external round trip
+(lb_fusion_request / lb_fusion_scores) from a small random causal word LM, and
+the line adds the round trip's breakdown (no CPU baseline in that mode).
 """
 
 from __future__ import annotations
@@ -43,6 +46,9 @@ def parse():
                     help="utterances decoded by the CPU oracle (0 = four per host thread, at most 16 threads)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true", help="skip per-kernel event timing")
+    ap.add_argument("--fusion-scorer", choices=("synthetic", "lm"), default="synthetic",
+                    help="lm: fusion scores come back through the external round trip from a small "
+                         "randomly initialised causal word LM (the LLM stand-in)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (reads and writes MIB MiB) and exit; "
                          "its FETCH_SIZE / WRITE_SIZE counters calibrate the HBM traffic figures")
@@ -183,7 +189,11 @@ def main():
     B, T = d.logits.shape[:2]
     log(f"workload {wl.name}: B={B} T={T} K={p.beam} lm={d.lm.counts} ({time.time() - t0:.1f}s)")
     t0 = time.time()
-    lp = lbm.make_params(p, max_batch=B, max_frames=T, fusion_seed=d.fusion_seed)
+    external = args.fusion_scorer == "lm"
+    if external and p.fusion_interval <= 0:
+        raise SystemExit(f"workload {wl.name} has no fusion")
+    lp = lbm.make_params(p, max_batch=B, max_frames=T, fusion_seed=d.fusion_seed,
+                         fusion_source=lbm.LB_FUSION_EXTERNAL if external else None)
     dec = lbm.Decoder(d.lexicon, d.lm, lp)
     log(f"lb_create {time.time() - t0:.1f}s")
     dev = torch.device("cuda:0")
@@ -205,8 +215,20 @@ def main():
     else:
         chunks = [(logits, torch.from_numpy(lengths_np).to(dev), T, lbm.LB_BEGIN | lbm.LB_END)]
 
+    rt = None
+    if external:
+        from workloads.fusion_lm import CausalWordLM, RoundTripStats, decode_external
+        flm = CausalWordLM(d.lm.vocab_size, d.lm.bos, seed=d.fusion_seed & 0xFFFFFFFF).to(dev)
+        fwords = torch.empty((B, K, lp.subbeams, W), dtype=torch.int32, device=dev)
+        fnw = torch.empty((B, K, lp.subbeams), dtype=torch.int32, device=dev)
+        rt = RoundTripStats()
+
     def step():
         for lg, ln, tc, fl in chunks:
+            if external:
+                decode_external(lbm, dec, lg, ln, fl, flm.score, hyps, scores, fwords, fnw, stream=stream,
+                                stats=rt)
+                continue
             st = lbm.lb_decode_batch(dec.handle, lg, ln, B, tc, fl, stream, hyps, scores)
             assert st == lbm.LB_OK
 
@@ -233,7 +255,10 @@ def main():
         return ev0.elapsed_time(ev1), lbm.lb_get_stats(dec.handle)
 
     # (1) the timed region: no per-kernel events
+    if rt is not None:
+        rt.__init__()
     wall_ms, s = timed_pass(0)
+    rt_clean = None if rt is None else dict(rt.__dict__)
     ms = wall_ms / args.steps
     exp_per_step = s.expansions / args.steps
     audio = float(lengths_np.sum()) * FRAME_SECONDS
@@ -288,6 +313,22 @@ def main():
         "kernels": kern,
         "roofline": roof,
     }
+    if external:
+        n = args.steps
+        out["config"]["fusion_scorer"] = ("external round trip: causal word LM (d=256, 2 layers, 4 heads, "
+                                          "random init, fp32), distinct sequences in batches of 256")
+        out["round_trip"] = {
+            "events_per_step": rt_clean["events"] / n,
+            "sequences_requested_per_step": rt_clean["requested"] / n,
+            "distinct_scored_per_step": rt_clean["scored"] / n,
+            "scorer_batches_per_step": rt_clean["batches"] / n,
+            "scorer_gpu_ms_per_step": rt_clean["scorer_ms"] / n,
+            "decoder_kernels_ms_per_step": sum(v["total_ms"] for k, v in kern.items() if k != "dominant") / n
+            if kern else None,
+            "note": "scorer_gpu_ms from events around the caller's scoring (torch stream); kernel time from "
+                    "the profiled pass; the rest of ms_per_step is host round trips and syncs",
+        }
+        args.no_cpu_baseline = True
     if not args.no_cpu_baseline:
         threads = min(os.cpu_count() or 1, 16)
         n = args.cpu_sample or 4 * threads

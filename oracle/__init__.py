@@ -40,6 +40,10 @@ def build(force: bool = True) -> str:
     return _LIB
 
 
+# fusion_mode 2: the caller's scorer, S(words[0..n)) in natural log
+SCORER_FN = ctypes.CFUNCTYPE(ctypes.c_double, ctypes.POINTER(ctypes.c_int32), ctypes.c_int32, ctypes.c_void_p)
+
+
 class _Params(ctypes.Structure):
     _fields_ = [("beam", ctypes.c_int32), ("subbeams", ctypes.c_int32),
                 ("alpha", ctypes.c_double), ("beta", ctypes.c_double), ("gamma", ctypes.c_double),
@@ -50,7 +54,8 @@ class _Params(ctypes.Structure):
                 ("merge_max", ctypes.c_int32), ("raw_logits", ctypes.c_int32),
                 ("eos_count", ctypes.c_int32), ("eos_ids", ctypes.c_int32 * 3),
                 ("fusion_seed", ctypes.c_uint64),
-                ("fusion_lo", ctypes.c_double), ("fusion_hi", ctypes.c_double)]
+                ("fusion_lo", ctypes.c_double), ("fusion_hi", ctypes.c_double),
+                ("scorer", SCORER_FN), ("scorer_ctx", ctypes.c_void_p)]
 
 
 _lib = None
@@ -103,15 +108,26 @@ class OracleResult:
         return float(min(self.margins.values()))
 
 
-def params_from(p, fusion_seed: int = 0, fusion_mode: int = 0, **overrides) -> _Params:
-    """orc params from a ``workloads.DecodeParams`` (plus overrides)."""
+def params_from(p, fusion_seed: int = 0, fusion_mode: int = 0, scorer=None, **overrides) -> _Params:
+    """orc params from a ``workloads.DecodeParams`` (plus overrides).
+
+    ``scorer``: a Python function of a word-id list returning its fusion score
+    (natural log); it selects fusion_mode 2."""
+    cb = None
+    if scorer is not None:
+        fusion_mode = 2
+        cb = SCORER_FN(lambda w, n, _ctx: float(scorer([int(w[i]) for i in range(n)])))
     d = dict(beam=p.beam, subbeams=p.subbeams, alpha=p.alpha, beta=p.beta, gamma=p.gamma,
              omega=p.omega, phi=p.phi, theta=p.theta, lam=p.lam,
              fusion_interval=p.fusion_interval, fusion_top_f=p.fusion_top_f,
              fusion_mode=fusion_mode, finalize=1, merge_max=0, raw_logits=0, fusion_seed=fusion_seed,
              fusion_lo=p.fusion_lo, fusion_hi=p.fusion_hi)
     d.update(overrides)
-    return _Params(**d)
+    q = _Params(**d)
+    if cb is not None:
+        q.scorer = cb
+        q._cb = cb  # the callback lives as long as the params
+    return q
 
 
 class Oracle:

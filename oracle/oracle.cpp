@@ -36,7 +36,8 @@
 //    App. I; a spelling's homophones are its distinct word ids, ascending);
 //    end-of-sentence marks tried at the final fusion (each sub-beam takes its
 //    best mark under the synthetic scorer, the first of equals, and the mark
-//    follows the output words).
+//    follows the output words); fusion scores from a scorer the caller passes
+//    in (a function of the word sequence), in place of the synthetic one.
 
 #include <algorithm>
 #include <cmath>
@@ -107,7 +108,8 @@ struct Params {
   double alpha, beta, gamma, omega, phi, theta, lam;
   int fusion_interval;  // 0 = no fusion
   int fusion_top_f;     // 0 = all entries
-  int fusion_mode;      // 0 = synthetic bigram scorer, 1 = the n-gram LM's own score (pin)
+  int fusion_mode;      // 0 = synthetic bigram scorer, 1 = the n-gram LM's own score (pin),
+                        // 2 = the caller's scorer (an external LLM stand-in)
   int finalize;         // 1 = end of utterance (final fusion, drop mid-word); 0 = rank the live beam
   int merge_max;        // 0 = contributions to a prefix combine by log-sum-exp; 1 = by max (App. E.1)
   int raw_logits;       // 0 = inputs are log-probabilities; 1 = raw scores, log-softmax per frame first
@@ -115,6 +117,8 @@ struct Params {
   int eos_ids[3];       // their word ids
   uint64_t fusion_seed;
   double fusion_lo, fusion_hi;
+  double (*scorer)(const int32_t* words, int32_t n, void* ctx);  // fusion_mode 2
+  void* scorer_ctx;
 };
 
 // ------------------------------------------------------------------ lexicon
@@ -243,9 +247,14 @@ double bigram_score(const Params& p, int a, int b) {
 }
 
 // Full-sequence fusion score of a word sequence (natural log): the seeded
-// synthetic word-bigram scorer that stands in for the LLM, or (mode 1) the
-// n-gram LM's own ln-scaled sentence score.
+// synthetic word-bigram scorer that stands in for the LLM, (mode 1) the n-gram
+// LM's own ln-scaled sentence score, or (mode 2) whatever the caller's scorer
+// returns for the sequence.
 double fusion_score(const Model& M, const Params& p, const std::vector<int>& words) {
+  if (p.fusion_mode == 2) {
+    const int32_t none = 0;
+    return p.scorer(words.empty() ? &none : words.data(), static_cast<int32_t>(words.size()), p.scorer_ctx);
+  }
   double s = 0.0;
   if (p.fusion_mode == 1) {
     std::vector<int> prefix;
@@ -518,6 +527,8 @@ struct orc_params {
   int32_t eos_ids[3];
   uint64_t fusion_seed;
   double fusion_lo, fusion_hi;
+  double (*scorer)(const int32_t* words, int32_t n, void* ctx);  // fusion_mode 2
+  void* scorer_ctx;
 };
 
 const char* orc_last_error(void) { return g_err.c_str(); }
@@ -598,6 +609,8 @@ static Params to_params(const orc_params* q) {
   p.fusion_seed = q->fusion_seed;
   p.fusion_lo = q->fusion_lo;
   p.fusion_hi = q->fusion_hi;
+  p.scorer = q->scorer;
+  p.scorer_ctx = q->scorer_ctx;
   return p;
 }
 
@@ -616,7 +629,8 @@ int32_t orc_decode(void* h, const orc_params* q, const float* logits, int32_t T,
                    double* out_total, double* out_acoustic, int32_t* out_labels,
                    int32_t* out_nlabels, uint64_t* out_keys, double* out_margins,
                    double* out_frame_lse, int64_t* out_stats) {
-  if (!h || !q || !logits || T < 0 || q->beam < 1 || q->subbeams < 1) {
+  if (!h || !q || !logits || T < 0 || q->beam < 1 || q->subbeams < 1 || q->fusion_mode < 0 ||
+      q->fusion_mode > 2 || (q->fusion_mode == 2 && !q->scorer)) {
     g_err = "invalid argument";
     return -1;
   }
@@ -666,6 +680,7 @@ double orc_log10p(void* h, const int32_t* ctx, int32_t n_ctx, int32_t w) {
 double orc_fusion_score(void* h, const orc_params* q, const int32_t* words, int32_t n) {
   const Model& M = *static_cast<const Model*>(h);
   Params p = to_params(q);
+  if (p.fusion_mode == 2 && !p.scorer) return std::numeric_limits<double>::quiet_NaN();
   return fusion_score(M, p, std::vector<int>(words, words + n));
 }
 

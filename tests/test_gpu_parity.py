@@ -214,6 +214,76 @@ def test_external_fusion_round_trip(name):
         dec.close()
 
 
+@pytest.mark.parametrize("name", ["t-c20k", "t-stream"])
+def test_external_fusion_causal_lm(name):
+    """The external round trip with a randomly initialised causal word LM as the
+    scorer (the LLM stand-in; distinct sequences scored once, in batches).  Both
+    sides see the same number for a sequence (scores are memoised as float32),
+    and the oracle takes them through its caller-scorer mode."""
+    import torch
+    from workloads.fusion_lm import CausalWordLM, RoundTripStats, decode_external
+    d = load_workload(name)
+    p = d.workload.params
+    B, T = d.logits.shape[:2]
+    dev = torch.device("cuda:0")
+    lm = CausalWordLM(d.lm.vocab_size, d.lm.bos, seed=11).to(dev)
+    memo = {}
+
+    def scorer_gpu(rows, lens):
+        vals = lm.score(rows, lens).cpu().numpy()
+        R, N = rows.cpu().numpy(), lens.cpu().numpy()
+        out = []
+        for r, n, v in zip(R, N, vals):
+            out.append(memo.setdefault(tuple(int(x) for x in r[:n]), np.float32(v)))
+        return torch.tensor(np.array(out, np.float32), device=dev)
+
+    def scorer_orc(words):
+        key = tuple(words)
+        if key not in memo:
+            t = torch.tensor([list(words) or [0]], dtype=torch.int32, device=dev)
+            memo[key] = np.float32(lm.score(t, torch.tensor([len(words)], device=dev))[0].item())
+        return float(memo[key])
+
+    lp = lbm.make_params(p, max_batch=B, max_frames=T, fusion_seed=d.fusion_seed,
+                         fusion_source=lbm.LB_FUSION_EXTERNAL)
+    dec = lbm.Decoder(d.lexicon, d.lm, lp)
+    K, O, W = lp.beam, lp.subbeams, lp.max_words_out
+    logits = torch.from_numpy(d.logits).to(dev)
+    hyps = torch.empty((B, K, W), dtype=torch.int32, device=dev)
+    scores = torch.empty((B, K), dtype=torch.float32, device=dev)
+    words = torch.empty((B, K, O, W), dtype=torch.int32, device=dev)
+    nw = torch.empty((B, K, O), dtype=torch.int32, device=dev)
+    st = RoundTripStats()
+    chunk = d.workload.chunk or T
+    nch = (T + chunk - 1) // chunk
+    for c in range(nch):
+        lo, hi = c * chunk, min(T, (c + 1) * chunk)
+        ln = np.clip(d.lengths - lo, 0, hi - lo).astype(np.int32)
+        fl = (lbm.LB_BEGIN if c == 0 else 0) | (lbm.LB_END if c == nch - 1 else 0)
+        decode_external(lbm, dec, logits[:, lo:hi].contiguous(), torch.from_numpy(ln).to(dev), fl,
+                        scorer_gpu, hyps, scores, words, nw, stats=st)
+    torch.cuda.synchronize()
+    assert dec.status() == lbm.LB_OK
+    H, S = hyps.cpu().numpy(), scores.cpu().numpy()
+    out = []
+    for b in range(B):
+        ws, sc = [], []
+        for r in range(K):
+            if not np.isfinite(S[b, r]):
+                break
+            ws.append([int(x) for x in H[b, r][H[b, r] >= 0]])
+            sc.append(S[b, r])
+        out.append((ws, np.array(sc, np.float32)))
+    dec.close()
+    say(f"[case] external causal LM {name}: {st.events} events, {st.requested} sequences asked, "
+        f"{st.scored} scored, {st.batches} batches")
+    assert st.events > 0 and 0 < st.scored < st.requested
+    check_parity(d, out, range(B), name=f"external-lm/{name}", oracle_overrides=dict(scorer=scorer_orc))
+    # the scorer decides something: the synthetic scorer gives other scores
+    syn = gpu_decode(d, chunk=d.workload.chunk)
+    assert any(len(a[1]) and len(b[1]) and abs(float(a[1][0]) - float(b[1][0])) > 1e-3 for a, b in zip(out, syn))
+
+
 # ---------------------------------------------------------------- recombination by max, raw scores in
 
 

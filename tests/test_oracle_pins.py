@@ -147,6 +147,34 @@ def test_brute_force_with_fusion(tiny, seed):
     assert res.stats["fused"] > 0
 
 
+def test_brute_force_with_caller_scorer(tiny):
+    """Fusion scores from a scorer the caller passes in (an arbitrary function of
+    the word sequence): the final fusion follows it exactly."""
+    lex, lm, orc = tiny
+    calls = []
+
+    def scorer(ws):
+        calls.append(tuple(ws))
+        h = 0
+        for w in ws:
+            h = (h * 1000003 + w + 1) % 2147483647
+        return -0.5 - (h % 977) / 100.0
+
+    T = 7
+    lg = tiny_logits(T, 9)
+    p = DecodeParams(fusion_interval=3, fusion_top_f=0)
+    params = oracle.params_from(p, scorer=scorer, **BIG)
+    assert params.fusion_mode == 2
+    res = orc.decode(lg, params)
+    D = p.alpha * lg.astype(np.float64)
+    expect = bf.complete_hypotheses(D, TINY_CLASSES, TINY_WORDS, p.beta, p.gamma, lambda ws: p.phi * scorer(ws))
+    check_against_brute(res, expect)
+    assert res.stats["fused"] > 0 and calls
+    # without a scorer, mode 2 is refused
+    with pytest.raises(RuntimeError):
+        orc.decode(lg, oracle.params_from(p, fusion_mode=2, **BIG))
+
+
 def test_brute_force_end_of_sentence_marks(tiny):
     """The final fusion with end-of-sentence marks: every reading's fusion
     score takes its best mark (the first of equals), and the mark follows the
@@ -343,6 +371,12 @@ def test_fusion_identity():
         assert base.labels == fused.labels and base.words == fused.words
         np.testing.assert_allclose(base.total, fused.total, atol=1e-9)
         n_out += len(base.total)
+        # the same through the caller-scorer path, the n-gram score computed here
+        own = ngram_reading_score(orc, d.lm, 1.0)
+        via = orc.decode(lg, oracle.params_from(p, beam=32, fusion_interval=5, fusion_top_f=0,
+                                                phi=p.omega, scorer=own))
+        assert via.words == base.words
+        np.testing.assert_allclose(via.total, base.total, atol=1e-9)
         other = orc.decode(lg, oracle.params_from(p, beam=32, fusion_interval=5, fusion_top_f=0,
                                                   fusion_seed=d.fusion_seed))
         if len(base.total) and len(other.total):
