@@ -130,6 +130,13 @@ typedef struct lb_params {
                               with every mark appended, the best counts and is
                               appended to the output words (first of equals wins) */
   int32_t eos_ids[3];      /* the marks' LM word ids                              */
+  int32_t heavy_homophones; /* trie nodes with at least this many words are scored
+                              through the explicit-continuation index (0 = 16,
+                              < 0 = never): per (context, node) only the homophones
+                              that have an n-gram entry are looked up, the others
+                              back off to their unigrams and are ranked by a walk
+                              over the node's words in unigram order.  Results are
+                              the same either way (Eq. (1) evaluated exactly)     */
 } lb_params;
 
 typedef struct lb_decoder lb_decoder;

@@ -62,7 +62,8 @@ class lb_params(ctypes.Structure):
                 ("fusion_hi", ctypes.c_double), ("lm_load_factor", ctypes.c_double),
                 ("arena_nodes_per_stream", ctypes.c_int64),
                 ("merge", ctypes.c_int32), ("input", ctypes.c_int32),
-                ("eos_count", ctypes.c_int32), ("eos_ids", ctypes.c_int32 * 3)]
+                ("eos_count", ctypes.c_int32), ("eos_ids", ctypes.c_int32 * 3),
+                ("heavy_homophones", ctypes.c_int32)]
 
 
 class lb_stats(ctypes.Structure):

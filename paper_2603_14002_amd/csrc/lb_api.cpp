@@ -16,7 +16,7 @@
 
 using namespace lb;
 
-static_assert(sizeof(lb_params) == 152, "lb_params layout");
+static_assert(sizeof(lb_params) == 160, "lb_params layout");
 static_assert(sizeof(lb_ngram_desc) == 144, "lb_ngram_desc layout");
 static_assert(sizeof(lb_lexicon_desc) == 32, "lb_lexicon_desc layout");
 static_assert(sizeof(lb_stats) == 248, "lb_stats layout");
@@ -263,7 +263,62 @@ lb_status validate(const lb_lexicon_desc* lex, const lb_ngram_desc* lm, const lb
   return LB_OK;
 }
 
-lb_status build_tables(lb_decoder* d, const HostTrie& trie, const lb_ngram_desc* lm, double lf) {
+// Explicit-continuation index of one order: entries (key = context id << 32 |
+// node word offset, homophone index) grouped by key into an open-addressing
+// table with the n-gram tables' bucket layout and probe order.
+struct PresEntry {
+  uint64_t key;
+  uint32_t h;
+  bool operator<(const PresEntry& o) const { return key != o.key ? key < o.key : h < o.h; }
+};
+
+lb_status upload_pres(lb_decoder* d, std::vector<PresEntry>& ent, PresTable* out) {
+  lb_status st;
+  std::sort(ent.begin(), ent.end());
+  ent.erase(std::unique(ent.begin(), ent.end(),
+                        [](const PresEntry& a, const PresEntry& b) { return a.key == b.key && a.h == b.h; }),
+            ent.end());
+  size_t nkeys = 0;
+  for (size_t i = 0; i < ent.size(); ++i) nkeys += (i == 0 || ent[i].key != ent[i - 1].key) ? 1 : 0;
+  const uint64_t nb = buckets_for(static_cast<int64_t>(nkeys), 0.5);
+  std::vector<PresSlot> slots(nb * 4, PresSlot{kEmptyKey, 0, 0});
+  std::vector<uint32_t> lists;
+  for (size_t i = 0; i < ent.size();) {
+    size_t j = i;
+    while (j < ent.size() && ent[j].key == ent[i].key) ++j;
+    const uint32_t n = static_cast<uint32_t>(j - i);
+    uint32_t a = ent[i].h;
+    if (n > 1) {
+      a = static_cast<uint32_t>(lists.size());
+      for (size_t k = i; k < j; ++k) lists.push_back(ent[k].h);
+    }
+    uint64_t bk = bucket_of(ent[i].key, nb);
+    for (;;) {
+      int s = 0;
+      while (s < 4 && slots[bk * 4 + s].key != kEmptyKey) ++s;
+      if (s < 4) {
+        slots[bk * 4 + s] = PresSlot{ent[i].key, a, n};
+        break;
+      }
+      bk = (bk + 1 == nb) ? 0 : bk + 1;
+    }
+    i = j;
+  }
+  if (lists.size() >= 0xFFFFFFFFull) return fail(LB_ERR_CAPACITY, "continuation index too large");
+  PresSlot* ds = nullptr;
+  uint32_t* dl = nullptr;
+  if ((st = d->alloc(&ds, slots.size())) != LB_OK) return st;
+  if ((st = d->alloc(&dl, lists.size())) != LB_OK) return st;
+  LB_HIP(hipMemcpy(ds, slots.data(), slots.size() * sizeof(PresSlot), hipMemcpyHostToDevice));
+  if (!lists.empty()) LB_HIP(hipMemcpy(dl, lists.data(), lists.size() * sizeof(uint32_t), hipMemcpyHostToDevice));
+  out->slots = ds;
+  out->nbuckets = nb;
+  out->lists = dl;
+  return LB_OK;
+}
+
+lb_status build_tables(lb_decoder* d, const HostTrie& trie, const lb_ngram_desc* lm, double lf,
+                       uint32_t heavy_min) {
   lb_status st;
   // trie
   TrieNode* dtrie = nullptr;
@@ -292,6 +347,46 @@ lb_status build_tables(lb_decoder* d, const HostTrie& trie, const lb_ngram_desc*
   LB_HIP(hipMemcpy(duni, uni.data(), V * sizeof(Unigram), hipMemcpyHostToDevice));
   d->S.uni = duni;
 
+  // each node's words in (unigram log10 p desc, index asc) order, and, for the
+  // heavy nodes, every (node, index) a word id occupies
+  std::vector<WordRank> wrank(trie.words.size());
+  std::vector<uint32_t> mem_off(static_cast<size_t>(V) + 1, 0);
+  std::vector<std::pair<uint32_t, uint32_t>> mem;  // (node word offset, index) by word id
+  for (size_t k = 0; k + 1 < trie.nodes.size(); ++k) {
+    const uint32_t wo = trie.nodes[k].word_off;
+    const uint32_t H = static_cast<uint32_t>(trie.nodes[k].mask >> kWordCountShift);
+    for (uint32_t h = 0; h < H; ++h) {
+      const int32_t w = trie.words[wo + h];
+      wrank[wo + h] = WordRank{w, uni[w].logp, uni[w].bo, h};
+      if (H >= heavy_min) mem_off[static_cast<size_t>(w) + 1] += 1;
+    }
+    std::stable_sort(wrank.begin() + wo, wrank.begin() + wo + H,
+                     [](const WordRank& a, const WordRank& b) { return a.logp > b.logp; });
+  }
+  for (int32_t v = 0; v < V; ++v) mem_off[v + 1] += mem_off[v];
+  mem.resize(mem_off[V]);
+  {
+    std::vector<uint32_t> fill(mem_off.begin(), mem_off.end() - 1);
+    for (size_t k = 0; k + 1 < trie.nodes.size(); ++k) {
+      const uint32_t wo = trie.nodes[k].word_off;
+      const uint32_t H = static_cast<uint32_t>(trie.nodes[k].mask >> kWordCountShift);
+      if (H < heavy_min) continue;
+      for (uint32_t h = 0; h < H; ++h) mem[fill[trie.words[wo + h]]++] = {wo, h};
+    }
+  }
+  WordRank* dwrank = nullptr;
+  if ((st = d->alloc(&dwrank, wrank.size())) != LB_OK) return st;
+  LB_HIP(hipMemcpy(dwrank, wrank.data(), wrank.size() * sizeof(WordRank), hipMemcpyHostToDevice));
+  d->S.wrank = dwrank;
+  const bool any_heavy = !mem.empty();
+  std::vector<PresEntry> pres[3];
+  // an n-gram (context id, w) marks w at each heavy node that holds it
+  auto mark = [&](int n, uint32_t ctx, int32_t w) {
+    if (w < 0 || w >= V) return;
+    for (uint32_t m = mem_off[w]; m < mem_off[w + 1]; ++m)
+      pres[n - 2].push_back(PresEntry{(static_cast<uint64_t>(ctx) << 32) | mem[m].first, mem[m].second});
+  };
+
   // orders 2..4: open-addressing tables filled on the device
   NgramTable* tabs[3] = {&d->S.t2, &d->S.t3, &d->S.t4};
   for (int n = 2; n <= 4; ++n) {
@@ -308,30 +403,45 @@ lb_status build_tables(lb_decoder* d, const HostTrie& trie, const lb_ngram_desc*
   int32_t* sids = nullptr;
   float* slp = nullptr;
   float* sbo = nullptr;
+  uint32_t* sctx = nullptr;
   int64_t maxc = 0;
   for (int n = 2; n <= 4; ++n) maxc = std::max(maxc, lm->count[n - 1]);
   const int64_t chunk = std::min<int64_t>(kChunk, std::max<int64_t>(maxc, 1));
   LB_HIP(hipMalloc(&sids, chunk * 4 * sizeof(int32_t)));
   LB_HIP(hipMalloc(&slp, chunk * sizeof(float)));
   LB_HIP(hipMalloc(&sbo, chunk * sizeof(float)));
+  LB_HIP(hipMalloc(&sctx, chunk * sizeof(uint32_t)));
+  std::vector<uint32_t> hctx;
   hipError_t err = hipSuccess;
   for (int n = 2; n <= 4 && err == hipSuccess; ++n) {
     const int64_t cnt = lm->count[n - 1];
     for (int64_t s = 0; s < cnt && err == hipSuccess; s += chunk) {
       const int64_t m = std::min(chunk, cnt - s);
-      err = hipMemcpy(sids, lm->ids[n - 1] + s * n, m * n * sizeof(int32_t), hipMemcpyHostToDevice);
+      const int32_t* ids = lm->ids[n - 1] + s * n;
+      err = hipMemcpy(sids, ids, m * n * sizeof(int32_t), hipMemcpyHostToDevice);
       if (err == hipSuccess) err = hipMemcpy(slp, lm->log10p[n - 1] + s, m * sizeof(float), hipMemcpyHostToDevice);
       if (err == hipSuccess && n < 4)
         err = hipMemcpy(sbo, lm->backoff[n - 1] + s, m * sizeof(float), hipMemcpyHostToDevice);
       if (err == hipSuccess)
         err = launch_build_order(n, sids, slp, n < 4 ? sbo : nullptr, m, V, d->S.t2, d->S.t3, *tabs[n - 2], dflags,
-                                 nullptr);
+                                 any_heavy && n > 2 ? sctx : nullptr, nullptr);
       if (err == hipSuccess) err = hipDeviceSynchronize();
+      if (err == hipSuccess && any_heavy) {
+        if (n == 2) {
+          for (int64_t e = 0; e < m; ++e) mark(2, static_cast<uint32_t>(ids[e * 2]), ids[e * 2 + 1]);
+        } else {
+          hctx.resize(m);
+          err = hipMemcpy(hctx.data(), sctx, m * sizeof(uint32_t), hipMemcpyDeviceToHost);
+          for (int64_t e = 0; e < m && err == hipSuccess; ++e)
+            if (hctx[e] != kNone) mark(n, hctx[e], ids[e * n + n - 1]);
+        }
+      }
     }
   }
   (void)hipFree(sids);
   (void)hipFree(slp);
   (void)hipFree(sbo);
+  (void)hipFree(sctx);
   if (err != hipSuccess) return fail(LB_ERR_HIP, std::string("n-gram table build: ") + hipGetErrorString(err));
   uint32_t flags = 0;
   LB_HIP(hipMemcpy(&flags, dflags, sizeof(flags), hipMemcpyDeviceToHost));
@@ -339,6 +449,11 @@ lb_status build_tables(lb_decoder* d, const HostTrie& trie, const lb_ngram_desc*
   if (flags & kFlagBuildContext) return fail(LB_ERR_INVALID_ARG, "n-gram whose context is not an n-gram of the lower order");
   if (flags & kFlagBuildDup) return fail(LB_ERR_INVALID_ARG, "duplicate n-gram");
   if (flags & kFlagBuildFull) return fail(LB_ERR_CAPACITY, "n-gram hash table full");
+  PresTable* ptabs[3] = {&d->S.p2, &d->S.p3, &d->S.p4};
+  for (int k = 0; k < 3; ++k) {
+    if ((st = upload_pres(d, pres[k], ptabs[k])) != LB_OK) return st;
+    std::vector<PresEntry>().swap(pres[k]);
+  }
 
   // root of the word-history arena: the empty history, context <s>
   HistNode root{};
@@ -431,6 +546,7 @@ lb_status lb_create(const lb_lexicon_desc* lex, const lb_ngram_desc* lm, const l
       (st = d->alloc(&S.arena_n, B)) != LB_OK || (st = d->alloc(&S.arena, 1 + cap * B)) != LB_OK ||
       (st = d->alloc(&S.scrL, static_cast<size_t>(B) * scap)) != LB_OK ||
       (st = d->alloc(&S.scrS, static_cast<size_t>(B) * scap)) != LB_OK ||
+      (st = d->alloc(&S.scrE, static_cast<size_t>(B) * K * kMaxSub * kMaxExplicit)) != LB_OK ||
       (st = d->alloc(&S.flags, 1)) != LB_OK || (st = d->alloc(&S.counters, static_cast<size_t>(B) * kNumCounters)) != LB_OK ||
       (st = d->alloc(&S.fsel, BK)) != LB_OK || (st = d->alloc(&S.fsel_n, B)) != LB_OK ||
       (st = d->alloc(&d->ext.d_flag, B)) != LB_OK) {
@@ -451,7 +567,9 @@ lb_status lb_create(const lb_lexicon_desc* lex, const lb_ngram_desc* lm, const l
     LB_HIP(hipMemset(S.counters, 0, static_cast<size_t>(B) * kNumCounters * sizeof(unsigned long long)));
     return LB_OK;
   };
-  if ((st = init()) != LB_OK || (st = build_tables(d, trie, lm, lf)) != LB_OK) {
+  const uint32_t heavy_min = p.heavy_homophones == 0 ? static_cast<uint32_t>(kHeavyDefault)
+                             : (p.heavy_homophones < 0 ? 0xFFFFFFFFu : static_cast<uint32_t>(p.heavy_homophones));
+  if ((st = init()) != LB_OK || (st = build_tables(d, trie, lm, lf, heavy_min)) != LB_OK) {
     std::string msg = g_err;
     delete d;
     return fail(st, msg);
@@ -468,6 +586,7 @@ lb_status lb_create(const lb_lexicon_desc* lex, const lb_ngram_desc* lm, const l
   P.raw_input = p.input == LB_INPUT_LOGITS ? 1 : 0;
   P.eos_count = p.eos_count;
   for (int k = 0; k < 3; ++k) P.eos_ids[k] = p.eos_ids[k];
+  P.heavy_min = heavy_min;
   P.alpha = p.alpha;
   P.beta = p.beta;
   P.gamma = p.gamma;

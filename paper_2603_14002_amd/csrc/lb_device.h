@@ -18,6 +18,14 @@
 //               empty history (context <s>), stream b owns [1+b*cap, 1+(b+1)*cap)
 //   scrL, scrS  [max_batch][K*O*Hmax] per-stream n-gram lookup results of a
 //               frame (Hmax: the largest homophone set)
+//   wrank       WordRank[] parallel to trie_words: each node's words again, in
+//               (unigram log10 p desc, index asc) order
+//   p2, p3, p4  explicit-continuation index of the heavy nodes (many homophones):
+//               (context, node) -> the node's homophones h whose n-gram
+//               (context, word h) exists, for contexts of orders 1, 2, 3
+//               (word id, 2-gram slot, 3-gram slot); same bucket layout as t2..t4
+//   scrE        [max_batch][K*4*kMaxExplicit] per-stream explicit homophone
+//               lists of a frame's heavy query groups
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -36,6 +44,8 @@ constexpr uint32_t kRootNode = 0;                      // trie root
 constexpr uint32_t kRootHist = 0;                      // empty word history
 constexpr double kLn10 = 2.302585092994045684017991454684364208;
 constexpr int kWordCountShift = 48;  // TrieNode::mask bits 48..63: words ending at the node
+constexpr int kMaxExplicit = 16;     // a heavy group with more explicit homophones takes the full path
+constexpr int kHeavyDefault = 16;    // default homophone count from which a node is heavy
 
 // overflow / error flag bits (DevState::flags)
 constexpr uint32_t kFlagArena = 1u;
@@ -72,6 +82,29 @@ struct NgramTable {
   uint64_t nbuckets;
 };
 
+// A word of a trie node: its id, unigram log10 p and backoff, and its index
+// among the node's words (ascending ids).
+struct WordRank {
+  int32_t w;
+  float logp;
+  float bo;
+  uint32_t h;
+};
+
+// Explicit-continuation index slot: key = (context id << 32) | node word offset;
+// n homophone indices, stored in `a` itself when n == 1, else at lists[a..a+n).
+struct PresSlot {
+  uint64_t key;
+  uint32_t a;
+  uint32_t n;
+};
+
+struct PresTable {
+  PresSlot* slots;
+  uint64_t nbuckets;
+  const uint32_t* lists;
+};
+
 // Word-history node: the word sequence (parent chain) of an orthographic
 // sub-beam plus the n-gram state after its last word: the word itself (the
 // 1-word context), the slots of the 2- and 3-word contexts (kNone if absent)
@@ -104,6 +137,7 @@ struct DevParams {
   int32_t raw_input;  // 1: per-frame scores are raw, log-softmax them first
   int32_t eos_count;  // end-of-sentence marks tried at the final synthetic fusion
   int32_t eos_ids[3];
+  uint32_t heavy_min;  // nodes with at least this many words use the explicit-continuation index
   double alpha, beta, gamma, comega, phi, theta, lam;
   uint64_t seed;
   double lo, hi;
@@ -140,6 +174,11 @@ struct DevState {
   // n-gram LM
   const Unigram* uni;
   NgramTable t2, t3, t4;
+  // heavy nodes: words in unigram order, explicit-continuation index, and the
+  // per-stream explicit homophone lists of a frame ([B][K*kMaxSub*kMaxExplicit])
+  const WordRank* wrank;
+  PresTable p2, p3, p4;
+  uint32_t* scrE;
 };
 
 // SplitMix64 output for state x (Steele, Lea & Flood, OOPSLA 2014).

@@ -22,6 +22,7 @@ constexpr double kNegInf = -HUGE_VAL;
 constexpr int kBins = 1024;         // score bins of the top-K selection
 constexpr int kBoundaryCap = 256;   // candidates resolved exactly inside the boundary bin
 constexpr int kMaxLevels = 16;      // refinement levels of the top-K selection
+constexpr uint32_t kGroupHeavy = 0x80000000u;  // query group scored through its explicit homophones
 
 // ------------------------------------------------------------------ block helpers
 
@@ -265,12 +266,16 @@ __device__ inline int insert(const NgramTable& t, uint64_t key, float lp, float 
   return 2;
 }
 
+// Inserts a chunk of order-`order` n-grams; each n-gram's context id (the word
+// id for order 2, the slot of its context n-gram for orders 3 and 4) goes to
+// ctx_out[e] when ctx_out is given (kNone on error).
 __global__ void k_build_order(int order, const int32_t* __restrict__ ids, const float* __restrict__ lp,
                               const float* __restrict__ bo, int64_t count, int32_t vocab, NgramTable t2,
-                              NgramTable t3, NgramTable dst, uint32_t* flags) {
+                              NgramTable t3, NgramTable dst, uint32_t* flags, uint32_t* ctx_out) {
   const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
   for (int64_t e = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; e < count; e += stride) {
     const int32_t* r = ids + e * order;
+    if (ctx_out) ctx_out[e] = kNone;
     bool ok = true;
     for (int k = 0; k < order; ++k) ok = ok && r[k] >= 0 && r[k] < vocab;
     if (!ok) {
@@ -296,6 +301,7 @@ __global__ void k_build_order(int order, const int32_t* __restrict__ ids, const 
       }
     }
     const uint64_t key = (ctx << 32) | static_cast<uint32_t>(r[order - 1]);
+    if (ctx_out) ctx_out[e] = static_cast<uint32_t>(ctx);
     const int st = insert(dst, key, lp[e], bo ? bo[e] : 0.0f);
     if (st == 1) atomicOr(flags, kFlagBuildDup);
     if (st == 2) atomicOr(flags, kFlagBuildFull);
@@ -329,7 +335,9 @@ struct Bucket {
   uint4 s0, s1, s2, s3;
 };
 
-__device__ __forceinline__ Bucket load_bucket(const NgramTable& t, uint64_t bk) {
+// (NgramTable and PresTable share the bucket layout: 16-B slots {u64 key, u32, u32})
+template <typename Table>
+__device__ __forceinline__ Bucket load_bucket(const Table& t, uint64_t bk) {
   const uint4* line = reinterpret_cast<const uint4*>(t.slots + bk * 4);
   Bucket q;
   q.s0 = line[0];
@@ -343,16 +351,17 @@ __device__ __forceinline__ uint64_t slot_key(const uint4& v) {
   return static_cast<uint64_t>(v.x) | (static_cast<uint64_t>(v.y) << 32);
 }
 
-// Scans a bucket for `key`: 1 found (slot index and values set), 0 absent, -1 bucket full.
-__device__ __forceinline__ int scan_bucket(const Bucket& q, uint64_t key, uint64_t bk, uint32_t* slot, float* lp,
-                                           float* bo) {
+// Scans a bucket for `key`: 1 found (slot index and the slot's two values set),
+// 0 absent, -1 bucket full.
+__device__ __forceinline__ int scan_bucket(const Bucket& q, uint64_t key, uint64_t bk, uint32_t* slot, uint32_t* z,
+                                           uint32_t* w) {
 #define LB_SCAN_SLOT(V, K)                              \
   {                                                     \
     const uint64_t kk = slot_key(V);                    \
     if (kk == key) {                                    \
       *slot = static_cast<uint32_t>(bk * 4 + (K));      \
-      *lp = __uint_as_float((V).z);                     \
-      *bo = __uint_as_float((V).w);                     \
+      *z = (V).z;                                       \
+      *w = (V).w;                                       \
       return 1;                                         \
     }                                                   \
     if (kk == kEmptyKey) return 0;                      \
@@ -367,13 +376,14 @@ __device__ __forceinline__ int scan_bucket(const Bucket& q, uint64_t key, uint64
 
 // Resolves a lookup whose first bucket `bk` is already loaded; linear probing
 // continues bucket by bucket while buckets are full.
-__device__ __forceinline__ bool resolve(const NgramTable& t, uint64_t key, uint64_t bk, const Bucket& first,
-                                        uint32_t* slot, float* lp, float* bo, uint32_t* lines) {
-  int r = scan_bucket(first, key, bk, slot, lp, bo);
+template <typename Table>
+__device__ __forceinline__ bool resolve(const Table& t, uint64_t key, uint64_t bk, const Bucket& first,
+                                        uint32_t* slot, uint32_t* z, uint32_t* w, uint32_t* lines) {
+  int r = scan_bucket(first, key, bk, slot, z, w);
   for (uint64_t it = 1; r < 0 && it < t.nbuckets; ++it) {
     bk = (bk + 1 == t.nbuckets) ? 0 : bk + 1;
     ++*lines;
-    r = scan_bucket(load_bucket(t, bk), key, bk, slot, lp, bo);
+    r = scan_bucket(load_bucket(t, bk), key, bk, slot, z, w);
   }
   return r == 1;
 }
@@ -421,10 +431,12 @@ __device__ __forceinline__ LmResult lm_lookup(const DevState& S, int32_t w, cons
   const Unigram u = S.uni[w];
   *lines += 1u + (has3 ? 1u : 0u) + (has4 ? 1u : 0u);
   uint32_t s2 = kNone, s3 = kNone, s4 = kNone;
-  float p2 = 0.f, bb2 = 0.f, p3 = 0.f, bb3 = 0.f, p4 = 0.f, bb4 = 0.f;
-  const bool f2 = resolve(S.t2, k2, b2, q2, &s2, &p2, &bb2, lines);
-  const bool f3 = has3 && resolve(S.t3, k3, b3, q3, &s3, &p3, &bb3, lines);
-  const bool f4 = has4 && resolve(S.t4, k4, b4, q4, &s4, &p4, &bb4, lines);
+  uint32_t z2 = 0, y2 = 0, z3 = 0, y3 = 0, z4 = 0, y4 = 0;
+  const bool f2 = resolve(S.t2, k2, b2, q2, &s2, &z2, &y2, lines);
+  const bool f3 = has3 && resolve(S.t3, k3, b3, q3, &s3, &z3, &y3, lines);
+  const bool f4 = has4 && resolve(S.t4, k4, b4, q4, &s4, &z4, &y4, lines);
+  const float p2 = __uint_as_float(z2), bb2 = __uint_as_float(y2), p3 = __uint_as_float(z3),
+              bb3 = __uint_as_float(y3), p4 = __uint_as_float(z4);
   // log10 P(w | context) by backoff, innermost order first
   double lp;
   if (f4) {
@@ -458,6 +470,39 @@ __device__ __forceinline__ unsigned long long group_key(const Ctx& ctx, uint32_t
   const uint64_t tag = ctx.c3 != kNone ? 2u : (ctx.c2 != kNone ? 1u : 0u);
   const uint64_t id = ctx.c3 != kNone ? ctx.c3 : (ctx.c2 != kNone ? ctx.c2 : static_cast<uint32_t>(ctx.word));
   return (tag << 62) | (id << 30) | woff;
+}
+
+// The homophones of the node at word offset `woff` that have an explicit
+// n-gram with context `ctx`, from the explicit-continuation index of orders 2,
+// 3 and 4 (contexts: the last word, the 2-word slot, the 3-word slot).  The
+// first buckets of the three probes are loaded together.  Order n's result is
+// hit[n-2] = {a, count}: the index is `a` itself when count == 1, else
+// lists[a..a+count).
+struct PresHit {
+  uint32_t a, n;
+};
+
+__device__ __forceinline__ void pres_lookup(const DevState& S, const Ctx& ctx, uint32_t woff, PresHit* hit,
+                                            uint32_t* lines) {
+  const uint64_t k2 = (static_cast<uint64_t>(static_cast<uint32_t>(ctx.word)) << 32) | woff;
+  const uint64_t k3 = (static_cast<uint64_t>(ctx.c2) << 32) | woff;
+  const uint64_t k4 = (static_cast<uint64_t>(ctx.c3) << 32) | woff;
+  const bool has3 = ctx.c2 != kNone;
+  const bool has4 = ctx.c3 != kNone;
+  const uint64_t b2 = bucket_of(k2, S.p2.nbuckets);
+  const uint64_t b3 = has3 ? bucket_of(k3, S.p3.nbuckets) : 0;
+  const uint64_t b4 = has4 ? bucket_of(k4, S.p4.nbuckets) : 0;
+  const Bucket q2 = load_bucket(S.p2, b2);
+  const Bucket q3 = has3 ? load_bucket(S.p3, b3) : Bucket{};
+  const Bucket q4 = has4 ? load_bucket(S.p4, b4) : Bucket{};
+  *lines += 1u + (has3 ? 1u : 0u) + (has4 ? 1u : 0u);
+  uint32_t slot;
+  hit[0] = PresHit{0, 0};
+  hit[1] = PresHit{0, 0};
+  hit[2] = PresHit{0, 0};
+  resolve(S.p2, k2, b2, q2, &slot, &hit[0].a, &hit[0].n, lines);
+  if (has3) resolve(S.p3, k3, b3, q3, &slot, &hit[1].a, &hit[1].n, lines);
+  if (has4) resolve(S.p4, k4, b4, q4, &slot, &hit[2].a, &hit[2].n, lines);
 }
 
 // ------------------------------------------------------------------ decoding loop
@@ -505,7 +550,7 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
   constexpr int NC = (kSep + LPB - 1) / LPB;  // extension slots per lane
   constexpr int NPM = KMAX * kMaxSub;  // (completed word, sub-beam) pairs per frame, at most
   constexpr int SEL_BYTES = kBins * 4 + kBoundaryCap * 16;
-  constexpr int LM_BYTES = 52 * NPM + 16;
+  constexpr int LM_BYTES = 56 * NPM + 16;
   constexpr int UNI_BYTES = SEL_BYTES > LM_BYTES ? SEL_BYTES : LM_BYTES;
   static_assert(20 * KMAX <= SEL_BYTES, "fusion sort scratch");
   const int b = blockIdx.x;
@@ -529,7 +574,7 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
   __shared__ uint32_t sSelSrc[KMAX];
   // hypotheses that completed a word this frame
   __shared__ uint32_t sEvBeam[KMAX], sEvSrc[KMAX], sEvWoff[KMAX], sEvH[KMAX];
-  __shared__ int32_t sNG;
+  __shared__ int32_t sNG, sHeavy;
   __shared__ double sRed[2 * NW], sRedB[2 * NW];
   __shared__ int32_t sScan[NW], sScanB[NW], sScanC[NW], sScanD[NW];
   __shared__ int32_t sBucket, sAbove, sBucketCnt, sBCount;
@@ -945,7 +990,10 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
     {
       unsigned long long* const gk = reinterpret_cast<unsigned long long*>(sSel);
       for (int q = tid; q < NPM; q += BLOCK) gk[q] = kEmptyKey;
-      if (tid == 0) sNG = 0;
+      if (tid == 0) {
+        sNG = 0;
+        sHeavy = 0;
+      }
     }
     const int r = tid;
     int is_event = 0;
@@ -1018,6 +1066,7 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
     uint32_t* const sGH = sGwoff + NPM;
     Ctx* const sGctx = reinterpret_cast<Ctx*>(sGH + NPM);             // 24 B each
     int32_t* const sGoff = reinterpret_cast<int32_t*>(sGctx + NPM);  // NPM + 1 entries
+    uint32_t* const sGcnt = reinterpret_cast<uint32_t*>(sGoff + NPM + 1);  // lookups | kGroupHeavy
     lds_barrier();
     for (int pr = tid; pr < nev * kMaxSub; pr += BLOCK) {
       const int e = pr / kMaxSub;
@@ -1037,6 +1086,7 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
             sGwoff[g] = sEvWoff[e];
             sGH[g] = sEvH[e];
             sGctx[g] = ctx;
+            if (sEvH[e] >= P.heavy_min) sHeavy = 1;
             break;
           }
           if (prev == key) break;
@@ -1052,6 +1102,39 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
       const int q = sPairG[pr];
       if (q >= 0) sPairG[pr] = sGId[q];
     }
+    // heavy groups (nodes with many homophones): the homophones with an explicit
+    // n-gram for the group's context, from the continuation index; the others
+    // back off to their unigrams and are not looked up.  A group with more than
+    // kMaxExplicit of them is looked up in full.
+    uint32_t* const scrE = S.scrE + static_cast<size_t>(b) * P.K * kMaxSub * kMaxExplicit;
+    const bool heavy_frame = sHeavy != 0;
+    for (int g = tid; g < NG; g += BLOCK) {
+      const uint32_t Hg = sGH[g];
+      uint32_t cnt = Hg;
+      if (Hg >= P.heavy_min) {
+        PresHit hit[3];
+        pres_lookup(S, sGctx[g], sGwoff[g], hit, &lines);
+        const uint32_t ne = hit[0].n + hit[1].n + hit[2].n;
+        if (ne <= static_cast<uint32_t>(kMaxExplicit)) {
+          uint32_t* E = scrE + static_cast<size_t>(g) * kMaxExplicit;
+#pragma unroll
+          for (int o3 = 0; o3 < 3; ++o3) {
+            if (hit[o3].n == 1) {
+              *E++ = hit[o3].a;
+            } else {
+              const uint32_t* lst = (o3 == 0 ? S.p2.lists : (o3 == 1 ? S.p3.lists : S.p4.lists)) + hit[o3].a;
+              for (uint32_t m = 0; m < hit[o3].n; ++m) *E++ = lst[m];
+            }
+          }
+          cnt = ne | kGroupHeavy;
+        }
+      }
+      sGcnt[g] = cnt;
+    }
+    if (heavy_frame)
+      __syncthreads();  // the explicit lists (global memory) are read by other threads
+    else
+      lds_barrier();
     // lookup offsets of the groups
     int U = 0;
     {
@@ -1060,7 +1143,7 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
 #pragma unroll
       for (int q = 0; q < PG; ++q) {
         const int g = tid * PG + q;
-        loc += g < NG ? static_cast<int>(sGH[g]) : 0;
+        loc += g < NG ? static_cast<int>(sGcnt[g] & ~kGroupHeavy) : 0;
       }
       int pre = block_scan<BLOCK, false>(loc, sScanD, &U);
 #pragma unroll
@@ -1068,7 +1151,7 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
         const int g = tid * PG + q;
         if (g < NG) {
           sGoff[g] = pre;
-          pre += static_cast<int>(sGH[g]);
+          pre += static_cast<int>(sGcnt[g] & ~kGroupHeavy);
         }
       }
       if (tid == 0) sGoff[NG] = U;
@@ -1085,7 +1168,8 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
         const int mid = (lo + hi + 1) >> 1;
         if (sGoff[mid] <= u) lo = mid; else hi = mid - 1;
       }
-      const uint32_t h = static_cast<uint32_t>(u - sGoff[lo]);
+      const uint32_t k = static_cast<uint32_t>(u - sGoff[lo]);
+      const uint32_t h = (sGcnt[lo] & kGroupHeavy) ? scrE[static_cast<size_t>(lo) * kMaxExplicit + k] : k;
       const int32_t w = S.trie_words[sGwoff[lo] + h];
       const LmResult res = lm_lookup(S, w, sGctx[lo], &lines);
       scrL[u] = res.lp;
@@ -1093,54 +1177,137 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
     }
     __syncthreads();  // the lookup results (global memory) are read by other threads
     // each completed word (one wavefront): its top-o by (score desc, j*H + h
-    // asc), lambda pruning, word-history nodes (o reserved per word, in order)
+    // asc), lambda pruning, word-history nodes (o reserved per word, in order).
+    // A candidate's source: its lookup result in the scratch (>= 0), or, for a
+    // homophone that backs off to its unigram in a heavy group, -1 - its rank
+    // in the node's unigram order.
     for (int e = wave; e < nev; e += NW) {
       const uint32_t rr = sEvBeam[e];
       const uint32_t i = sEvSrc[e];
       const uint32_t H = sEvH[e];
+      const uint32_t woff = sEvWoff[e];
       const int nsub = (C.meta[i] >> 8) & 0xFF;
       const int nq = nsub * static_cast<int>(H);
       double tL[kMaxSub];
-      int tq[kMaxSub];
+      int tq[kMaxSub], ts[kMaxSub];
 #pragma unroll
       for (int k = 0; k < kMaxSub; ++k) {
         tL[k] = kNegInf;
         tq[k] = 0x7FFFFFFF;
+        ts[k] = 0;
       }
-      auto insert = [&](double L, int qq) {
+      auto insert = [&](double L, int qq, int ss) {
 #pragma unroll
         for (int k = 0; k < kMaxSub; ++k) {
           if (k < O && (L > tL[k] || (L == tL[k] && qq < tq[k]))) {
             const double t = tL[k];
-            const int u = tq[k];
+            const int u = tq[k], v = ts[k];
             tL[k] = L;
             tq[k] = qq;
+            ts[k] = ss;
             L = t;
             qq = u;
+            ss = v;
           }
         }
       };
-      // the sub-beams' scores and result offsets (a group's results are
-      // contiguous in the scratch); lane h reads homophone h of every sub-beam
+      // the sub-beams' scores, groups and result offsets (a group's results
+      // are contiguous in the scratch)
       double Lw[kMaxSub];
-      const double* lp[kMaxSub];
+      int gid[kMaxSub], goff[kMaxSub];
+      uint32_t gcnt[kMaxSub];
+      bool any_full = false, any_heavy = false;
 #pragma unroll
       for (int j = 0; j < kMaxSub; ++j) {
         const int jj = j < nsub ? j : 0;
         Lw[j] = C.Lw[i * kMaxSub + jj];
-        lp[j] = scrL + sGoff[sPairG[e * kMaxSub + jj]];
+        gid[j] = sPairG[e * kMaxSub + jj];
+        goff[j] = sGoff[gid[j]];
+        gcnt[j] = sGcnt[gid[j]];
+        if (j < nsub) {
+          any_heavy |= (gcnt[j] & kGroupHeavy) != 0;
+          any_full |= (gcnt[j] & kGroupHeavy) == 0;
+        }
       }
-      for (int h = lane; h < static_cast<int>(H); h += 64) {
-        double a[kMaxSub];
+      // full groups: lane h reads homophone h of every such sub-beam
+      if (any_full) {
+        for (int h = lane; h < static_cast<int>(H); h += 64) {
+          double a[kMaxSub];
 #pragma unroll
-        for (int j = 0; j < kMaxSub; ++j) a[j] = j < nsub ? lp[j][h] : 0.0;
+          for (int j = 0; j < kMaxSub; ++j)
+            a[j] = (j < nsub && !(gcnt[j] & kGroupHeavy)) ? scrL[goff[j] + h] : 0.0;
 #pragma unroll
-        for (int j = 0; j < kMaxSub; ++j)
-          if (j < nsub) insert(Lw[j] + P.comega * a[j], j * static_cast<int>(H) + h);
+          for (int j = 0; j < kMaxSub; ++j)
+            if (j < nsub && !(gcnt[j] & kGroupHeavy))
+              insert(Lw[j] + P.comega * a[j], j * static_cast<int>(H) + h, goff[j] + h);
+        }
+      }
+      if (any_heavy) {
+        // heavy groups: lane m holds the m-th explicit homophone; its first
+        // occurrence is a candidate with its looked-up score
+        uint32_t eh[kMaxSub];
+        int ne[kMaxSub];
+#pragma unroll
+        for (int j = 0; j < kMaxSub; ++j) {
+          const bool hv = j < nsub && (gcnt[j] & kGroupHeavy);
+          ne[j] = hv ? static_cast<int>(gcnt[j] & ~kGroupHeavy) : 0;
+          eh[j] = lane < ne[j] ? scrE[static_cast<size_t>(gid[j]) * kMaxExplicit + lane] : kNone;
+        }
+#pragma unroll
+        for (int j = 0; j < kMaxSub; ++j) {
+          if (ne[j] > 0) {
+            bool dup = false;
+            for (int m = 0; m < ne[j]; ++m) {
+              const uint32_t x = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(eh[j]), m));
+              dup |= m < lane && x == eh[j];
+            }
+            if (lane < ne[j] && !dup)
+              insert(Lw[j] + P.comega * scrL[goff[j] + lane], j * static_cast<int>(H) + static_cast<int>(eh[j]),
+                     goff[j] + lane);
+          }
+        }
+        // the other homophones of a heavy group score bo3 + bo2 + bo1 + log10 p1(w)
+        // (Katz backoff to the unigram), monotone in log10 p1: walk the node's
+        // words in unigram order, 64 at a time, until every heavy sub-beam has
+        // o candidates strictly above all that remain
+        int cum[kMaxSub];
+        Ctx cx[kMaxSub];
+#pragma unroll
+        for (int j = 0; j < kMaxSub; ++j) {
+          cum[j] = 0;
+          cx[j] = sGctx[gid[j]];
+        }
+#pragma unroll 1
+        for (int c0 = 0; c0 < static_cast<int>(H); c0 += 64) {
+          const int k = c0 + lane;
+          const bool valid = k < static_cast<int>(H);
+          WordRank wr = WordRank{0, 0.0f, 0.0f, kNone};
+          if (valid) wr = S.wrank[woff + k];
+          const int last = (static_cast<int>(H) - 1 - c0) < 63 ? static_cast<int>(H) - 1 - c0 : 63;
+          bool more = false;
+#pragma unroll
+          for (int j = 0; j < kMaxSub; ++j) {
+            if (j < nsub && (gcnt[j] & kGroupHeavy)) {
+              bool member = false;
+              for (int m = 0; m < ne[j]; ++m)
+                member |= static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(eh[j]), m)) == wr.h;
+              const double lp = static_cast<double>(cx[j].bo3) +
+                                (static_cast<double>(cx[j].bo2) +
+                                 (static_cast<double>(cx[j].bo1) + static_cast<double>(wr.logp)));
+              const double L = Lw[j] + P.comega * lp;
+              const bool cand = valid && !member;
+              if (cand) insert(L, j * static_cast<int>(H) + static_cast<int>(wr.h), -1 - k);
+              const double lastL = readlane_f64(L, last);
+              cum[j] += __popcll(__ballot(cand && L > lastL));
+              more |= cum[j] < O;
+            }
+          }
+          if (!more) break;
+        }
       }
       // O rounds of wavefront arg-max; lane k keeps the k-th winner
       double myL = kNegInf, bestL = kNegInf;
-      int myq = 0, kept = 0;
+      int myq = 0, mys = 0, kept = 0;
 #pragma unroll 1
       for (int k = 0; k < O; ++k) {
         double bL = tL[0];
@@ -1149,15 +1316,20 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
         if (bL == kNegInf) break;
         if (k == 0) bestL = bL;
         if (bL < bestL - P.lam) break;
+        const bool holder = tL[0] == bL && tq[0] == bq;  // one lane: queries are distinct
+        const int hl = __builtin_ctzll(__ballot(holder));
+        const int bs = __builtin_amdgcn_readlane(ts[0], hl);
         if (lane == k) {
           myL = bL;
           myq = bq;
+          mys = bs;
         }
-        if (tL[0] == bL && tq[0] == bq) {  // the lane holding the winner (queries are distinct)
+        if (holder) {
 #pragma unroll
           for (int m = 0; m + 1 < kMaxSub; ++m) {
             tL[m] = tL[m + 1];
             tq[m] = tq[m + 1];
+            ts[m] = ts[m + 1];
           }
           tL[kMaxSub - 1] = kNegInf;
           tq[kMaxSub - 1] = 0x7FFFFFFF;
@@ -1168,9 +1340,19 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
       const bool room = static_cast<uint64_t>(abase) + O <= S.arena_cap;
       if (lane < kept && room) {
         const uint32_t j = static_cast<uint32_t>(myq) / H;
-        const uint32_t h = static_cast<uint32_t>(myq) - j * H;
         const uint32_t ph = C.hist[i * kMaxSub + j];
-        const QState st = scrS[sGoff[sPairG[e * kMaxSub + j]] + h];
+        QState st;
+        if (mys >= 0) {
+          st = scrS[mys];
+        } else {
+          const WordRank wr = S.wrank[woff + static_cast<uint32_t>(-1 - mys)];
+          st.c2 = kNone;
+          st.c3 = kNone;
+          st.bo2 = 0.0f;
+          st.bo3 = 0.0f;
+          st.w = wr.w;
+          st.bo1 = wr.bo;
+        }
         const int32_t w = st.w;
         HistNode hn;
         hn.parent = ph;
@@ -1575,12 +1757,12 @@ void set_launch_events(hipEvent_t start, hipEvent_t stop) {
 
 hipError_t launch_build_order(int order, const int32_t* ids, const float* lp, const float* bo, int64_t count,
                               int32_t vocab, NgramTable t2, NgramTable t3, NgramTable dst, uint32_t* flags,
-                              hipStream_t st) {
+                              uint32_t* ctx_out, hipStream_t st) {
   if (count <= 0) return hipSuccess;
   const int64_t blocks = (count + 255) / 256;
   const int grid = static_cast<int>(blocks < 65536 ? blocks : 65536);
   hipLaunchKernelGGL(k_build_order, dim3(grid), dim3(256), 0, st, order, ids, lp, bo, count, vocab, t2, t3,
-                     dst, flags);
+                     dst, flags, ctx_out);
   return hipGetLastError();
 }
 

@@ -13,7 +13,7 @@ void set_launch_events(hipEvent_t start, hipEvent_t stop);
 
 hipError_t launch_build_order(int order, const int32_t* ids, const float* lp, const float* bo, int64_t count,
                               int32_t vocab, NgramTable t2, NgramTable t3, NgramTable dst, uint32_t* flags,
-                              hipStream_t st);
+                              uint32_t* ctx_out, hipStream_t st);
 hipError_t launch_begin(const DevParams& P, const DevState& S, int32_t B, hipStream_t st);
 hipError_t launch_decode(int K, const DevParams& P, const DevState& S, const float* logits,
                          const int32_t* lengths, int32_t B, int32_t Tc, int32_t tau0, int32_t tau1, hipStream_t st);

@@ -31,7 +31,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_struct_sizes_match_header_layout():
-    assert ctypes.sizeof(lbm.lb_params) == 152
+    assert ctypes.sizeof(lbm.lb_params) == 160
     assert ctypes.sizeof(lbm.lb_ngram_desc) == 144
     assert ctypes.sizeof(lbm.lb_lexicon_desc) == 32
     assert ctypes.sizeof(lbm.lb_stats) == 248

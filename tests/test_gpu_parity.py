@@ -121,6 +121,73 @@ def test_zero_length_and_tiny_lexicon():
     check_parity(d, out, range(3), params=p, name="tiny")
 
 
+@pytest.mark.parametrize("name", ["t-c20k", "t-c125k", "t-k256"])
+def test_heavy_homophone_paths(name):
+    """Nodes with many homophones are scored through the explicit-continuation
+    index and a walk in unigram order.  Forced on for every node with two or
+    more words, and switched off: both match the oracle, and the default path
+    gives bit-identical outputs to the full lookups while doing fewer."""
+    d = load_workload(name, batch=8 if name != "t-k256" else 2)
+    B = d.logits.shape[0]
+    runs = {}
+    for heavy in (0, -1, 2):
+        out, dec = gpu_decode(d, lb_overrides=dict(heavy_homophones=heavy), return_decoder=True)
+        runs[heavy] = (out, dec.stats().lm_lookups, dec.stats().lm_queries)
+        dec.close()
+        say(f"[case] heavy={heavy} {name}: lookups {runs[heavy][1]} of {runs[heavy][2]} queries")
+        if heavy != 0:
+            check_parity(d, out, range(B), name=f"{name}/heavy={heavy}")
+    for heavy in (-1, 2):
+        for (wa, sa), (wb, sb) in zip(runs[0][0], runs[heavy][0]):
+            assert wa == wb and np.array_equal(sa, sb)
+    assert runs[0][2] == runs[-1][2] == runs[2][2]
+    assert runs[2][1] < runs[0][1] < runs[-1][1]
+
+
+@pytest.mark.parametrize("case", ["tied-unigrams", "many-explicit"])
+def test_heavy_walk_edges(case):
+    """One node with 100 homophones.  tied-unigrams: equal unigram scores, so
+    the walk in unigram order never stops early (two chunks of 64) and ties
+    fall to the lowest index; many-explicit: after <s> 20 of them have a bigram
+    (more than the explicit list holds, so that group is looked up in full),
+    after other words a few do."""
+    H = 100
+    words = [(1,)] * H + [(2,), (3, 1), (2, 2)]
+    W = len(words)
+    lex = lexicon_from(words)
+    rng = np.random.default_rng(5)
+    if case == "tied-unigrams":
+        uni_lp = [-2.0] * H + [-1.5, -1.2, -1.8]
+    else:
+        uni_lp = list(np.round(rng.uniform(-4.0, -1.0, H), 3)) + [-1.5, -1.2, -1.8]
+    uni = [((w,), float(uni_lp[w]), -0.25) for w in range(W)] + [((W,), -99.0, -0.5), ((W + 1,), -1.0, 0.0),
+                                                                   ((W + 2,), -3.0, 0.0)]
+    big = [((W, 100), -0.4, -0.3), ((100, 7), -0.6, -0.2), ((100, 70), -0.3, -0.1), ((7, 101), -0.2, -0.2)]
+    if case == "many-explicit":
+        big += [((W, h), float(-1.0 - 0.01 * h), -0.2) for h in range(10, 30)]
+    big += [((70, h), -0.9, -0.1) for h in (3, 40, 99)]
+    tri = [((W, 100, 7), -0.1, -0.1), ((100, 70, 3), -0.2, 0.0)]
+    four = [((W, 100, 7, 101), -0.05)]
+    lm = lm_from_entries(W, [uni, sorted(set(big)), tri, four])
+    seq = [2, 40, 1, 40, 1, 40, 3, 1, 40, 1, 40, 2, 40]
+    lg = np.stack([peaked_logits([c for c in seq for _ in range(2)], strong=2.5, seed=sd) for sd in range(4)])
+    wl = load_workload("t-c1k").workload
+    p = DecodeParams(beam=32, subbeams=3, fusion_interval=5, fusion_top_f=0, lam=8.0)
+    wl = wl.__class__(**{**wl.__dict__, "params": p})
+    T = lg.shape[1]
+    d = WorkloadData(wl, lex, lm, lg, np.full(4, T, np.int32), np.zeros((4, T), np.int32), [[]] * 4, 17)
+    outs = {}
+    for heavy in (2, -1):
+        for fin in (True, False):
+            say(f"[case] heavy walk {case} heavy={heavy} finalize={fin}")
+            out = gpu_decode(d, params=p, finalize=fin, lb_overrides=dict(heavy_homophones=heavy))
+            check_parity(d, out, range(4), params=p, name=f"walk/{case}/{heavy}/{fin}", finalize=fin)
+            outs[(heavy, fin)] = out
+    for fin in (True, False):
+        for (wa, sa), (wb, sb) in zip(outs[(2, fin)], outs[(-1, fin)]):
+            assert wa == wb and np.array_equal(sa, sb)
+
+
 @pytest.mark.parametrize("sigma", [0.0, 1e-3], ids=["exact-ties", "clustered"])
 def test_crowded_boundary_bins(sigma):
     """Uniform (or nearly uniform) log-probs make thousands of candidates share
