@@ -574,7 +574,8 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
   __shared__ uint32_t sSelSrc[KMAX];
   // hypotheses that completed a word this frame
   __shared__ uint32_t sEvBeam[KMAX], sEvSrc[KMAX], sEvWoff[KMAX], sEvH[KMAX];
-  __shared__ int32_t sNG, sHeavy;
+  __shared__ int32_t sNG, sHeavy, sNLarge;
+  __shared__ int32_t sLarge[KMAX];  // completed words ranked by a whole wavefront
   __shared__ double sRed[2 * NW], sRedB[2 * NW];
   __shared__ int32_t sScan[NW], sScanB[NW], sScanC[NW], sScanD[NW];
   __shared__ int32_t sBucket, sAbove, sBucketCnt, sBCount;
@@ -993,6 +994,7 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
       if (tid == 0) {
         sNG = 0;
         sHeavy = 0;
+        sNLarge = 0;
       }
     }
     const int r = tid;
@@ -1176,18 +1178,188 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
       scrS[u] = res.st;
     }
     __syncthreads();  // the lookup results (global memory) are read by other threads
-    // each completed word (one wavefront): its top-o by (score desc, j*H + h
-    // asc), lambda pruning, word-history nodes (o reserved per word, in order).
-    // A candidate's source: its lookup result in the scratch (>= 0), or, for a
+    // each completed word: its top-o by (score desc, j*H + h asc), lambda
+    // pruning, word-history nodes (o reserved per word, in order).  A
+    // candidate's source: its lookup result in the scratch (>= 0), or, for a
     // homophone that backs off to its unigram in a heavy group, -1 - its rank
-    // in the node's unigram order.
-    for (int e = wave; e < nev; e += NW) {
+    // in the node's unigram order.  A word is ranked by one thread, unless one
+    // of its sub-beams' groups was looked up in full over more than
+    // kThreadMaxH homophones: those words get a wavefront each.
+    auto write_node = [&](int e, int k, double L, int q, int src) {
       const uint32_t rr = sEvBeam[e];
+      const uint32_t i = sEvSrc[e];
+      const uint32_t H = sEvH[e];
+      const uint32_t j = static_cast<uint32_t>(q) / H;
+      const uint32_t ph = C.hist[i * kMaxSub + j];
+      QState st;
+      if (src >= 0) {
+        st = scrS[src];
+      } else {
+        const WordRank wr = S.wrank[sEvWoff[e] + static_cast<uint32_t>(-1 - src)];
+        st.c2 = kNone;
+        st.c3 = kNone;
+        st.bo2 = 0.0f;
+        st.bo3 = 0.0f;
+        st.w = wr.w;
+        st.bo1 = wr.bo;
+      }
+      const HistNode par = S.arena[ph];
+      HistNode hn;
+      hn.parent = ph;
+      hn.word = st.w;
+      hn.c2 = st.c2;
+      hn.c3 = st.c3;
+      hn.bo1 = st.bo1;
+      hn.bo2 = st.bo2;
+      hn.bo3 = st.bo3;
+      hn.depth = par.depth + 1;
+      hn.sfus = synth ? par.sfus + bigram_score(P, par.word, st.w) : 0.0;
+      const uint32_t node = arena0 + arena_n + static_cast<uint32_t>(e * O + k);
+      S.arena[node] = hn;
+      N.Lw[rr * kMaxSub + k] = L;
+      N.hist[rr * kMaxSub + k] = node;
+    };
+    auto close_event = [&](int e, int kept) {
+      const uint32_t rr = sEvBeam[e];
+      const uint32_t i = sEvSrc[e];
+      const bool room = static_cast<uint64_t>(arena_n) + static_cast<uint64_t>(e + 1) * O <= S.arena_cap;
+      if (room)
+        N.meta[rr] = (N.meta[rr] & 0xFFu) | (static_cast<uint32_t>(kept) << 8);
+      else
+        atomicOr(S.flags, kFlagArena);
+      c_words += 1;
+      c_queries += static_cast<uint64_t>(((C.meta[i] >> 8) & 0xFF) * sEvH[e]);
+    };
+    {
+      constexpr uint32_t kThreadMaxH = 16;
+      bool mine = false;
+      if (tid < nev) {
+        const int nsub = (C.meta[sEvSrc[tid]] >> 8) & 0xFF;
+        bool large = false;
+        for (int j = 0; j < nsub; ++j) {
+          const int g = sPairG[tid * kMaxSub + j];
+          large |= !(sGcnt[g] & kGroupHeavy) && sGH[g] > kThreadMaxH;
+        }
+        if (large)
+          sLarge[atomicAdd(&sNLarge, 1)] = tid;
+        else
+          mine = true;
+      }
+      if (mine) {
+        const int e = tid;
+        const uint32_t i = sEvSrc[e];
+        const int H = static_cast<int>(sEvH[e]);
+        const uint32_t woff = sEvWoff[e];
+        const int nsub = (C.meta[i] >> 8) & 0xFF;
+        double tL[kMaxSub];
+        int tq[kMaxSub], ts[kMaxSub];
+#pragma unroll
+        for (int k = 0; k < kMaxSub; ++k) {
+          tL[k] = kNegInf;
+          tq[k] = 0x7FFFFFFF;
+          ts[k] = 0;
+        }
+        auto insert = [&](double L, int qq, int ss) {
+#pragma unroll
+          for (int k = 0; k < kMaxSub; ++k) {
+            if (k < O && (L > tL[k] || (L == tL[k] && qq < tq[k]))) {
+              const double t = tL[k];
+              const int u = tq[k], v = ts[k];
+              tL[k] = L;
+              tq[k] = qq;
+              ts[k] = ss;
+              L = t;
+              qq = u;
+              ss = v;
+            }
+          }
+        };
+        bool any_heavy = false;
+#pragma unroll
+        for (int j = 0; j < kMaxSub; ++j) {
+          if (j < nsub) {
+            const double Lw = C.Lw[i * kMaxSub + j];
+            const int g = sPairG[e * kMaxSub + j];
+            const int off = sGoff[g];
+            const uint32_t cnt = sGcnt[g];
+            if (!(cnt & kGroupHeavy)) {
+              for (int h = 0; h < H; ++h) insert(Lw + P.comega * scrL[off + h], j * H + h, off + h);
+            } else {
+              any_heavy = true;
+              const uint32_t* E = scrE + static_cast<size_t>(g) * kMaxExplicit;
+              const int ne = static_cast<int>(cnt & ~kGroupHeavy);
+              for (int m = 0; m < ne; ++m) {
+                const uint32_t hm = E[m];
+                bool dup = false;
+                for (int m2 = 0; m2 < m; ++m2) dup |= E[m2] == hm;
+                if (!dup) insert(Lw + P.comega * scrL[off + m], j * H + static_cast<int>(hm), off + m);
+              }
+            }
+          }
+        }
+        if (any_heavy) {
+          // the heavy groups' other homophones in unigram order (scores
+          // non-increasing): a sub-beam is done once its o-th such candidate
+          // scores strictly above the next word's
+          int nw[kMaxSub];
+          double Lth[kMaxSub];
+#pragma unroll
+          for (int j = 0; j < kMaxSub; ++j) {
+            nw[j] = 0;
+            Lth[j] = HUGE_VAL;
+          }
+#pragma unroll 1
+          for (int k = 0; k < H; ++k) {
+            const WordRank wr = S.wrank[woff + k];
+            bool need = false;
+#pragma unroll
+            for (int j = 0; j < kMaxSub; ++j) {
+              if (j < nsub) {
+                const int g = sPairG[e * kMaxSub + j];
+                const uint32_t cnt = sGcnt[g];
+                if (cnt & kGroupHeavy) {
+                  const Ctx cx = sGctx[g];
+                  const double lp = static_cast<double>(cx.bo3) +
+                                    (static_cast<double>(cx.bo2) +
+                                     (static_cast<double>(cx.bo1) + static_cast<double>(wr.logp)));
+                  const double L = C.Lw[i * kMaxSub + j] + P.comega * lp;
+                  if (nw[j] < O || !(Lth[j] > L)) {
+                    need = true;
+                    const uint32_t* E = scrE + static_cast<size_t>(g) * kMaxExplicit;
+                    const int ne = static_cast<int>(cnt & ~kGroupHeavy);
+                    bool member = false;
+                    for (int m = 0; m < ne; ++m) member |= E[m] == wr.h;
+                    if (!member) {
+                      insert(L, j * H + static_cast<int>(wr.h), -1 - k);
+                      nw[j] += 1;
+                      if (nw[j] == O) Lth[j] = L;
+                    }
+                  }
+                }
+              }
+            }
+            if (!need) break;
+          }
+        }
+        int kept = 0;
+#pragma unroll
+        for (int k = 0; k < kMaxSub; ++k)
+          if (k < O && tL[k] != kNegInf && !(tL[k] < tL[0] - P.lam)) kept = k + 1;
+        const bool room = static_cast<uint64_t>(arena_n) + static_cast<uint64_t>(e + 1) * O <= S.arena_cap;
+#pragma unroll
+        for (int k = 0; k < kMaxSub; ++k)
+          if (k < kept && room) write_node(e, k, tL[k], tq[k], ts[k]);
+        close_event(e, kept);
+      }
+    }
+    lds_barrier();  // the list of wavefront-ranked words
+    const int nlarge = sNLarge;
+    for (int x = wave; x < nlarge; x += NW) {
+      const int e = sLarge[x];
       const uint32_t i = sEvSrc[e];
       const uint32_t H = sEvH[e];
       const uint32_t woff = sEvWoff[e];
       const int nsub = (C.meta[i] >> 8) & 0xFF;
-      const int nq = nsub * static_cast<int>(H);
       double tL[kMaxSub];
       int tq[kMaxSub], ts[kMaxSub];
 #pragma unroll
@@ -1336,48 +1508,9 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
         }
         kept = k + 1;
       }
-      const uint32_t abase = arena_n + static_cast<uint32_t>(e * O);
-      const bool room = static_cast<uint64_t>(abase) + O <= S.arena_cap;
-      if (lane < kept && room) {
-        const uint32_t j = static_cast<uint32_t>(myq) / H;
-        const uint32_t ph = C.hist[i * kMaxSub + j];
-        QState st;
-        if (mys >= 0) {
-          st = scrS[mys];
-        } else {
-          const WordRank wr = S.wrank[woff + static_cast<uint32_t>(-1 - mys)];
-          st.c2 = kNone;
-          st.c3 = kNone;
-          st.bo2 = 0.0f;
-          st.bo3 = 0.0f;
-          st.w = wr.w;
-          st.bo1 = wr.bo;
-        }
-        const int32_t w = st.w;
-        HistNode hn;
-        hn.parent = ph;
-        hn.word = w;
-        hn.c2 = st.c2;
-        hn.c3 = st.c3;
-        hn.bo1 = st.bo1;
-        hn.bo2 = st.bo2;
-        hn.bo3 = st.bo3;
-        const HistNode par = S.arena[ph];
-        hn.depth = par.depth + 1;
-        hn.sfus = synth ? par.sfus + bigram_score(P, par.word, w) : 0.0;
-        const uint32_t node = arena0 + abase + static_cast<uint32_t>(lane);
-        S.arena[node] = hn;
-        N.Lw[rr * kMaxSub + lane] = myL;
-        N.hist[rr * kMaxSub + lane] = node;
-      }
-      if (lane == 0) {
-        if (room)
-          N.meta[rr] = (N.meta[rr] & 0xFFu) | (static_cast<uint32_t>(kept) << 8);
-        else
-          atomicOr(S.flags, kFlagArena);
-        c_words += 1;
-        c_queries += static_cast<uint64_t>(nq);
-      }
+      const bool room = static_cast<uint64_t>(arena_n) + static_cast<uint64_t>(e + 1) * O <= S.arena_cap;
+      if (lane < kept && room) write_node(e, lane, myL, myq, mys);
+      if (lane == 0) close_event(e, kept);
     }
     arena_n += static_cast<uint32_t>(nev * O);
     c_exp += static_cast<uint64_t>(n) * kClasses;
