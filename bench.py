@@ -110,11 +110,12 @@ def measured_traffic(workload: str):
 def algorithmic_bytes(s, B, T, p, lp):
     """Bytes the method itself moves in the counted work (all launches of the
     pass): the logits once, a 16-B trie node per 41 expansions, the beam state
-    read and written once per call, per n-gram query the probed 64-B bucket
-    lines plus the unigram entry (8 B), the word id (4 B) and the context's
-    40-B history node, counted per lookup (the queries of a stream-frame that
-    share context and word are looked up once), and a 40-B history node
-    written per kept word (at most o per completed word)."""
+    read and written once per call, the probed 64-B bucket lines (n-gram and
+    continuation-index tables), per lookup the unigram entry (8 B) and the word
+    id (4 B) (the queries of a stream-frame that share context and word are
+    looked up once; homophones that back off to their unigram are not looked
+    up), and per completed word and sub-beam the context's 64-B history node
+    read and a 64-B history node written (at most o per completed word)."""
     state = 48 + 12 * p.subbeams          # key, pkey, a_b, a_nb, total, node, meta + o x (L, hist)
     calls = max(1, int(s.launches[0]))
     parts = {
@@ -122,8 +123,8 @@ def algorithmic_bytes(s, B, T, p, lp):
         "trie": float(s.expansions) * 16.0 / 41.0,
         "state": 2.0 * calls * B * p.beam * state,
         "ngram_lines": float(s.probe_lines) * LINE_BYTES,
-        "ngram_other": float(s.lm_lookups) * (8 + 4 + 40),
-        "history_nodes": float(s.word_events) * p.subbeams * 40.0,
+        "ngram_other": float(s.lm_lookups) * (8 + 4),
+        "history_nodes": float(s.word_events) * p.subbeams * 128.0,
     }
     parts["total"] = sum(parts.values())
     return parts

@@ -465,6 +465,9 @@ lb_status build_tables(lb_decoder* d, const HostTrie& trie, const lb_ngram_desc*
   root.bo2 = 0.0f;
   root.bo3 = 0.0f;
   root.sfus = 0.0;
+  root.depth = 0;
+  root.w1 = root.w2 = root.w3 = -1;
+  root.up2 = root.up3 = root.up4 = kNone;
   LB_HIP(hipMemcpy(d->S.arena, &root, sizeof(root), hipMemcpyHostToDevice));
   return LB_OK;
 }

@@ -105,11 +105,13 @@ struct PresTable {
   const uint32_t* lists;
 };
 
-// Word-history node: the word sequence (parent chain) of an orthographic
-// sub-beam plus the n-gram state after its last word: the word itself (the
-// 1-word context), the slots of the 2- and 3-word contexts (kNone if absent)
-// and the three backoff weights, the number of words in the chain, and the
-// running synthetic fusion score.
+// Word-history node (64 B, one line): the word sequence (parent chain) of an
+// orthographic sub-beam plus the n-gram state after its last word: the word
+// itself (the 1-word context), the slots of the 2- and 3-word contexts (kNone
+// if absent) and the three backoff weights, the number of words in the chain,
+// the running synthetic fusion score, and a window for tracing words back:
+// the words of the three nearest ancestors and the ancestors 2, 3 and 4
+// levels up (fields past the root are not read).
 struct HistNode {
   uint32_t parent;
   int32_t word;
@@ -118,7 +120,10 @@ struct HistNode {
   float bo1, bo2, bo3;
   uint32_t depth;
   double sfus;
+  int32_t w1, w2, w3;
+  uint32_t up2, up3, up4;
 };
+static_assert(sizeof(HistNode) == 64, "history node is one 64-B line");
 
 // n-gram state after a queried word: slots of its 2- and 3-word contexts and
 // their backoffs, the word and its unigram backoff.

@@ -1214,6 +1214,12 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
       hn.bo3 = st.bo3;
       hn.depth = par.depth + 1;
       hn.sfus = synth ? par.sfus + bigram_score(P, par.word, st.w) : 0.0;
+      hn.w1 = par.word;
+      hn.w2 = par.w1;
+      hn.w3 = par.w2;
+      hn.up2 = par.parent;
+      hn.up3 = par.up2;
+      hn.up4 = par.up3;
       const uint32_t node = arena0 + arena_n + static_cast<uint32_t>(e * O + k);
       S.arena[node] = hn;
       N.Lw[rr * kMaxSub + k] = L;
@@ -1764,12 +1770,29 @@ __global__ __launch_bounds__(BLOCK) void k_fuse_select(const DevParams P, const 
 // External scorer, step 2: word sequences of every sub-beam of the selected
 // hypotheses, words [B][K][O][W] (-1 padded) and n_words [B][K][O] (-1 where
 // nothing is to be scored).
+// Writes the `depth` words of history h into row[0..min(depth, W)), four per
+// node read (the node's word and its window of three ancestors' words).
+__device__ inline void trace_words(const DevState& S, uint32_t h, int depth, int32_t* row, int W) {
+  int d = depth;
+  while (d >= 1) {
+    const HistNode x = S.arena[h];
+    if (d - 1 < W) row[d - 1] = x.word;
+    if (d >= 2 && d - 2 < W) row[d - 2] = x.w1;
+    if (d >= 3 && d - 3 < W) row[d - 3] = x.w2;
+    if (d >= 4 && d - 4 < W) row[d - 4] = x.w3;
+    if (d <= 4) break;
+    h = x.up4;
+    d -= 4;
+  }
+}
+
 template <int BLOCK>
 __global__ __launch_bounds__(BLOCK) void k_fuse_export(const DevParams P, const DevState S,
                                                        int32_t* __restrict__ words, int32_t* __restrict__ n_words) {
   const int b = blockIdx.x;
   const size_t gb = static_cast<size_t>(b) * P.K;
   const int F = S.fsel_n[b];
+  __shared__ int32_t sLen[BLOCK * kMaxSub];  // words written per request row (BLOCK >= K)
   for (int idx = threadIdx.x; idx < P.K * P.O; idx += BLOCK) {
     const int r = idx / P.O;
     const int j = idx - r * P.O;
@@ -1783,16 +1806,20 @@ __global__ __launch_bounds__(BLOCK) void k_fuse_export(const DevParams P, const 
         const uint32_t h = S.hist[bi * P.O + j];
         len = static_cast<int>(S.arena[h].depth);
         if (len > P.W) atomicOr(S.flags, kFlagWords);
-        int k = len - 1;
-        for (uint32_t x = h; x != kRootHist && k >= 0; x = S.arena[x].parent, --k)
-          if (k < P.W) row[k] = S.arena[x].word;
-        for (int k2 = len; k2 < P.W; ++k2) row[k2] = -1;
+        trace_words(S, h, len, row, P.W);
         if (len > P.W) len = P.W;
       }
     }
-    if (len < 0)
-      for (int k2 = 0; k2 < P.W; ++k2) row[k2] = -1;
+    sLen[idx] = len < 0 ? 0 : len;
     n_words[slot] = len;
+  }
+  __syncthreads();
+  // -1 past each row's words, the whole block on consecutive addresses
+  int32_t* const rows = words + gb * P.O * P.W;
+  const int total = P.K * P.O * P.W;
+  for (int x = threadIdx.x; x < total; x += BLOCK) {
+    const int idx = x / P.W;
+    if (x - idx * P.W >= sLen[idx]) rows[x] = -1;
   }
 }
 
@@ -1837,8 +1864,11 @@ __global__ __launch_bounds__(BLOCK) void k_output(const DevParams P, const DevSt
   (void)block_scan<BLOCK>(ok ? 1 : 0, sScan, &m);
   bitonic_sort<BLOCK>(sc, ky, ix);
   if (tid == 0) S.t0[b] += lengths[b];
+  int32_t* const sLen = reinterpret_cast<int32_t*>(ky);  // words written per rank (the keys are read)
+  __syncthreads();
   for (int r = tid; r < P.K; r += BLOCK) {
     int32_t* row = out_hyps + (static_cast<size_t>(b) * P.K + r) * P.W;
+    int n = 0;
     if (r < m) {
       const size_t bi = gb + ix[r];
       out_scores[static_cast<size_t>(b) * P.K + r] = static_cast<float>(sc[r]);
@@ -1851,17 +1881,22 @@ __global__ __launch_bounds__(BLOCK) void k_output(const DevParams P, const DevSt
         double e;
         mark = best_eos(P, top.word, &e);
       }
-      const int n = len + (mark >= 0 ? 1 : 0);
+      n = len + (mark >= 0 ? 1 : 0);
       if (n > P.W) atomicOr(S.flags, kFlagWords);
-      int k = len - 1;
-      for (uint32_t x = h; x != kRootHist && k >= 0; x = S.arena[x].parent, --k)
-        if (k < P.W) row[k] = S.arena[x].word;
+      trace_words(S, h, len, row, P.W);
       if (mark >= 0 && len < P.W) row[len] = mark;
-      for (int k2 = n; k2 < P.W; ++k2) row[k2] = -1;
     } else {
       out_scores[static_cast<size_t>(b) * P.K + r] = kNegInf;
-      for (int k2 = 0; k2 < P.W; ++k2) row[k2] = -1;
     }
+    sLen[r] = n < P.W ? n : P.W;
+  }
+  __syncthreads();
+  // -1 past each row's words, the whole block on consecutive addresses
+  int32_t* const rows = out_hyps + static_cast<size_t>(b) * P.K * P.W;
+  const int total = P.K * P.W;
+  for (int x = tid; x < total; x += BLOCK) {
+    const int r = x / P.W;
+    if (x - r * P.W >= sLen[r]) rows[x] = -1;
   }
 }
 
