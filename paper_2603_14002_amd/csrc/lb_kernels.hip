@@ -539,8 +539,13 @@ struct BeamLds {
 //     over all threads; the top-o survive lambda pruning and receive
 //     word-history nodes;
 //   * Eq. (2) with the synthetic scorer on fusion frames.
-template <int KMAX, int LPB>
-__global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const DevState S,
+// WPE: wavefronts per SIMD the register allocation aims for (two workgroups of
+// 512 threads per CU need 4).  DB: the hypotheses are double-buffered in LDS;
+// otherwise one buffer is rewritten in place (every source entry is read into
+// registers before any new entry is written), which lets two K = 256
+// workgroups share a CU.
+template <int KMAX, int LPB, int WPE, bool DB>
+__global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE))) void k_decode(const DevParams P, const DevState S,
                                                        const float* __restrict__ logits,
                                                        const int32_t* __restrict__ lengths, int32_t Tc,
                                                        int32_t tau0, int32_t tau1) {
@@ -549,8 +554,10 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
   constexpr int NW = BLOCK / 64;
   constexpr int NC = (kSep + LPB - 1) / LPB;  // extension slots per lane
   constexpr int NPM = KMAX * kMaxSub;  // (completed word, sub-beam) pairs per frame, at most
+  constexpr int NPL = NPM < 256 ? NPM : 256;  // pairs grouped at once
+  constexpr int NEB = NPL / kMaxSub;          // completed words per batch
   constexpr int SEL_BYTES = kBins * 4 + kBoundaryCap * 16;
-  constexpr int LM_BYTES = 56 * NPM + 16;
+  constexpr int LM_BYTES = 56 * NPL + 16;
   constexpr int UNI_BYTES = SEL_BYTES > LM_BYTES ? SEL_BYTES : LM_BYTES;
   static_assert(20 * KMAX <= SEL_BYTES, "fusion sort scratch");
   const int b = blockIdx.x;
@@ -561,7 +568,7 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
   const int tend = len < tau1 ? len : tau1;
   if (tau0 >= tend) return;
 
-  __shared__ BeamLds<KMAX> sBeam[2];
+  __shared__ BeamLds<KMAX> sBeam[DB ? 2 : 1];
   __shared__ double sD[48];  // classes 0..40; 41..47 are zero (slots past the separator)
   __shared__ double sAb2[KMAX], sAnb2[KMAX], sPt2[KMAX], sStay[KMAX];
   __shared__ uint64_t sMask[KMAX];
@@ -573,7 +580,7 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
   __shared__ int32_t sLvBeta[kMaxLevels], sLvShift[kMaxLevels];
   __shared__ uint32_t sSelSrc[KMAX];
   // hypotheses that completed a word this frame
-  __shared__ uint32_t sEvBeam[KMAX], sEvSrc[KMAX], sEvWoff[KMAX], sEvH[KMAX];
+  __shared__ uint32_t sEvBeam[KMAX], sEvWoff[KMAX], sEvH[KMAX];
   __shared__ int32_t sNG, sHeavy, sNLarge;
   __shared__ int32_t sLarge[KMAX];  // completed words ranked by a whole wavefront
   __shared__ double sRed[2 * NW], sRedB[2 * NW];
@@ -618,12 +625,12 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
   }
   if (tid < 3) sCnt[tid] = 0;
   uint32_t arena_n = S.arena_n[b];
+  int cur = 0;  // the current buffer (DB)
   uint32_t lines = 0, c_words = 0;  // per thread
   uint64_t c_queries = 0;
   uint64_t c_exp = 0, c_fused = 0, c_lookups = 0;  // uniform
   double* const scrL = S.scrL + static_cast<size_t>(b) * S.scap;
   QState* const scrS = S.scrS + static_cast<size_t>(b) * S.scap;
-  int cur = 0;
   // D = alpha * log-probs of a frame into sD, by wavefront 0 (every lane):
   // raw scores are first normalised by a log-softmax over the 41 classes
   auto set_row = [&](const DevParams& Pr, float xin) {
@@ -651,8 +658,8 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
     asm volatile("" : "+v"(tid));
     const int lane = tid & 63;
     const int wave = tid >> 6;
-    BeamLds<KMAX>& C = sBeam[cur];
-    BeamLds<KMAX>& N = sBeam[cur ^ 1];
+    BeamLds<KMAX>& C = sBeam[DB ? cur : 0];        // the frame's hypotheses
+    BeamLds<KMAX>& N = sBeam[DB ? (cur ^ 1) : 0];  // the new ones (the same buffer when !DB)
 
     // the next frame's log-probs are loaded meanwhile
     if (tid < kClasses && tau + 1 < tend) dnext = logits[(static_cast<size_t>(b) * Tc + tau + 1) * kClasses + tid];
@@ -990,7 +997,7 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
     // the top-K scratch it shares is no longer read.)
     {
       unsigned long long* const gk = reinterpret_cast<unsigned long long*>(sSel);
-      for (int q = tid; q < NPM; q += BLOCK) gk[q] = kEmptyKey;
+      for (int q = tid; q < NPL; q += BLOCK) gk[q] = kEmptyKey;
       if (tid == 0) {
         sNG = 0;
         sHeavy = 0;
@@ -999,59 +1006,87 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
     }
     const int r = tid;
     int is_event = 0;
-    uint32_t ev_src = 0, ev_woff = 0, ev_H = 0;
+    uint32_t ev_woff = 0, ev_H = 0;
     bool tn_load = false;
     TrieNode tn{};
+    // every new entry's fields from its source, into registers first
+    uint64_t w_key = 0, w_pkey = 0, w_tmask = 0;
+    double w_ab = 0.0, w_anb = 0.0, w_pt = 0.0;
+    uint32_t w_node = 0, w_meta = 0, w_first = 0, w_woff = 0;
+    double w_Lw[kMaxSub];
+    uint32_t w_hist[kMaxSub];
     if (r < nsel) {
       const uint32_t src = sSelSrc[r];
       const int i = src & 0xFFFF;
       const int v = src >> 16;
       const uint32_t meta_i = C.meta[i];
-      const int nsub = (meta_i >> 8) & 0xFF;
       if (v == 0) {
-        N.key[r] = C.key[i];
-        N.pkey[r] = C.pkey[i];
-        N.ab[r] = sAb2[i];
-        N.anb[r] = sAnb2[i];
-        N.pt[r] = sPt2[i];
-        N.node[r] = C.node[i];
-        N.meta[r] = meta_i;
-        N.tmask[r] = C.tmask[i];
-        N.first[r] = C.first[i];
-        N.woff[r] = C.woff[i];
+        w_key = C.key[i];
+        w_pkey = C.pkey[i];
+        w_ab = sAb2[i];
+        w_anb = sAnb2[i];
+        w_pt = sPt2[i];
+        w_node = C.node[i];
+        w_meta = meta_i;
+        w_tmask = C.tmask[i];
+        w_first = C.first[i];
+        w_woff = C.woff[i];
       } else {
         const int last = meta_i & 0xFF;
         const double base = (v == last) ? C.ab[i] : C.pt[i];
         const double anb = (base + sD[v]) + (v == kSep ? P.gamma : P.beta);
         const uint64_t tm = C.tmask[i];
-        N.key[r] = prefix_step(C.key[i], v);
-        N.pkey[r] = C.key[i];
-        N.ab[r] = kNegInf;
-        N.anb[r] = anb;
-        N.pt[r] = anb;  // log-sum-exp(-inf, anb)
+        w_key = prefix_step(C.key[i], v);
+        w_pkey = C.key[i];
+        w_ab = kNegInf;
+        w_anb = anb;
+        w_pt = anb;  // log-sum-exp(-inf, anb)
         uint32_t child = kRootNode;
         if (v != kSep) child = C.first[i] + __popcll(tm & ((1ull << v) - 1ull));
-        N.node[r] = child;
-        N.meta[r] = static_cast<uint32_t>(v) | (meta_i & 0xFF00u);
+        w_node = child;
+        w_meta = static_cast<uint32_t>(v) | (meta_i & 0xFF00u);
         tn = S.trie[child];
         tn_load = true;
         if (v == kSep) {
           is_event = 1;
-          ev_src = static_cast<uint32_t>(i);
           ev_woff = C.woff[i];
           ev_H = static_cast<uint32_t>(tm >> kWordCountShift);
         }
       }
-      for (int j = 0; j < nsub; ++j) {
-        N.Lw[r * kMaxSub + j] = C.Lw[i * kMaxSub + j];
-        N.hist[r * kMaxSub + j] = C.hist[i * kMaxSub + j];
+      const int nsub = (meta_i >> 8) & 0xFF;
+#pragma unroll
+      for (int j = 0; j < kMaxSub; ++j) {
+        w_Lw[j] = j < nsub ? C.Lw[i * kMaxSub + j] : 0.0;
+        w_hist[j] = j < nsub ? C.hist[i * kMaxSub + j] : 0u;
+      }
+    }
+    if constexpr (!DB) lds_barrier();  // every source entry has been read
+    if (r < nsel) {
+      N.key[r] = w_key;
+      N.pkey[r] = w_pkey;
+      N.ab[r] = w_ab;
+      N.anb[r] = w_anb;
+      N.pt[r] = w_pt;
+      N.node[r] = w_node;
+      N.meta[r] = w_meta;
+      if (!tn_load) {
+        N.tmask[r] = w_tmask;
+        N.first[r] = w_first;
+        N.woff[r] = w_woff;
+      }
+      const int nsub = (w_meta >> 8) & 0xFF;
+#pragma unroll
+      for (int j = 0; j < kMaxSub; ++j) {
+        if (j < nsub) {
+          N.Lw[r * kMaxSub + j] = w_Lw[j];
+          N.hist[r * kMaxSub + j] = w_hist[j];
+        }
       }
     }
     int nev = 0;
     const int erank = block_scan<BLOCK, false>(is_event, sScanC, &nev);
     if (is_event) {
       sEvBeam[erank] = static_cast<uint32_t>(r);
-      sEvSrc[erank] = ev_src;
       sEvWoff[erank] = ev_woff;
       sEvH[erank] = ev_H;
     }
@@ -1060,26 +1095,41 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
     // words are scored once per distinct group (n-gram context, completed-word
     // node): the pairs (word e, sub-beam j) are grouped in an LDS hash table,
     // the groups' lookups spread over all threads into the stream's scratch,
-    // and each completed word ranks its queries from there.
+    // and each completed word ranks its queries from there.  Words are taken
+    // in batches of NEB (the grouping tables hold NPL pairs).
     unsigned long long* const sGKey = reinterpret_cast<unsigned long long*>(sSel);
-    int32_t* const sGId = reinterpret_cast<int32_t*>(sSel + 8 * NPM);
-    int32_t* const sPairG = sGId + NPM;  // pair -> hash slot, then -> group
-    uint32_t* const sGwoff = reinterpret_cast<uint32_t*>(sPairG + NPM);
-    uint32_t* const sGH = sGwoff + NPM;
-    Ctx* const sGctx = reinterpret_cast<Ctx*>(sGH + NPM);             // 24 B each
-    int32_t* const sGoff = reinterpret_cast<int32_t*>(sGctx + NPM);  // NPM + 1 entries
-    uint32_t* const sGcnt = reinterpret_cast<uint32_t*>(sGoff + NPM + 1);  // lookups | kGroupHeavy
+    int32_t* const sGId = reinterpret_cast<int32_t*>(sSel + 8 * NPL);
+    int32_t* const sPairG = sGId + NPL;  // pair -> hash slot, then -> group
+    uint32_t* const sGwoff = reinterpret_cast<uint32_t*>(sPairG + NPL);
+    uint32_t* const sGH = sGwoff + NPL;
+    Ctx* const sGctx = reinterpret_cast<Ctx*>(sGH + NPL);             // 24 B each
+    int32_t* const sGoff = reinterpret_cast<int32_t*>(sGctx + NPL);  // NPL + 1 entries
+    uint32_t* const sGcnt = reinterpret_cast<uint32_t*>(sGoff + NPL + 1);  // lookups | kGroupHeavy
+#pragma unroll 1
+    for (int e0 = 0; e0 < nev; e0 += NEB) {
+    const int nb = nev - e0 < NEB ? nev - e0 : NEB;
+    if (e0 > 0) {
+      // the next batch: the previous one's scratch reads are done; fresh grouping table
+      __syncthreads();
+      for (int q = tid; q < NPL; q += BLOCK) sGKey[q] = kEmptyKey;
+      if (tid == 0) {
+        sNG = 0;
+        sHeavy = 0;
+        sNLarge = 0;
+      }
+    }
     lds_barrier();
-    for (int pr = tid; pr < nev * kMaxSub; pr += BLOCK) {
-      const int e = pr / kMaxSub;
-      const int j = pr - e * kMaxSub;
-      const uint32_t i = sEvSrc[e];
+    for (int pr = tid; pr < nb * kMaxSub; pr += BLOCK) {
+      const int el = pr / kMaxSub;
+      const int e = e0 + el;
+      const int j = pr - el * kMaxSub;
+      const uint32_t rr = sEvBeam[e];
       int slot = -1;
-      if (j < static_cast<int>((C.meta[i] >> 8) & 0xFF)) {
-        const uint32_t ph = C.hist[i * kMaxSub + j];
+      if (j < static_cast<int>((N.meta[rr] >> 8) & 0xFF)) {
+        const uint32_t ph = N.hist[rr * kMaxSub + j];
         const Ctx ctx = ctx_of(S.arena[ph]);
         const unsigned long long key = group_key(ctx, sEvWoff[e]);
-        uint32_t q = static_cast<uint32_t>(splitmix64(key)) & (NPM - 1);
+        uint32_t q = static_cast<uint32_t>(splitmix64(key)) & (NPL - 1);
         for (;;) {
           const unsigned long long prev = atomicCAS(&sGKey[q], kEmptyKey, key);
           if (prev == kEmptyKey) {
@@ -1092,7 +1142,7 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
             break;
           }
           if (prev == key) break;
-          q = (q + 1) & (NPM - 1);
+          q = (q + 1) & (NPL - 1);
         }
         slot = static_cast<int>(q);
       }
@@ -1100,7 +1150,7 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
     }
     lds_barrier();
     const int NG = sNG;
-    for (int pr = tid; pr < nev * kMaxSub; pr += BLOCK) {
+    for (int pr = tid; pr < nb * kMaxSub; pr += BLOCK) {
       const int q = sPairG[pr];
       if (q >= 0) sPairG[pr] = sGId[q];
     }
@@ -1140,7 +1190,7 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
     // lookup offsets of the groups
     int U = 0;
     {
-      constexpr int PG = (NPM + BLOCK - 1) / BLOCK;
+      constexpr int PG = (NPL + BLOCK - 1) / BLOCK;
       int loc = 0;
 #pragma unroll
       for (int q = 0; q < PG; ++q) {
@@ -1185,12 +1235,10 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
     // in the node's unigram order.  A word is ranked by one thread, unless one
     // of its sub-beams' groups was looked up in full over more than
     // kThreadMaxH homophones: those words get a wavefront each.
-    auto write_node = [&](int e, int k, double L, int q, int src) {
+    // (ph: the winner's parent history, read before any of the word's
+    // sub-beams is overwritten)
+    auto write_node = [&](int e, int k, double L, uint32_t ph, int src) {
       const uint32_t rr = sEvBeam[e];
-      const uint32_t i = sEvSrc[e];
-      const uint32_t H = sEvH[e];
-      const uint32_t j = static_cast<uint32_t>(q) / H;
-      const uint32_t ph = C.hist[i * kMaxSub + j];
       QState st;
       if (src >= 0) {
         st = scrS[src];
@@ -1225,38 +1273,37 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
       N.Lw[rr * kMaxSub + k] = L;
       N.hist[rr * kMaxSub + k] = node;
     };
-    auto close_event = [&](int e, int kept) {
+    auto close_event = [&](int e, int kept, int nsub) {
       const uint32_t rr = sEvBeam[e];
-      const uint32_t i = sEvSrc[e];
       const bool room = static_cast<uint64_t>(arena_n) + static_cast<uint64_t>(e + 1) * O <= S.arena_cap;
       if (room)
         N.meta[rr] = (N.meta[rr] & 0xFFu) | (static_cast<uint32_t>(kept) << 8);
       else
         atomicOr(S.flags, kFlagArena);
       c_words += 1;
-      c_queries += static_cast<uint64_t>(((C.meta[i] >> 8) & 0xFF) * sEvH[e]);
+      c_queries += static_cast<uint64_t>(nsub * sEvH[e]);
     };
     {
       constexpr uint32_t kThreadMaxH = 16;
       bool mine = false;
-      if (tid < nev) {
-        const int nsub = (C.meta[sEvSrc[tid]] >> 8) & 0xFF;
+      if (tid < nb) {
+        const int nsub = (N.meta[sEvBeam[e0 + tid]] >> 8) & 0xFF;
         bool large = false;
         for (int j = 0; j < nsub; ++j) {
           const int g = sPairG[tid * kMaxSub + j];
           large |= !(sGcnt[g] & kGroupHeavy) && sGH[g] > kThreadMaxH;
         }
         if (large)
-          sLarge[atomicAdd(&sNLarge, 1)] = tid;
+          sLarge[atomicAdd(&sNLarge, 1)] = e0 + tid;
         else
           mine = true;
       }
       if (mine) {
-        const int e = tid;
-        const uint32_t i = sEvSrc[e];
+        const int e = e0 + tid;
+        const uint32_t rr = sEvBeam[e];
         const int H = static_cast<int>(sEvH[e]);
         const uint32_t woff = sEvWoff[e];
-        const int nsub = (C.meta[i] >> 8) & 0xFF;
+        const int nsub = (N.meta[rr] >> 8) & 0xFF;
         double tL[kMaxSub];
         int tq[kMaxSub], ts[kMaxSub];
 #pragma unroll
@@ -1284,8 +1331,8 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
 #pragma unroll
         for (int j = 0; j < kMaxSub; ++j) {
           if (j < nsub) {
-            const double Lw = C.Lw[i * kMaxSub + j];
-            const int g = sPairG[e * kMaxSub + j];
+            const double Lw = N.Lw[rr * kMaxSub + j];
+            const int g = sPairG[(e - e0) * kMaxSub + j];
             const int off = sGoff[g];
             const uint32_t cnt = sGcnt[g];
             if (!(cnt & kGroupHeavy)) {
@@ -1321,14 +1368,14 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
 #pragma unroll
             for (int j = 0; j < kMaxSub; ++j) {
               if (j < nsub) {
-                const int g = sPairG[e * kMaxSub + j];
+                const int g = sPairG[(e - e0) * kMaxSub + j];
                 const uint32_t cnt = sGcnt[g];
                 if (cnt & kGroupHeavy) {
                   const Ctx cx = sGctx[g];
                   const double lp = static_cast<double>(cx.bo3) +
                                     (static_cast<double>(cx.bo2) +
                                      (static_cast<double>(cx.bo1) + static_cast<double>(wr.logp)));
-                  const double L = C.Lw[i * kMaxSub + j] + P.comega * lp;
+                  const double L = N.Lw[rr * kMaxSub + j] + P.comega * lp;
                   if (nw[j] < O || !(Lth[j] > L)) {
                     need = true;
                     const uint32_t* E = scrE + static_cast<size_t>(g) * kMaxExplicit;
@@ -1352,20 +1399,23 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
         for (int k = 0; k < kMaxSub; ++k)
           if (k < O && tL[k] != kNegInf && !(tL[k] < tL[0] - P.lam)) kept = k + 1;
         const bool room = static_cast<uint64_t>(arena_n) + static_cast<uint64_t>(e + 1) * O <= S.arena_cap;
+        uint32_t ph[kMaxSub];
+#pragma unroll
+        for (int k = 0; k < kMaxSub; ++k) ph[k] = k < kept ? N.hist[rr * kMaxSub + tq[k] / H] : 0u;
 #pragma unroll
         for (int k = 0; k < kMaxSub; ++k)
-          if (k < kept && room) write_node(e, k, tL[k], tq[k], ts[k]);
-        close_event(e, kept);
+          if (k < kept && room) write_node(e, k, tL[k], ph[k], ts[k]);
+        close_event(e, kept, nsub);
       }
     }
     lds_barrier();  // the list of wavefront-ranked words
     const int nlarge = sNLarge;
     for (int x = wave; x < nlarge; x += NW) {
       const int e = sLarge[x];
-      const uint32_t i = sEvSrc[e];
+      const uint32_t rr = sEvBeam[e];
       const uint32_t H = sEvH[e];
       const uint32_t woff = sEvWoff[e];
-      const int nsub = (C.meta[i] >> 8) & 0xFF;
+      const int nsub = (N.meta[rr] >> 8) & 0xFF;
       double tL[kMaxSub];
       int tq[kMaxSub], ts[kMaxSub];
 #pragma unroll
@@ -1398,8 +1448,8 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
 #pragma unroll
       for (int j = 0; j < kMaxSub; ++j) {
         const int jj = j < nsub ? j : 0;
-        Lw[j] = C.Lw[i * kMaxSub + jj];
-        gid[j] = sPairG[e * kMaxSub + jj];
+        Lw[j] = N.Lw[rr * kMaxSub + jj];
+        gid[j] = sPairG[(e - e0) * kMaxSub + jj];
         goff[j] = sGoff[gid[j]];
         gcnt[j] = sGcnt[gid[j]];
         if (j < nsub) {
@@ -1515,8 +1565,11 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
         kept = k + 1;
       }
       const bool room = static_cast<uint64_t>(arena_n) + static_cast<uint64_t>(e + 1) * O <= S.arena_cap;
-      if (lane < kept && room) write_node(e, lane, myL, myq, mys);
-      if (lane == 0) close_event(e, kept);
+      // every lane reads its parent before any lane writes (one wavefront, in order)
+      const uint32_t ph = lane < kept ? N.hist[rr * kMaxSub + static_cast<uint32_t>(myq) / H] : 0u;
+      if (lane < kept && room) write_node(e, lane, myL, ph, mys);
+      if (lane == 0) close_event(e, kept, nsub);
+    }
     }
     arena_n += static_cast<uint32_t>(nev * O);
     c_exp += static_cast<uint64_t>(n) * kClasses;
@@ -1588,12 +1641,12 @@ __global__ __launch_bounds__(KMAX * LPB) void k_decode(const DevParams P, const 
       c_fused += static_cast<uint64_t>(F);
     }
     lds_barrier();
-    cur ^= 1;
+    if constexpr (DB) cur ^= 1;
   }
 
   // ---- the beam back to HBM
   {
-    const BeamLds<KMAX>& E = sBeam[cur];
+    const BeamLds<KMAX>& E = sBeam[DB ? cur : 0];
     if (tid < n) {
       const size_t g = gb + tid;
       S.key[g] = E.key[tid];
@@ -1950,18 +2003,41 @@ hipError_t launch_begin(const DevParams& P, const DevState& S, int32_t B, hipStr
   } while (0)
 
 // Decode-kernel shapes: (hypotheses per workgroup, lanes per hypothesis).
+// Compute units of the current device (queried once).
+int cu_count() {
+  static int n = 0;
+  if (n <= 0) {
+    int dev = 0, c = 0;
+    if (hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&c, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && c > 0)
+      n = c;
+    else
+      n = 256;
+  }
+  return n;
+}
+
 hipError_t launch_decode(int K, const DevParams& P, const DevState& S, const float* logits,
                          const int32_t* lengths, int32_t B, int32_t Tc, int32_t tau0, int32_t tau1, hipStream_t st) {
+  // One workgroup per stream.  When the batch has more streams than one
+  // round of workgroups holds, the instances that fit more workgroups per CU
+  // (fewer registers, at the price of some spilling) are used: K = 64 with 4
+  // per CU instead of 3, K = 256 with 2 (512 threads, one LDS buffer) instead of 1.
+  const int cus = cu_count();
   if (K <= 16)
-    LB_LAUNCH((k_decode<16, 4>), dim3(B), dim3(64), st, P, S, logits, lengths, Tc, tau0, tau1);
+    LB_LAUNCH((k_decode<16, 4, 1, true>), dim3(B), dim3(64), st, P, S, logits, lengths, Tc, tau0, tau1);
   else if (K <= 32)
-    LB_LAUNCH((k_decode<32, 4>), dim3(B), dim3(128), st, P, S, logits, lengths, Tc, tau0, tau1);
+    LB_LAUNCH((k_decode<32, 4, 1, true>), dim3(B), dim3(128), st, P, S, logits, lengths, Tc, tau0, tau1);
+  else if (K <= 64 && B > 3 * cus)
+    LB_LAUNCH((k_decode<64, 4, 4, true>), dim3(B), dim3(256), st, P, S, logits, lengths, Tc, tau0, tau1);
   else if (K <= 64)
-    LB_LAUNCH((k_decode<64, 4>), dim3(B), dim3(256), st, P, S, logits, lengths, Tc, tau0, tau1);
+    LB_LAUNCH((k_decode<64, 4, 1, true>), dim3(B), dim3(256), st, P, S, logits, lengths, Tc, tau0, tau1);
   else if (K <= 128)
-    LB_LAUNCH((k_decode<128, 4>), dim3(B), dim3(512), st, P, S, logits, lengths, Tc, tau0, tau1);
+    LB_LAUNCH((k_decode<128, 4, 1, true>), dim3(B), dim3(512), st, P, S, logits, lengths, Tc, tau0, tau1);
+  else if (B > cus)
+    LB_LAUNCH((k_decode<256, 2, 4, false>), dim3(B), dim3(512), st, P, S, logits, lengths, Tc, tau0, tau1);
   else
-    LB_LAUNCH((k_decode<256, 4>), dim3(B), dim3(1024), st, P, S, logits, lengths, Tc, tau0, tau1);
+    LB_LAUNCH((k_decode<256, 2, 1, true>), dim3(B), dim3(512), st, P, S, logits, lengths, Tc, tau0, tau1);
   return hipGetLastError();
 }
 
