@@ -553,6 +553,7 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
   constexpr int HS = 2 * KMAX;  // LDS hash slots for the current prefix keys
   constexpr int NW = BLOCK / 64;
   constexpr int NC = (kSep + LPB - 1) / LPB;  // extension slots per lane
+  static_assert(LPB <= 16 && LPB * NC < 64, "a lane's slots stay below symbol 64");
   constexpr int NPM = KMAX * kMaxSub;  // (completed word, sub-beam) pairs per frame, at most
   constexpr int NPL = NPM < 256 ? NPM : 256;  // pairs grouped at once
   constexpr int NEB = NPL / kMaxSub;          // completed words per batch
@@ -569,7 +570,7 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
   if (tau0 >= tend) return;
 
   __shared__ BeamLds<KMAX> sBeam[DB ? 2 : 1];
-  __shared__ double sD[48];  // classes 0..40; 41..47 are zero (slots past the separator)
+  __shared__ double sD[64];  // classes 0..40; 41..63 are zero (slots past the separator)
   __shared__ double sAb2[KMAX], sAnb2[KMAX], sPt2[KMAX], sStay[KMAX];
   __shared__ uint64_t sMask[KMAX];
   __shared__ unsigned long long sHKey[HS];
@@ -641,7 +642,7 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
       const double sum = wave_sum(lane < kClasses ? exp(x - m) : 0.0);
       x = (x - m) - log(sum);
     }
-    if (lane < 48) sD[lane] = lane < kClasses ? Pr.alpha * x : 0.0;
+    sD[lane] = lane < kClasses ? Pr.alpha * x : 0.0;
   };
   // the first frame's row now; each frame loads the next frame's row early and
   // writes it to sD after the frame's last global wait
@@ -757,8 +758,9 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
       c_p = C.pt[hi_];
       c_L = C.Lw[hi_ * kMaxSub];
       // slot k <-> symbol 1 + ln + LPB*k: bit LPB*k of c_rel is its mask bit
-      // (mask bits 41..47 are zero, so slots past the separator are invalid)
-      c_rel = sMask[hi_] >> (1 + ln);
+      // (slots past the separator are invalid: the mask is cut to bits 1..40,
+      // its bits 48..63 hold the node's word count)
+      c_rel = (sMask[hi_] & ((2ull << kSep) - 1ull)) >> (1 + ln);
       c_rep = static_cast<int>(C.meta[hi_] & 0xFF) - 1 - ln;  // LPB*k of the repeat symbol
       c_key = C.key[hi_];
       if (ln == 0) c_stay = sStay[hi_];
@@ -2019,25 +2021,34 @@ int cu_count() {
 
 hipError_t launch_decode(int K, const DevParams& P, const DevState& S, const float* logits,
                          const int32_t* lengths, int32_t B, int32_t Tc, int32_t tau0, int32_t tau1, hipStream_t st) {
-  // One workgroup per stream.  When the batch has more streams than one
-  // round of workgroups holds, the instances that fit more workgroups per CU
-  // (fewer registers, at the price of some spilling) are used: K = 64 with 4
-  // per CU instead of 3, K = 256 with 2 (512 threads, one LDS buffer) instead of 1.
+  // One workgroup per stream.  A batch that leaves CUs to spare gets more
+  // lanes per hypothesis (up to 512 threads per stream, LPB <= 16); a batch
+  // with more streams than one round of workgroups holds gets the instances
+  // that fit more workgroups per CU (fewer registers, at the price of some
+  // spilling): K = 64 with 4 per CU instead of 3, K = 256 with 2 per CU
+  // (one LDS buffer).
   const int cus = cu_count();
-  if (K <= 16)
+  const bool spare = B <= cus;
+  if (K <= 16 && spare)
+    LB_LAUNCH((k_decode<16, 16, 1, true>), dim3(B), dim3(256), st, P, S, logits, lengths, Tc, tau0, tau1);
+  else if (K <= 16)
     LB_LAUNCH((k_decode<16, 4, 1, true>), dim3(B), dim3(64), st, P, S, logits, lengths, Tc, tau0, tau1);
+  else if (K <= 32 && spare)
+    LB_LAUNCH((k_decode<32, 16, 1, true>), dim3(B), dim3(512), st, P, S, logits, lengths, Tc, tau0, tau1);
   else if (K <= 32)
     LB_LAUNCH((k_decode<32, 4, 1, true>), dim3(B), dim3(128), st, P, S, logits, lengths, Tc, tau0, tau1);
+  else if (K <= 64 && spare)
+    LB_LAUNCH((k_decode<64, 8, 1, true>), dim3(B), dim3(512), st, P, S, logits, lengths, Tc, tau0, tau1);
   else if (K <= 64 && B > 3 * cus)
     LB_LAUNCH((k_decode<64, 4, 4, true>), dim3(B), dim3(256), st, P, S, logits, lengths, Tc, tau0, tau1);
   else if (K <= 64)
     LB_LAUNCH((k_decode<64, 4, 1, true>), dim3(B), dim3(256), st, P, S, logits, lengths, Tc, tau0, tau1);
   else if (K <= 128)
     LB_LAUNCH((k_decode<128, 4, 1, true>), dim3(B), dim3(512), st, P, S, logits, lengths, Tc, tau0, tau1);
-  else if (B > cus)
-    LB_LAUNCH((k_decode<256, 2, 4, false>), dim3(B), dim3(512), st, P, S, logits, lengths, Tc, tau0, tau1);
-  else
+  else if (spare)
     LB_LAUNCH((k_decode<256, 2, 1, true>), dim3(B), dim3(512), st, P, S, logits, lengths, Tc, tau0, tau1);
+  else
+    LB_LAUNCH((k_decode<256, 2, 4, false>), dim3(B), dim3(512), st, P, S, logits, lengths, Tc, tau0, tau1);
   return hipGetLastError();
 }
 

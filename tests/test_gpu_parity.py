@@ -121,6 +121,28 @@ def test_zero_length_and_tiny_lexicon():
     check_parity(d, out, range(3), params=p, name="tiny")
 
 
+@pytest.mark.parametrize("name,big", [("t-c1k", 300), ("t-c20k", 300), ("t-c125k", 300), ("t-c125k", 800),
+                                      ("t-k256", 300)])
+def test_launch_instances_by_batch_size(name, big):
+    """The decode kernel has instances per beam size and batch size (more lanes
+    per hypothesis when the batch leaves CUs to spare, more workgroups per CU
+    when it has more streams than one round holds).  A large batch made of
+    copies of a small one decodes every copy exactly like the small batch,
+    which matches the oracle."""
+    d = load_workload(name, batch=4)
+    n = d.logits.shape[0]
+    say(f"[case] instances {name}: B={n} and B={big}")
+    small = gpu_decode(d)
+    check_parity(d, small, range(n), name=f"{name}/B={n}")
+    reps = (big + n - 1) // n
+    tile = lambda a: np.concatenate([a] * reps)[:big]
+    db = WorkloadData(d.workload, d.lexicon, d.lm, tile(d.logits), tile(d.lengths), tile(d.targets),
+                      (d.words * reps)[:big], d.fusion_seed)
+    out = gpu_decode(db)
+    for b in range(big):
+        assert out[b][0] == small[b % n][0] and np.array_equal(out[b][1], small[b % n][1]), b
+
+
 @pytest.mark.parametrize("name", ["t-c20k", "t-c125k", "t-k256"])
 def test_heavy_homophone_paths(name):
     """Nodes with many homophones are scored through the explicit-continuation
