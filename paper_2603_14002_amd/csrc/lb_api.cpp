@@ -139,6 +139,7 @@ struct lb_decoder {
   lb_params p{};
   DevParams P{};
   DevState S{};
+  KArgs* dargs = nullptr;  // device copy of P and S for the decode kernel
   int block = 64;       // workgroup size of the fusion / output kernels (>= beam)
   std::vector<void*> allocs;
   int64_t launches[kKinds] = {};
@@ -600,6 +601,16 @@ lb_status lb_create(const lb_lexicon_desc* lex, const lb_ngram_desc* lm, const l
   P.seed = p.fusion_seed;
   P.lo = p.fusion_lo;
   P.hi = p.fusion_hi;
+  {
+    const KArgs ka{P, S};
+    hipError_t e = hipSuccess;
+    if ((st = d->alloc(&d->dargs, 1)) != LB_OK ||
+        (e = hipMemcpy(d->dargs, &ka, sizeof(KArgs), hipMemcpyHostToDevice)) != hipSuccess) {
+      std::string msg = st != LB_OK ? g_err : std::string("hipMemcpy: ") + hipGetErrorString(e);
+      delete d;
+      return fail(st != LB_OK ? st : LB_ERR_HIP, msg);
+    }
+  }
   *out = d;
   return LB_OK;
 }
@@ -665,7 +676,7 @@ lb_status lb_decode_batch(lb_decoder* d, const float* logits, const int32_t* len
   }
   if (start < stop)
     LB_HIP(launch(kKindDecode,
-                  [&] { return launch_decode(P.K, P, S, logits, lengths, batch, frames, start, stop, st); }));
+                  [&] { return launch_decode(P.K, d->dargs, P, S, logits, lengths, batch, frames, start, stop, st); }));
   if (fuse_tau >= 0) {
     for (int32_t b = 0; b < batch; ++b) {
       const int64_t t = X.t0[b] + fuse_tau;

@@ -186,6 +186,14 @@ struct DevState {
   uint32_t* scrE;
 };
 
+// The decode kernel's parameters and state, kept in device memory (written
+// once by lb_create) and read through a constant-memory pointer.
+struct KArgs {
+  DevParams P;
+  DevState S;
+};
+#define LB_CONST __attribute__((address_space(4)))
+
 // SplitMix64 output for state x (Steele, Lea & Flood, OOPSLA 2014).
 __host__ __device__ inline uint64_t splitmix64(uint64_t x) {
   uint64_t z = x + 0x9E3779B97F4A7C15ull;

@@ -543,12 +543,20 @@ struct BeamLds {
 // 512 threads per CU need 4).  DB: the hypotheses are double-buffered in LDS;
 // otherwise one buffer is rewritten in place (every source entry is read into
 // registers before any new entry is written), which lets two K = 256
-// workgroups share a CU.
-template <int KMAX, int LPB, int WPE, bool DB>
-__global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE))) void k_decode(const DevParams P, const DevState S,
-                                                       const float* __restrict__ logits,
-                                                       const int32_t* __restrict__ lengths, int32_t Tc,
-                                                       int32_t tau0, int32_t tau1) {
+// workgroups share a CU.  CA: P and S are read from the device copy through a
+// constant-memory pointer (else from the by-value arguments).
+template <int KMAX, int LPB, int WPE, bool DB, bool CA>
+__global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE))) void k_decode(
+    const KArgs LB_CONST* A_, const DevParams Pv, const DevState Sv, const float* __restrict__ logits,
+    const int32_t* __restrict__ lengths, int32_t Tc, int32_t tau0, int32_t tau1) {
+  // With CA, P and S are read through a pointer that is made opaque in every
+  // frame, so that each field is loaded (scalar, from the constant cache)
+  // where it is used instead of staying live in scalar registers across the
+  // whole loop
+  const KArgs LB_CONST* A = A_;
+#define P (CA ? *(const DevParams*)(&A->P) : Pv)
+#define S (CA ? *(const DevState*)(&A->S) : Sv)
+
   constexpr int BLOCK = KMAX * LPB;
   constexpr int HS = 2 * KMAX;  // LDS hash slots for the current prefix keys
   constexpr int NW = BLOCK / 64;
@@ -657,6 +665,7 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
     // live in registers across all frames)
     int tid = threadIdx.x;
     asm volatile("" : "+v"(tid));
+    if constexpr (CA) asm volatile("" : "+s"(A));
     const int lane = tid & 63;
     const int wave = tid >> 6;
     BeamLds<KMAX>& C = sBeam[DB ? cur : 0];        // the frame's hypotheses
@@ -1696,6 +1705,9 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
 
 // Selects the top-F hypotheses of stream b by (total desc, key asc) into
 // S.fsel[b][0..F) and S.fsel_n[b] (F = all hypotheses when top_f <= 0).
+#undef P
+#undef S
+
 template <int BLOCK>
 __device__ void select_fused(const DevParams& P, const DevState& S, int b, int top_f, double* sc, uint64_t* ky,
                              uint32_t* ix) {
@@ -2019,36 +2031,49 @@ int cu_count() {
   return n;
 }
 
-hipError_t launch_decode(int K, const DevParams& P, const DevState& S, const float* logits,
-                         const int32_t* lengths, int32_t B, int32_t Tc, int32_t tau0, int32_t tau1, hipStream_t st) {
+hipError_t launch_decode(int K, const KArgs* args, const DevParams& P, const DevState& S, const float* logits,
+                         const int32_t* lengths, int32_t B, int32_t Tc, int32_t tau0, int32_t tau1,
+                         hipStream_t st) {
+  const KArgs LB_CONST* A = (const KArgs LB_CONST*)args;
   // One workgroup per stream.  A batch that leaves CUs to spare gets more
   // lanes per hypothesis (up to 512 threads per stream, LPB <= 16); a batch
   // with more streams than one round of workgroups holds gets the instances
   // that fit more workgroups per CU (fewer registers, at the price of some
   // spilling): K = 64 with 4 per CU instead of 3, K = 256 with 2 per CU
-  // (one LDS buffer).
+  // (one LDS buffer, by-value arguments: constant-memory loads there make the
+  // LDS waits coarser).
   const int cus = cu_count();
   const bool spare = B <= cus;
   if (K <= 16 && spare)
-    LB_LAUNCH((k_decode<16, 16, 1, true>), dim3(B), dim3(256), st, P, S, logits, lengths, Tc, tau0, tau1);
+    LB_LAUNCH((k_decode<16, 16, 1, true, true>), dim3(B), dim3(256), st, A, P, S, logits, lengths, Tc,
+              tau0, tau1);
   else if (K <= 16)
-    LB_LAUNCH((k_decode<16, 4, 1, true>), dim3(B), dim3(64), st, P, S, logits, lengths, Tc, tau0, tau1);
+    LB_LAUNCH((k_decode<16, 4, 1, true, true>), dim3(B), dim3(64), st, A, P, S, logits, lengths, Tc,
+              tau0, tau1);
   else if (K <= 32 && spare)
-    LB_LAUNCH((k_decode<32, 16, 1, true>), dim3(B), dim3(512), st, P, S, logits, lengths, Tc, tau0, tau1);
+    LB_LAUNCH((k_decode<32, 16, 1, true, true>), dim3(B), dim3(512), st, A, P, S, logits, lengths, Tc,
+              tau0, tau1);
   else if (K <= 32)
-    LB_LAUNCH((k_decode<32, 4, 1, true>), dim3(B), dim3(128), st, P, S, logits, lengths, Tc, tau0, tau1);
+    LB_LAUNCH((k_decode<32, 4, 1, true, true>), dim3(B), dim3(128), st, A, P, S, logits, lengths, Tc,
+              tau0, tau1);
   else if (K <= 64 && spare)
-    LB_LAUNCH((k_decode<64, 8, 1, true>), dim3(B), dim3(512), st, P, S, logits, lengths, Tc, tau0, tau1);
+    LB_LAUNCH((k_decode<64, 8, 1, true, true>), dim3(B), dim3(512), st, A, P, S, logits, lengths, Tc,
+              tau0, tau1);
   else if (K <= 64 && B > 3 * cus)
-    LB_LAUNCH((k_decode<64, 4, 4, true>), dim3(B), dim3(256), st, P, S, logits, lengths, Tc, tau0, tau1);
+    LB_LAUNCH((k_decode<64, 4, 4, true, true>), dim3(B), dim3(256), st, A, P, S, logits, lengths, Tc,
+              tau0, tau1);
   else if (K <= 64)
-    LB_LAUNCH((k_decode<64, 4, 1, true>), dim3(B), dim3(256), st, P, S, logits, lengths, Tc, tau0, tau1);
+    LB_LAUNCH((k_decode<64, 4, 1, true, true>), dim3(B), dim3(256), st, A, P, S, logits, lengths, Tc,
+              tau0, tau1);
   else if (K <= 128)
-    LB_LAUNCH((k_decode<128, 4, 1, true>), dim3(B), dim3(512), st, P, S, logits, lengths, Tc, tau0, tau1);
+    LB_LAUNCH((k_decode<128, 4, 1, true, true>), dim3(B), dim3(512), st, A, P, S, logits, lengths, Tc,
+              tau0, tau1);
   else if (spare)
-    LB_LAUNCH((k_decode<256, 2, 1, true>), dim3(B), dim3(512), st, P, S, logits, lengths, Tc, tau0, tau1);
+    LB_LAUNCH((k_decode<256, 2, 1, true, true>), dim3(B), dim3(512), st, A, P, S, logits, lengths, Tc,
+              tau0, tau1);
   else
-    LB_LAUNCH((k_decode<256, 2, 4, false>), dim3(B), dim3(512), st, P, S, logits, lengths, Tc, tau0, tau1);
+    LB_LAUNCH((k_decode<256, 2, 4, false, false>), dim3(B), dim3(512), st, A, P, S, logits, lengths, Tc,
+              tau0, tau1);
   return hipGetLastError();
 }
 
