@@ -600,6 +600,11 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
   uint32_t* const sHisto = reinterpret_cast<uint32_t*>(sSel);
   double* const sBScore = reinterpret_cast<double*>(sSel + kBins * 4);
   uint64_t* const sBKey = reinterpret_cast<uint64_t*>(sSel + kBins * 4 + kBoundaryCap * 8);
+  // write-back staging of the sub-beams (one-buffer instances), past the
+  // grouping keys that the write-back clears
+  double* const sStL = reinterpret_cast<double*>(sSel + 8 * NPL);
+  uint32_t* const sStH = reinterpret_cast<uint32_t*>(sStL + KMAX * kMaxSub);
+  static_assert(DB || 8 * NPL + 12 * KMAX * kMaxSub <= UNI_BYTES, "write-back staging fits the shared scratch");
 
   const size_t gb = static_cast<size_t>(b) * P.K;
   const int O = P.O;
@@ -849,6 +854,9 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
     // level-0 bin of each of the lane's candidates, kept packed 16 bits per slot
     // (0xFFFF: no candidate); exact scores are recomputed only inside the boundary bin
     uint32_t binp[(NC + 1) / 2];
+    // (the candidates' inputs are made opaque here so that their scores are
+    // recomputed below instead of being kept live across the block reduction)
+    asm volatile("" : "+v"(c_ab), "+v"(c_p), "+v"(c_L), "+v"(c_rel), "+v"(c_key));
     uint32_t bin_stay = 0xFFFFu;
     if (c_stay != kNegInf && c_stay >= thr) {
       bin_stay = static_cast<uint32_t>(bin0(0, c_stay));
@@ -1065,10 +1073,19 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
         }
       }
       const int nsub = (meta_i >> 8) & 0xFF;
+      if constexpr (DB) {
 #pragma unroll
-      for (int j = 0; j < kMaxSub; ++j) {
-        w_Lw[j] = j < nsub ? C.Lw[i * kMaxSub + j] : 0.0;
-        w_hist[j] = j < nsub ? C.hist[i * kMaxSub + j] : 0u;
+        for (int j = 0; j < kMaxSub; ++j) {
+          w_Lw[j] = j < nsub ? C.Lw[i * kMaxSub + j] : 0.0;
+          w_hist[j] = j < nsub ? C.hist[i * kMaxSub + j] : 0u;
+        }
+      } else {
+        // in place: the sub-beams go through the free part of the shared
+        // scratch (registers would spill)
+        for (int j = 0; j < nsub; ++j) {
+          sStL[r * kMaxSub + j] = C.Lw[i * kMaxSub + j];
+          sStH[r * kMaxSub + j] = C.hist[i * kMaxSub + j];
+        }
       }
     }
     if constexpr (!DB) lds_barrier();  // every source entry has been read
@@ -1086,11 +1103,18 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
         N.woff[r] = w_woff;
       }
       const int nsub = (w_meta >> 8) & 0xFF;
+      if constexpr (DB) {
 #pragma unroll
-      for (int j = 0; j < kMaxSub; ++j) {
-        if (j < nsub) {
-          N.Lw[r * kMaxSub + j] = w_Lw[j];
-          N.hist[r * kMaxSub + j] = w_hist[j];
+        for (int j = 0; j < kMaxSub; ++j) {
+          if (j < nsub) {
+            N.Lw[r * kMaxSub + j] = w_Lw[j];
+            N.hist[r * kMaxSub + j] = w_hist[j];
+          }
+        }
+      } else {
+        for (int j = 0; j < nsub; ++j) {
+          N.Lw[r * kMaxSub + j] = sStL[r * kMaxSub + j];
+          N.hist[r * kMaxSub + j] = sStH[r * kMaxSub + j];
         }
       }
     }
