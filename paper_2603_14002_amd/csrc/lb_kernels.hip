@@ -1032,8 +1032,6 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
     uint64_t w_key = 0, w_pkey = 0, w_tmask = 0;
     double w_ab = 0.0, w_anb = 0.0, w_pt = 0.0;
     uint32_t w_node = 0, w_meta = 0, w_first = 0, w_woff = 0;
-    double w_Lw[kMaxSub];
-    uint32_t w_hist[kMaxSub];
     if (r < nsel) {
       const uint32_t src = sSelSrc[r];
       const int i = src & 0xFFFF;
@@ -1074,10 +1072,10 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
       }
       const int nsub = (meta_i >> 8) & 0xFF;
       if constexpr (DB) {
-#pragma unroll
-        for (int j = 0; j < kMaxSub; ++j) {
-          w_Lw[j] = j < nsub ? C.Lw[i * kMaxSub + j] : 0.0;
-          w_hist[j] = j < nsub ? C.hist[i * kMaxSub + j] : 0u;
+        // two buffers: the sub-beams are copied straight across
+        for (int j = 0; j < nsub; ++j) {
+          N.Lw[r * kMaxSub + j] = C.Lw[i * kMaxSub + j];
+          N.hist[r * kMaxSub + j] = C.hist[i * kMaxSub + j];
         }
       } else {
         // in place: the sub-beams go through the free part of the shared
@@ -1102,16 +1100,8 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
         N.first[r] = w_first;
         N.woff[r] = w_woff;
       }
-      const int nsub = (w_meta >> 8) & 0xFF;
-      if constexpr (DB) {
-#pragma unroll
-        for (int j = 0; j < kMaxSub; ++j) {
-          if (j < nsub) {
-            N.Lw[r * kMaxSub + j] = w_Lw[j];
-            N.hist[r * kMaxSub + j] = w_hist[j];
-          }
-        }
-      } else {
+      if constexpr (!DB) {
+        const int nsub = (w_meta >> 8) & 0xFF;
         for (int j = 0; j < nsub; ++j) {
           N.Lw[r * kMaxSub + j] = sStL[r * kMaxSub + j];
           N.hist[r * kMaxSub + j] = sStH[r * kMaxSub + j];
