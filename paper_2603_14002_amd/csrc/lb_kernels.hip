@@ -581,7 +581,8 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
   __shared__ double sD[64];  // classes 0..40; 41..63 are zero (slots past the separator)
   __shared__ double sAb2[KMAX], sAnb2[KMAX], sPt2[KMAX], sStay[KMAX];
   __shared__ uint64_t sMask[KMAX];
-  __shared__ unsigned long long sHKey[HS];
+  // two tables: the one of this frame, and the next frame's, cleared meanwhile
+  __shared__ unsigned long long sHKey[2][HS];
   __shared__ int32_t sHIdx[HS];
   // top-K selection scratch; the LM step and the fusion sort reuse it
   __shared__ __align__(16) unsigned char sSel[UNI_BYTES];
@@ -640,6 +641,8 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
   if (tid < 3) sCnt[tid] = 0;
   uint32_t arena_n = S.arena_n[b];
   int cur = 0;  // the current buffer (DB)
+  int hb = 0;   // the current prefix-key table
+  for (int q = tid; q < HS; q += BLOCK) sHKey[0][q] = kEmptyKey;
   uint32_t lines = 0, c_words = 0;  // per thread
   uint64_t c_queries = 0;
   uint64_t c_exp = 0, c_fused = 0, c_lookups = 0;  // uniform
@@ -678,26 +681,22 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
 
     // the next frame's log-probs are loaded meanwhile
     if (tid < kClasses && tau + 1 < tend) dnext = logits[(static_cast<size_t>(b) * Tc + tau + 1) * kClasses + tid];
-    for (int s = tid; s < HS; s += BLOCK) sHKey[s] = kEmptyKey;
+    unsigned long long* const hkey = sHKey[hb];
+    for (int s = tid; s < HS; s += BLOCK) sHKey[hb ^ 1][s] = kEmptyKey;
     for (int d = tid; d < kBins; d += BLOCK) sHisto[d] = 0;
     if (tid == 0) sBCount = 0;
-    uint64_t my_key = 0, my_pkey = kNoParent;
-    double my_anb = kNegInf;
+
+    // ---- prefix keys into an LDS hash table (cleared during the last frame)
+    uint64_t my_pkey = kNoParent;
     uint32_t my_meta = 0;
     if (tid < n) {
-      my_key = C.key[tid];
+      const uint64_t my_key = C.key[tid];
       my_pkey = C.pkey[tid];
-      my_anb = C.anb[tid];
       my_meta = C.meta[tid];
       sMask[tid] = C.tmask[tid];
-    }
-    lds_barrier();
-
-    // ---- prefix keys into an LDS hash table
-    if (tid < n) {
       uint32_t s = static_cast<uint32_t>(my_key) & (HS - 1);
       for (;;) {
-        const unsigned long long prev = atomicCAS(&sHKey[s], kEmptyKey, my_key);
+        const unsigned long long prev = atomicCAS(&hkey[s], kEmptyKey, my_key);
         if (prev == kEmptyKey) {
           sHIdx[s] = tid;
           break;
@@ -709,28 +708,26 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
 
     // ---- recombination: a hypothesis whose parent prefix is also live receives
     // the parent's extension by its last symbol; that extension is removed from
-    // the parent's fan-out.
-    int par = -1;
-    if (tid < n && my_pkey != kNoParent) {
-      uint32_t s = static_cast<uint32_t>(my_pkey) & (HS - 1);
-      for (int probes = 0; probes < HS; ++probes) {
-        const unsigned long long k = sHKey[s];
-        if (k == kEmptyKey) break;
-        if (k == my_pkey) {
-          par = sHIdx[s];
-          break;
-        }
-        s = (s + 1) & (HS - 1);
-      }
-      if (par >= 0) atomicAnd(reinterpret_cast<unsigned long long*>(&sMask[par]), ~(1ull << (my_meta & 0xFF)));
-    }
-    lds_barrier();
-
-    // ---- stay candidates (blank-stay, repeat-stay, merged parent extension)
+    // the parent's fan-out.  Stay candidates: blank-stay, repeat-stay, merged
+    // parent extension.
     if (tid < n) {
+      int par = -1;
+      if (my_pkey != kNoParent) {
+        uint32_t s = static_cast<uint32_t>(my_pkey) & (HS - 1);
+        for (int probes = 0; probes < HS; ++probes) {
+          const unsigned long long k = hkey[s];
+          if (k == kEmptyKey) break;
+          if (k == my_pkey) {
+            par = sHIdx[s];
+            break;
+          }
+          s = (s + 1) & (HS - 1);
+        }
+        if (par >= 0) atomicAnd(reinterpret_cast<unsigned long long*>(&sMask[par]), ~(1ull << (my_meta & 0xFF)));
+      }
       const int last = my_meta & 0xFF;
       const double ab2 = C.pt[tid] + sD[0];
-      const double rep = last ? my_anb + sD[last] : kNegInf;
+      const double rep = last ? C.anb[tid] + sD[last] : kNegInf;
       double ext = kNegInf;
       if (par >= 0) {
         const double base = (last == static_cast<int>(C.meta[par] & 0xFF)) ? C.ab[par] : C.pt[par];
@@ -757,6 +754,7 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
       sStay[tid] = pt2 + C.Lw[tid * kMaxSub];
     }
     lds_barrier();
+    hb ^= 1;
 
     // ---- this lane's candidates: slot k is the extension by v = 1 + ln + LPB*k,
     // plus the merged stay on lane 0; scores are recomputed in every pass (same
