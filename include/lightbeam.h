@@ -148,9 +148,12 @@ typedef struct lb_stats {
   int64_t lm_queries;   /* (sub-beam, homophone) n-gram queries                   */
   int64_t fused;        /* hypotheses rescored by delayed fusion                  */
   int64_t frames;       /* stream-frames decoded                                  */
-  int64_t probe_lines;  /* 64-B n-gram hash-table lines read by the LM lookups    */
+  int64_t probe_lines;  /* 64-B hash-table lines read by the LM lookups (n-gram
+                           tables and the explicit-continuation index)           */
   int64_t lm_lookups;   /* n-gram lookups done: one per distinct (context, word)
-                           among a stream-frame's queries                        */
+                           among a stream-frame's queries, except homophones of
+                           heavy nodes that the continuation index shows to back
+                           off to their unigram (scored without a lookup)       */
   int64_t launches[8];  /* kernel launches: [0] decode (all frames of a call), [1]
                            output, [2] external-fusion select, [3] export, [4]
                            apply, [5] stream reset, [6..7] unused                */

@@ -534,16 +534,19 @@ struct BeamLds {
 //     exact rank inside the boundary bin), beam update, trie-state advance;
 //     hypothesis i is owned by LPB consecutive lanes: lane s of it handles the
 //     extensions v = 1+s, 1+s+LPB, ... and lane 0 also the merged stay;
-//   * Eq. (1) for the hypotheses that completed a word: every (sub-beam,
-//     homophone) pair is scored with the 4-gram backoff LM, the pairs spread
-//     over all threads; the top-o survive lambda pruning and receive
-//     word-history nodes;
+//   * Eq. (1) for the hypotheses that completed a word (in batches of NEB
+//     words): the (word, sub-beam) pairs are grouped by (n-gram context, trie
+//     node); each group is looked up once per homophone, or, for a node with
+//     many homophones, only for those the explicit-continuation index lists
+//     (the others back off to their unigrams); the lookups are spread over all
+//     threads; each word's top-o (one thread per word, or a wavefront for a
+//     word with a large fully looked-up group) survive lambda pruning and
+//     receive word-history nodes;
 //   * Eq. (2) with the synthetic scorer on fusion frames.
 // WPE: wavefronts per SIMD the register allocation aims for (two workgroups of
 // 512 threads per CU need 4).  DB: the hypotheses are double-buffered in LDS;
-// otherwise one buffer is rewritten in place (every source entry is read into
-// registers before any new entry is written), which lets two K = 256
-// workgroups share a CU.  CA: P and S are read from the device copy through a
+// otherwise one buffer is rewritten in place (every source entry is read before
+// any new entry is written), which lets two K = 256 workgroups share a CU.  CA: P and S are read from the device copy through a
 // constant-memory pointer (else from the by-value arguments).
 template <int KMAX, int LPB, int WPE, bool DB, bool CA>
 __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE))) void k_decode(
