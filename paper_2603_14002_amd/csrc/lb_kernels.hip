@@ -1239,6 +1239,15 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
       U = 0;
     }
     c_lookups += static_cast<uint64_t>(U);
+    // the results go to LDS when they fit in the grouping keys freed above (the
+    // usual case), else to the stream's scratch in global memory (always in
+    // the two-per-CU K = 256 instance, where the LDS path costs registers)
+    constexpr int kLdsRes = 12 * NPL / 32;
+    double* const sResL = reinterpret_cast<double*>(sSel);
+    QState* const sResS = reinterpret_cast<QState*>(sSel + 8 * kLdsRes);
+    const bool res_lds = CA && U <= kLdsRes;
+    auto res_lp = [&](int u) -> double { return res_lds ? sResL[u] : scrL[u]; };
+    auto res_st = [&](int u) -> QState { return res_lds ? sResS[u] : scrS[u]; };
     lds_barrier();
     for (int u = tid; u < U; u += BLOCK) {
       int lo = 0, hi = NG - 1;
@@ -1250,10 +1259,18 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
       const uint32_t h = (sGcnt[lo] & kGroupHeavy) ? scrE[static_cast<size_t>(lo) * kMaxExplicit + k] : k;
       const int32_t w = S.trie_words[sGwoff[lo] + h];
       const LmResult res = lm_lookup(S, w, sGctx[lo], &lines);
-      scrL[u] = res.lp;
-      scrS[u] = res.st;
+      if (res_lds) {
+        sResL[u] = res.lp;
+        sResS[u] = res.st;
+      } else {
+        scrL[u] = res.lp;
+        scrS[u] = res.st;
+      }
     }
-    __syncthreads();  // the lookup results (global memory) are read by other threads
+    if (res_lds)
+      lds_barrier();
+    else
+      __syncthreads();  // the lookup results (global memory) are read by other threads
     // each completed word: its top-o by (score desc, j*H + h asc), lambda
     // pruning, word-history nodes (o reserved per word, in order).  A
     // candidate's source: its lookup result in the scratch (>= 0), or, for a
@@ -1267,7 +1284,7 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
       const uint32_t rr = sEvBeam[e];
       QState st;
       if (src >= 0) {
-        st = scrS[src];
+        st = res_st(src);
       } else {
         const WordRank wr = S.wrank[sEvWoff[e] + static_cast<uint32_t>(-1 - src)];
         st.c2 = kNone;
@@ -1362,7 +1379,7 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
             const int off = sGoff[g];
             const uint32_t cnt = sGcnt[g];
             if (!(cnt & kGroupHeavy)) {
-              for (int h = 0; h < H; ++h) insert(Lw + P.comega * scrL[off + h], j * H + h, off + h);
+              for (int h = 0; h < H; ++h) insert(Lw + P.comega * res_lp(off + h), j * H + h, off + h);
             } else {
               any_heavy = true;
               const uint32_t* E = scrE + static_cast<size_t>(g) * kMaxExplicit;
@@ -1371,7 +1388,7 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
                 const uint32_t hm = E[m];
                 bool dup = false;
                 for (int m2 = 0; m2 < m; ++m2) dup |= E[m2] == hm;
-                if (!dup) insert(Lw + P.comega * scrL[off + m], j * H + static_cast<int>(hm), off + m);
+                if (!dup) insert(Lw + P.comega * res_lp(off + m), j * H + static_cast<int>(hm), off + m);
               }
             }
           }
@@ -1489,7 +1506,7 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
           double a[kMaxSub];
 #pragma unroll
           for (int j = 0; j < kMaxSub; ++j)
-            a[j] = (j < nsub && !(gcnt[j] & kGroupHeavy)) ? scrL[goff[j] + h] : 0.0;
+            a[j] = (j < nsub && !(gcnt[j] & kGroupHeavy)) ? res_lp(goff[j] + h) : 0.0;
 #pragma unroll
           for (int j = 0; j < kMaxSub; ++j)
             if (j < nsub && !(gcnt[j] & kGroupHeavy))
@@ -1516,7 +1533,7 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
               dup |= m < lane && x == eh[j];
             }
             if (lane < ne[j] && !dup)
-              insert(Lw[j] + P.comega * scrL[goff[j] + lane], j * static_cast<int>(H) + static_cast<int>(eh[j]),
+              insert(Lw[j] + P.comega * res_lp(goff[j] + lane), j * static_cast<int>(H) + static_cast<int>(eh[j]),
                      goff[j] + lane);
           }
         }
