@@ -1869,6 +1869,33 @@ __global__ __launch_bounds__(BLOCK) void k_fuse_select(const DevParams P, const 
 // External scorer, step 2: word sequences of every sub-beam of the selected
 // hypotheses, words [B][K][O][W] (-1 padded) and n_words [B][K][O] (-1 where
 // nothing is to be scored).
+// Writes -1 past each row's words: rows [nrows][W] with len[r] words in row r;
+// the whole block on consecutive addresses, 16 B per store when W allows.
+template <int BLOCK>
+__device__ inline void pad_rows(int32_t* rows, int nrows, int W, const int32_t* len) {
+  if ((W & 3) == 0 && (reinterpret_cast<uintptr_t>(rows) & 15) == 0) {
+    const int W4 = W >> 2;
+    for (int r = 0; r < nrows; ++r) {
+      int4* row = reinterpret_cast<int4*>(rows + static_cast<size_t>(r) * W);
+      const int n = len[r];
+      for (int c = threadIdx.x; c < W4; c += BLOCK) {
+        const int c0 = 4 * c;
+        if (c0 >= n) {
+          row[c] = make_int4(-1, -1, -1, -1);
+        } else if (c0 + 3 >= n) {
+          int32_t* e = rows + static_cast<size_t>(r) * W + c0;
+          for (int q = n - c0; q < 4; ++q) e[q] = -1;
+        }
+      }
+    }
+  } else {
+    for (int r = 0; r < nrows; ++r) {
+      int32_t* row = rows + static_cast<size_t>(r) * W;
+      for (int c = len[r] + static_cast<int>(threadIdx.x); c < W; c += BLOCK) row[c] = -1;
+    }
+  }
+}
+
 // Writes the `depth` words of history h into row[0..min(depth, W)), four per
 // node read (the node's word and its window of three ancestors' words).
 __device__ inline void trace_words(const DevState& S, uint32_t h, int depth, int32_t* row, int W) {
@@ -1913,13 +1940,7 @@ __global__ __launch_bounds__(BLOCK) void k_fuse_export(const DevParams P, const 
     n_words[slot] = len;
   }
   __syncthreads();
-  // -1 past each row's words, the whole block on consecutive addresses
-  int32_t* const rows = words + gb * P.O * P.W;
-  const int total = P.K * P.O * P.W;
-  for (int x = threadIdx.x; x < total; x += BLOCK) {
-    const int idx = x / P.W;
-    if (x - idx * P.W >= sLen[idx]) rows[x] = -1;
-  }
+  pad_rows<BLOCK>(words + gb * P.O * P.W, P.K * P.O, P.W, sLen);
 }
 
 // External scorer, step 3: apply the caller's scores [B][K][O] to the selection.
@@ -1990,13 +2011,7 @@ __global__ __launch_bounds__(BLOCK) void k_output(const DevParams P, const DevSt
     sLen[r] = n < P.W ? n : P.W;
   }
   __syncthreads();
-  // -1 past each row's words, the whole block on consecutive addresses
-  int32_t* const rows = out_hyps + static_cast<size_t>(b) * P.K * P.W;
-  const int total = P.K * P.W;
-  for (int x = tid; x < total; x += BLOCK) {
-    const int r = x / P.W;
-    if (x - r * P.W >= sLen[r]) rows[x] = -1;
-  }
+  pad_rows<BLOCK>(out_hyps + static_cast<size_t>(b) * P.K * P.W, P.K, P.W, sLen);
 }
 
 }  // namespace

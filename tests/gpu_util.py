@@ -69,6 +69,7 @@ def gpu_decode(d, params=None, chunk: int = 0, batch: Optional[int] = None, fusi
     assert st == lbm.LB_OK, lbm.lb_last_error()
     H = hyps.cpu().numpy()
     S = scores.cpu().numpy()
+    check_padding(H, S)
     out = []
     for b in range(B):
         words, sc = [], []
@@ -84,6 +85,17 @@ def gpu_decode(d, params=None, chunk: int = 0, batch: Optional[int] = None, fusi
         return out, dec
     dec.close()
     return out
+
+
+def check_padding(H: np.ndarray, S: np.ndarray) -> None:
+    """Every output row holds its words, then -1 to the end; ranks past the
+    last hypothesis are all -1 with a score of -inf."""
+    neg = H < 0
+    first = np.where(neg.any(-1), neg.argmax(-1), H.shape[-1])
+    tail = np.arange(H.shape[-1]) >= first[..., None]
+    assert np.all(H[tail] == -1), "output rows not -1 padded after their words"
+    empty = ~np.isfinite(S)
+    assert np.all(H[empty] == -1), "ranks without a hypothesis not all -1"
 
 
 @dataclass

@@ -276,6 +276,8 @@ def test_external_fusion_round_trip(name):
             lbm.lb_fusion_request(dec.handle, words, nw, None)
             torch.cuda.synchronize()
             Wh, Nh = words.cpu().numpy(), nw.cpu().numpy()
+            # each request row: its words, then -1 (rows not asked for: all -1)
+            assert np.all(Wh[np.arange(Wh.shape[-1]) >= np.maximum(Nh, 0)[..., None]] == -1)
             fs = np.zeros((B, K, O), np.float32)
             for b, r, j in zip(*np.nonzero(Nh >= 0)):
                 s = orc.fusion_score(op, [int(x) for x in Wh[b, r, j, :Nh[b, r, j]]])
