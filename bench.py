@@ -118,8 +118,10 @@ def algorithmic_bytes(s, B, T, p, lp):
     continuation-index tables), per lookup the unigram entry (8 B) and the word
     id (4 B) (the queries of a stream-frame that share context and word are
     looked up once; homophones that back off to their unigram are not looked
-    up), and per completed word and sub-beam the context's 64-B history node
-    read and a 64-B history node written (at most o per completed word)."""
+    up), per completed word and sub-beam the context's 64-B history node
+    read and a 64-B history node written (at most o per completed word), and,
+    when the decode launch also writes the call's output (no separate output
+    launch), the output rows: B x K x (W word ids + a score), 4 B each."""
     state = 48 + 12 * p.subbeams          # key, pkey, a_b, a_nb, total, node, meta + o x (L, hist)
     calls = max(1, int(s.launches[0]))
     parts = {
@@ -130,6 +132,9 @@ def algorithmic_bytes(s, B, T, p, lp):
         "ngram_other": float(s.lm_lookups) * (8 + 4),
         "history_nodes": float(s.word_events) * p.subbeams * 128.0,
     }
+    import paper_2603_14002_amd as lbm
+    if int(s.launches[lbm.KIND_OUTPUT]) == 0:
+        parts["output"] = float(calls) * B * p.beam * (lp.max_words_out + 1) * 4.0
     parts["total"] = sum(parts.values())
     return parts
 

@@ -458,7 +458,7 @@ lb_status build_tables(lb_decoder* d, const HostTrie& trie, const lb_ngram_desc*
 
   // root of the word-history arena: the empty history, context <s>
   HistNode root{};
-  root.parent = kNone;
+  root.blk = kNone;
   root.word = lm->bos_id;
   root.c2 = kNone;
   root.c3 = kNone;
@@ -467,8 +467,7 @@ lb_status build_tables(lb_decoder* d, const HostTrie& trie, const lb_ngram_desc*
   root.bo3 = 0.0f;
   root.sfus = 0.0;
   root.depth = 0;
-  root.w1 = root.w2 = root.w3 = -1;
-  root.up2 = root.up3 = root.up4 = kNone;
+  for (int i = 0; i < kHistBlock - 1; ++i) root.w[i] = -1;
   LB_HIP(hipMemcpy(d->S.arena, &root, sizeof(root), hipMemcpyHostToDevice));
   return LB_OK;
 }
@@ -674,9 +673,16 @@ lb_status lb_decode_batch(lb_decoder* d, const float* logits, const int32_t* len
     }
     if (fuse_tau >= 0) stop = fuse_tau + 1;
   }
+  // the output is written by the decode launch itself when nothing else
+  // follows it in this call (no fusion round trip), else by k_output
+  const int32_t fin = (flags & LB_END) ? 1 : 0;
+  const bool out_here = start < stop && fuse_tau < 0 && !(external && fin && !X.final_done);
+  bool out_done = false;
   if (start < stop)
-    LB_HIP(launch(kKindDecode,
-                  [&] { return launch_decode(P.K, d->dargs, P, S, logits, lengths, batch, frames, start, stop, st); }));
+    LB_HIP(launch(kKindDecode, [&] {
+      return launch_decode(P.K, d->dargs, P, S, logits, lengths, batch, frames, start, stop, out_here ? fin : 0,
+                           out_here ? out_hyps : nullptr, out_here ? out_scores : nullptr, &out_done, st);
+    }));
   if (fuse_tau >= 0) {
     for (int32_t b = 0; b < batch; ++b) {
       const int64_t t = X.t0[b] + fuse_tau;
@@ -699,9 +705,8 @@ lb_status lb_decode_batch(lb_decoder* d, const float* logits, const int32_t* len
     X.resume_tau = frames;
     return LB_NEED_FUSION;
   }
-  LB_HIP(launch(kKindOutput, [&] {
-    return launch_output(d->block, P, S, lengths, batch, (flags & LB_END) ? 1 : 0, out_hyps, out_scores, st);
-  }));
+  if (!out_done)
+    LB_HIP(launch(kKindOutput, [&] { return launch_output(d->block, P, S, lengths, batch, fin, out_hyps, out_scores, st); }));
   if (external) {
     for (int32_t b = 0; b < batch; ++b) X.t0[b] += X.len[b];
     X.in_call = false;

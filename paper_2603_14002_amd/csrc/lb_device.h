@@ -105,23 +105,26 @@ struct PresTable {
   const uint32_t* lists;
 };
 
-// Word-history node (64 B, one line): the word sequence (parent chain) of an
-// orthographic sub-beam plus the n-gram state after its last word: the word
-// itself (the 1-word context), the slots of the 2- and 3-word contexts (kNone
-// if absent) and the three backoff weights, the number of words in the chain,
-// the running synthetic fusion score, and a window for tracing words back:
-// the words of the three nearest ancestors and the ancestors 2, 3 and 4
-// levels up (fields past the root are not read).
+// Word-history node (64 B, one line): the word sequence of an orthographic
+// sub-beam plus the n-gram state after its last word: the word itself (the
+// 1-word context), the slots of the 2- and 3-word contexts (kNone if absent)
+// and the three backoff weights, the number of words in the chain (depth), the
+// running synthetic fusion score, and what a traceback needs.  The chain is
+// cut into blocks of kHistBlock words (depths 1..7, 8..14, ...): a node keeps
+// the words of the earlier nodes of its own block, nearest first, in w[0 ..
+// (depth - 1) % kHistBlock), and `blk`, the node that ends the previous block
+// (depth kHistBlock * floor((depth - 1) / kHistBlock); the root ends block 0),
+// so a traceback reads one node per block.
+constexpr int kHistBlock = 7;
 struct HistNode {
-  uint32_t parent;
+  uint32_t blk;
   int32_t word;
   uint32_t c2;
   uint32_t c3;
   float bo1, bo2, bo3;
   uint32_t depth;
   double sfus;
-  int32_t w1, w2, w3;
-  uint32_t up2, up3, up4;
+  int32_t w[kHistBlock - 1];
 };
 static_assert(sizeof(HistNode) == 64, "history node is one 64-B line");
 

@@ -4,8 +4,10 @@
 // workgroup per stream runs Alg. 1 over the call's frames with the stream's
 // beam resident in LDS (fan-out, recombination, theta / top-K pruning, trie
 // advance, Eq. (1) with the hashed 4-gram LM, Eq. (2) with the synthetic
-// scorer).  k_output ranks the hypotheses of each stream and writes word ids /
-// scores (after the final fusion at the end of an utterance).  k_fuse_select,
+// scorer).  The output -- each stream's hypotheses ranked, their word ids and
+// scores written (after the final fusion at the end of an utterance) -- is
+// written by the call's last k_decode launch, or by k_output when the call
+// ends without one.  k_fuse_select,
 // k_fuse_export and k_fuse_apply carry the round trip to an external fusion
 // scorer; k_build_order fills the n-gram hash tables; k_begin resets streams.
 #include <hip/hip_ext.h>
@@ -525,6 +527,11 @@ struct BeamLds {
   uint32_t woff[KMAX];   // the trie node's first word in trie_words
 };
 
+template <int NT, int N>
+__device__ __forceinline__ void emit_output(const DevParams& P, const DevState& S, int b, const int32_t* lengths, int32_t fin,
+                            int32_t* out_hyps, float* out_scores, double* sc, uint64_t* ky, uint32_t* ix,
+                            int32_t* sScan);
+
 // Frames [tau0, min(tau1, length)) of Alg. 1 for every stream: one workgroup
 // per stream, which keeps the stream's beam in LDS from frame to frame.  Each
 // frame:
@@ -551,7 +558,8 @@ struct BeamLds {
 template <int KMAX, int LPB, int WPE, bool DB, bool CA>
 __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE))) void k_decode(
     const KArgs LB_CONST* A_, const DevParams Pv, const DevState Sv, const float* __restrict__ logits,
-    const int32_t* __restrict__ lengths, int32_t Tc, int32_t tau0, int32_t tau1) {
+    const int32_t* __restrict__ lengths, int32_t Tc, int32_t tau0, int32_t tau1, int32_t out_fin,
+    int32_t* __restrict__ out_hyps, float* __restrict__ out_scores) {
   // With CA, P and S are read through a pointer that is made opaque in every
   // frame, so that each field is loaded (scalar, from the constant cache)
   // where it is used instead of staying live in scalar registers across the
@@ -578,7 +586,6 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
   const int wave = tid >> 6;
   const int len = lengths[b];
   const int tend = len < tau1 ? len : tau1;
-  if (tau0 >= tend) return;
 
   __shared__ BeamLds<KMAX> sBeam[DB ? 2 : 1];
   __shared__ double sD[64];  // classes 0..40; 41..63 are zero (slots past the separator)
@@ -609,6 +616,19 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
   double* const sStL = reinterpret_cast<double*>(sSel + 8 * NPL);
   uint32_t* const sStH = reinterpret_cast<uint32_t*>(sStL + KMAX * kMaxSub);
   static_assert(DB || 8 * NPL + 12 * KMAX * kMaxSub <= UNI_BYTES, "write-back staging fits the shared scratch");
+  // the output (when this launch writes it) sorts in the shared scratch.  The
+  // instance with by-value arguments never writes it: the output pointers would
+  // stay live in scalar registers across the frame loop
+  constexpr bool kOut = CA;
+  auto output = [&](const DevParams& Pr, const DevState& Sr) {
+    emit_output<BLOCK, KMAX>(Pr, Sr, b, lengths, out_fin, out_hyps, out_scores, reinterpret_cast<double*>(sSel),
+                             reinterpret_cast<uint64_t*>(sSel + 8 * KMAX),
+                             reinterpret_cast<uint32_t*>(sSel + 16 * KMAX), sScan);
+  };
+  if (tau0 >= tend) {  // no frames of this stream in the launch
+    if (kOut && out_hyps) output(P, S);
+    return;
+  }
 
   const size_t gb = static_cast<size_t>(b) * P.K;
   const int O = P.O;
@@ -1296,7 +1316,6 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
       }
       const HistNode par = S.arena[ph];
       HistNode hn;
-      hn.parent = ph;
       hn.word = st.w;
       hn.c2 = st.c2;
       hn.c3 = st.c3;
@@ -1305,12 +1324,12 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
       hn.bo3 = st.bo3;
       hn.depth = par.depth + 1;
       hn.sfus = synth ? par.sfus + bigram_score(P, par.word, st.w) : 0.0;
-      hn.w1 = par.word;
-      hn.w2 = par.w1;
-      hn.w3 = par.w2;
-      hn.up2 = par.parent;
-      hn.up3 = par.up2;
-      hn.up4 = par.up3;
+      // a parent that ends a block (the root included) starts a new one
+      const bool starts = par.depth % kHistBlock == 0;
+      hn.blk = starts ? ph : par.blk;
+      hn.w[0] = starts ? -1 : par.word;
+#pragma unroll
+      for (int i = 1; i < kHistBlock - 1; ++i) hn.w[i] = starts ? -1 : par.w[i - 1];
       const uint32_t node = arena0 + arena_n + static_cast<uint32_t>(e * O + k);
       S.arena[node] = hn;
       N.Lw[rr * kMaxSub + k] = L;
@@ -1731,17 +1750,22 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
     cn[kCntProbeLines] += sCnt[0];
     cn[kCntLookups] += c_lookups;
   }
+  if (kOut && out_hyps) {
+    __syncthreads();  // the beam is back in global memory
+    output(P, S);
+  }
 }
 
 // ------------------------------------------------------------------ delayed fusion
 
 // Selects the top-F hypotheses of stream b by (total desc, key asc) into
-// S.fsel[b][0..F) and S.fsel_n[b] (F = all hypotheses when top_f <= 0).
+// S.fsel[b][0..F) and S.fsel_n[b] (F = all hypotheses when top_f <= 0); the
+// sort covers BLOCK >= K entries (the workgroup may be larger).
 #undef P
 #undef S
 
 template <int BLOCK>
-__device__ void select_fused(const DevParams& P, const DevState& S, int b, int top_f, double* sc, uint64_t* ky,
+__device__ __forceinline__ void select_fused(const DevParams& P, const DevState& S, int b, int top_f, double* sc, uint64_t* ky,
                              uint32_t* ix) {
   const int tid = threadIdx.x;
   const int n = S.nbeam[b];
@@ -1752,7 +1776,7 @@ __device__ void select_fused(const DevParams& P, const DevState& S, int b, int t
       sc[tid] = S.pt[gb + tid] + S.Lw[(gb + tid) * P.O];
       ky[tid] = S.key[gb + tid];
       ix[tid] = tid;
-    } else {
+    } else if (tid < BLOCK) {
       sc[tid] = kNegInf;
       ky[tid] = ~0ull;
       ix[tid] = 0;
@@ -1788,7 +1812,7 @@ __device__ inline int32_t best_eos(const DevParams& P, int32_t word, double* sco
 // With `eos` (the final synthetic fusion) each sub-beam's fusion score also
 // takes its best end-of-sentence mark.
 template <int BLOCK>
-__device__ void apply_fused(const DevParams& P, const DevState& S, int b, const float* ext, bool eos = false) {
+__device__ __forceinline__ void apply_fused(const DevParams& P, const DevState& S, int b, const float* ext, bool eos = false) {
   const int tid = threadIdx.x;
   const size_t gb = static_cast<size_t>(b) * P.K;
   const int F = S.fsel_n[b];
@@ -1896,19 +1920,20 @@ __device__ inline void pad_rows(int32_t* rows, int nrows, int W, const int32_t* 
   }
 }
 
-// Writes the `depth` words of history h into row[0..min(depth, W)), four per
-// node read (the node's word and its window of three ancestors' words).
+// Writes the `depth` words of history h into row[0..min(depth, W)), one node
+// read per block of kHistBlock words (the node's word and the earlier words of
+// its block, then the node that ends the previous block).
 __device__ inline void trace_words(const DevState& S, uint32_t h, int depth, int32_t* row, int W) {
   int d = depth;
   while (d >= 1) {
     const HistNode x = S.arena[h];
+    const int nb = (d - 1) % kHistBlock;  // earlier words of the block
     if (d - 1 < W) row[d - 1] = x.word;
-    if (d >= 2 && d - 2 < W) row[d - 2] = x.w1;
-    if (d >= 3 && d - 3 < W) row[d - 3] = x.w2;
-    if (d >= 4 && d - 4 < W) row[d - 4] = x.w3;
-    if (d <= 4) break;
-    h = x.up4;
-    d -= 4;
+#pragma unroll
+    for (int i = 0; i < kHistBlock - 1; ++i)
+      if (i < nb && d - 2 - i < W) row[d - 2 - i] = x.w[i];
+    d -= nb + 1;
+    h = x.blk;
   }
 }
 
@@ -1952,20 +1977,20 @@ __global__ __launch_bounds__(BLOCK) void k_fuse_apply(const DevParams P, const D
 
 // ------------------------------------------------------------------ output
 
-template <int BLOCK>
-__global__ __launch_bounds__(BLOCK) void k_output(const DevParams P, const DevState S,
-                                                  const int32_t* __restrict__ lengths, int32_t fin,
-                                                  int32_t* __restrict__ out_hyps,
-                                                  float* __restrict__ out_scores) {
-  const int b = blockIdx.x;
+// One stream's output: at the end of an utterance the final synthetic fusion
+// over all hypotheses and the mid-word filter; then the hypotheses ranked by
+// (total desc, key asc), each one's words traced back from its best sub-beam,
+// rows padded with -1.  Run by a whole workgroup of NT threads; the sort covers
+// N >= K entries (N a power of two, N <= NT) in sc / ky / ix; sScan holds
+// NT / 64 entries.
+template <int NT, int N>
+__device__ __forceinline__ void emit_output(const DevParams& P, const DevState& S, int b, const int32_t* lengths, int32_t fin,
+                            int32_t* out_hyps, float* out_scores, double* sc, uint64_t* ky, uint32_t* ix,
+                            int32_t* sScan) {
   const int tid = threadIdx.x;
-  __shared__ double sc[BLOCK];
-  __shared__ uint64_t ky[BLOCK];
-  __shared__ uint32_t ix[BLOCK];
-  __shared__ int32_t sScan[BLOCK / 64];
   if (fin && P.fusion_source == 1 && P.fusion_interval > 0) {
-    select_fused<BLOCK>(P, S, b, 0, sc, ky, ix);
-    apply_fused<BLOCK>(P, S, b, nullptr, P.eos_count > 0);
+    select_fused<N>(P, S, b, 0, sc, ky, ix);
+    apply_fused<N>(P, S, b, nullptr, P.eos_count > 0);
   }
   const int n = S.nbeam[b];
   const size_t gb = static_cast<size_t>(b) * P.K;
@@ -1975,18 +2000,18 @@ __global__ __launch_bounds__(BLOCK) void k_output(const DevParams P, const DevSt
     sc[tid] = ok ? S.pt[gb + tid] + S.Lw[(gb + tid) * P.O] : kNegInf;
     ky[tid] = ok ? S.key[gb + tid] : ~0ull;
     ix[tid] = tid;
-  } else {
+  } else if (tid < N) {
     sc[tid] = kNegInf;
     ky[tid] = ~0ull;
     ix[tid] = 0;
   }
   int m = 0;
-  (void)block_scan<BLOCK>(ok ? 1 : 0, sScan, &m);
-  bitonic_sort<BLOCK>(sc, ky, ix);
+  (void)block_scan<NT>(ok ? 1 : 0, sScan, &m);
+  bitonic_sort<N>(sc, ky, ix);
   if (tid == 0) S.t0[b] += lengths[b];
   int32_t* const sLen = reinterpret_cast<int32_t*>(ky);  // words written per rank (the keys are read)
   __syncthreads();
-  for (int r = tid; r < P.K; r += BLOCK) {
+  for (int r = tid; r < P.K; r += NT) {
     int32_t* row = out_hyps + (static_cast<size_t>(b) * P.K + r) * P.W;
     int n = 0;
     if (r < m) {
@@ -2011,7 +2036,21 @@ __global__ __launch_bounds__(BLOCK) void k_output(const DevParams P, const DevSt
     sLen[r] = n < P.W ? n : P.W;
   }
   __syncthreads();
-  pad_rows<BLOCK>(out_hyps + static_cast<size_t>(b) * P.K * P.W, P.K, P.W, sLen);
+  pad_rows<NT>(out_hyps + static_cast<size_t>(b) * P.K * P.W, P.K, P.W, sLen);
+}
+
+// The output as a launch of its own (when the call's last decode launch did
+// not write it).
+template <int BLOCK>
+__global__ __launch_bounds__(BLOCK) void k_output(const DevParams P, const DevState S,
+                                                  const int32_t* __restrict__ lengths, int32_t fin,
+                                                  int32_t* __restrict__ out_hyps,
+                                                  float* __restrict__ out_scores) {
+  __shared__ double sc[BLOCK];
+  __shared__ uint64_t ky[BLOCK];
+  __shared__ uint32_t ix[BLOCK];
+  __shared__ int32_t sScan[BLOCK / 64];
+  emit_output<BLOCK, BLOCK>(P, S, blockIdx.x, lengths, fin, out_hyps, out_scores, sc, ky, ix, sScan);
 }
 
 }  // namespace
@@ -2079,8 +2118,8 @@ int cu_count() {
 }
 
 hipError_t launch_decode(int K, const KArgs* args, const DevParams& P, const DevState& S, const float* logits,
-                         const int32_t* lengths, int32_t B, int32_t Tc, int32_t tau0, int32_t tau1,
-                         hipStream_t st) {
+                         const int32_t* lengths, int32_t B, int32_t Tc, int32_t tau0, int32_t tau1, int32_t fin,
+                         int32_t* out_hyps, float* out_scores, bool* wrote_output, hipStream_t st) {
   const KArgs LB_CONST* A = (const KArgs LB_CONST*)args;
   // One workgroup per stream.  A batch that leaves CUs to spare gets more
   // lanes per hypothesis (up to 512 threads per stream, LPB <= 16); a batch
@@ -2091,36 +2130,34 @@ hipError_t launch_decode(int K, const KArgs* args, const DevParams& P, const Dev
   // LDS waits coarser).
   const int cus = cu_count();
   const bool spare = B <= cus;
+  // (an instance writes the output iff it reads its arguments from constant memory)
+#define LB_DECODE(KM, LP, WP, DBUF, CARGS, THREADS)                                                            \
+  do {                                                                                                        \
+    *wrote_output = (CARGS) && out_hyps != nullptr;                                                           \
+    LB_LAUNCH((k_decode<KM, LP, WP, DBUF, CARGS>), dim3(B), dim3(THREADS), st, A, P, S, logits, lengths, Tc, tau0, \
+              tau1, fin, out_hyps, out_scores);                                                               \
+  } while (0)
   if (K <= 16 && spare)
-    LB_LAUNCH((k_decode<16, 16, 1, true, true>), dim3(B), dim3(256), st, A, P, S, logits, lengths, Tc,
-              tau0, tau1);
+    LB_DECODE(16, 16, 1, true, true, 256);
   else if (K <= 16)
-    LB_LAUNCH((k_decode<16, 4, 1, true, true>), dim3(B), dim3(64), st, A, P, S, logits, lengths, Tc,
-              tau0, tau1);
+    LB_DECODE(16, 4, 1, true, true, 64);
   else if (K <= 32 && spare)
-    LB_LAUNCH((k_decode<32, 16, 1, true, true>), dim3(B), dim3(512), st, A, P, S, logits, lengths, Tc,
-              tau0, tau1);
+    LB_DECODE(32, 16, 1, true, true, 512);
   else if (K <= 32)
-    LB_LAUNCH((k_decode<32, 4, 1, true, true>), dim3(B), dim3(128), st, A, P, S, logits, lengths, Tc,
-              tau0, tau1);
+    LB_DECODE(32, 4, 1, true, true, 128);
   else if (K <= 64 && spare)
-    LB_LAUNCH((k_decode<64, 8, 1, true, true>), dim3(B), dim3(512), st, A, P, S, logits, lengths, Tc,
-              tau0, tau1);
+    LB_DECODE(64, 8, 1, true, true, 512);
   else if (K <= 64 && B > 3 * cus)
-    LB_LAUNCH((k_decode<64, 4, 4, true, true>), dim3(B), dim3(256), st, A, P, S, logits, lengths, Tc,
-              tau0, tau1);
+    LB_DECODE(64, 4, 4, true, true, 256);
   else if (K <= 64)
-    LB_LAUNCH((k_decode<64, 4, 1, true, true>), dim3(B), dim3(256), st, A, P, S, logits, lengths, Tc,
-              tau0, tau1);
+    LB_DECODE(64, 4, 1, true, true, 256);
   else if (K <= 128)
-    LB_LAUNCH((k_decode<128, 4, 1, true, true>), dim3(B), dim3(512), st, A, P, S, logits, lengths, Tc,
-              tau0, tau1);
+    LB_DECODE(128, 4, 1, true, true, 512);
   else if (spare)
-    LB_LAUNCH((k_decode<256, 2, 1, true, true>), dim3(B), dim3(512), st, A, P, S, logits, lengths, Tc,
-              tau0, tau1);
+    LB_DECODE(256, 2, 1, true, true, 512);
   else
-    LB_LAUNCH((k_decode<256, 2, 4, false, false>), dim3(B), dim3(512), st, A, P, S, logits, lengths, Tc,
-              tau0, tau1);
+    LB_DECODE(256, 2, 4, false, false, 512);
+#undef LB_DECODE
   return hipGetLastError();
 }
 
