@@ -1895,20 +1895,30 @@ __global__ __launch_bounds__(BLOCK) void k_fuse_select(const DevParams P, const 
 // nothing is to be scored).
 // Writes -1 past each row's words: rows [nrows][W] with len[r] words in row r;
 // the whole block on consecutive addresses, 16 B per store when W allows.
+typedef int v4i __attribute__((ext_vector_type(4)));
 template <int BLOCK>
 __device__ inline void pad_rows(int32_t* rows, int nrows, int W, const int32_t* len) {
-  if ((W & 3) == 0 && (reinterpret_cast<uintptr_t>(rows) & 15) == 0) {
+  if ((W & 3) == 0 && (reinterpret_cast<uintptr_t>(rows) & 15) == 0 && W > 0) {
+    // thread t writes the 16-B column t % per of rows t / per, t / per + rstep,
+    // ... (per = min(W / 4, BLOCK) columns of a row per pass, rstep rows)
     const int W4 = W >> 2;
-    for (int r = 0; r < nrows; ++r) {
-      int4* row = reinterpret_cast<int4*>(rows + static_cast<size_t>(r) * W);
-      const int n = len[r];
-      for (int c = threadIdx.x; c < W4; c += BLOCK) {
-        const int c0 = 4 * c;
-        if (c0 >= n) {
-          row[c] = make_int4(-1, -1, -1, -1);
-        } else if (c0 + 3 >= n) {
-          int32_t* e = rows + static_cast<size_t>(r) * W + c0;
-          for (int q = n - c0; q < 4; ++q) e[q] = -1;
+    const int per = W4 < BLOCK ? W4 : BLOCK;  // columns per pass of a row
+    const int rstep = BLOCK / per;            // rows per pass
+    const int tid = threadIdx.x;
+    if (tid < rstep * per) {
+      for (int r = tid / per; r < nrows; r += rstep) {
+        int4* row = reinterpret_cast<int4*>(rows + static_cast<size_t>(r) * W);
+        const int n = len[r];
+        for (int c = tid % per; c < W4; c += per) {
+          const int c0 = 4 * c;
+          if (c0 >= n) {
+            // streamed past the caches: the rows are read by the caller, not here
+            const v4i m1 = {-1, -1, -1, -1};
+            __builtin_nontemporal_store(m1, reinterpret_cast<v4i*>(row + c));
+          } else if (c0 + 3 >= n) {
+            int32_t* e = rows + static_cast<size_t>(r) * W + c0;
+            for (int q = n - c0; q < 4; ++q) e[q] = -1;
+          }
         }
       }
     }
