@@ -677,11 +677,10 @@ lb_status lb_decode_batch(lb_decoder* d, const float* logits, const int32_t* len
   // follows it in this call (no fusion round trip), else by k_output
   const int32_t fin = (flags & LB_END) ? 1 : 0;
   const bool out_here = start < stop && fuse_tau < 0 && !(external && fin && !X.final_done);
-  bool out_done = false;
   if (start < stop)
     LB_HIP(launch(kKindDecode, [&] {
-      return launch_decode(P.K, d->dargs, P, S, logits, lengths, batch, frames, start, stop, out_here ? fin : 0,
-                           out_here ? out_hyps : nullptr, out_here ? out_scores : nullptr, &out_done, st);
+      return launch_decode(P.K, d->dargs, logits, lengths, batch, frames, start, stop, out_here ? fin : 0,
+                           out_here ? out_hyps : nullptr, out_here ? out_scores : nullptr, st);
     }));
   if (fuse_tau >= 0) {
     for (int32_t b = 0; b < batch; ++b) {
@@ -705,7 +704,7 @@ lb_status lb_decode_batch(lb_decoder* d, const float* logits, const int32_t* len
     X.resume_tau = frames;
     return LB_NEED_FUSION;
   }
-  if (!out_done)
+  if (!out_here)
     LB_HIP(launch(kKindOutput, [&] { return launch_output(d->block, P, S, lengths, batch, fin, out_hyps, out_scores, st); }));
   if (external) {
     for (int32_t b = 0; b < batch; ++b) X.t0[b] += X.len[b];

@@ -550,29 +550,29 @@ __device__ __forceinline__ void emit_output(const DevParams& P, const DevState& 
 //     word with a large fully looked-up group) survive lambda pruning and
 //     receive word-history nodes;
 //   * Eq. (2) with the synthetic scorer on fusion frames.
-// WPE: wavefronts per SIMD the register allocation aims for (two workgroups of
-// 512 threads per CU need 4).  DB: the hypotheses are double-buffered in LDS;
-// otherwise one buffer is rewritten in place (every source entry is read before
-// any new entry is written), which lets two K = 256 workgroups share a CU.  CA: P and S are read from the device copy through a
-// constant-memory pointer (else from the by-value arguments).
-template <int KMAX, int LPB, int WPE, bool DB, bool CA>
+// WPE: wavefronts per SIMD the register allocation aims for (four workgroups
+// of 256 threads per CU need 4).  DB: the hypotheses are double-buffered in
+// LDS; otherwise one buffer is rewritten in place (every source entry is read
+// before any new entry is written), which lets two K = 256 workgroups share a
+// CU.  The decoder's parameters and state (P, S) are read from their device
+// copy A_ in constant memory.
+template <int KMAX, int LPB, int WPE, bool DB>
 __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE))) void k_decode(
-    const KArgs LB_CONST* A_, const DevParams Pv, const DevState Sv, const float* __restrict__ logits,
-    const int32_t* __restrict__ lengths, int32_t Tc, int32_t tau0, int32_t tau1, int32_t out_fin,
-    int32_t* __restrict__ out_hyps, float* __restrict__ out_scores) {
-  // With CA, P and S are read through a pointer that is made opaque in every
-  // frame, so that each field is loaded (scalar, from the constant cache)
-  // where it is used instead of staying live in scalar registers across the
-  // whole loop
+    const KArgs LB_CONST* A_, const float* __restrict__ logits, const int32_t* __restrict__ lengths, int32_t Tc,
+    int32_t tau0, int32_t tau1, int32_t out_fin, int32_t* __restrict__ out_hyps, float* __restrict__ out_scores) {
+  // P and S are read through a pointer that is made opaque in every frame, so
+  // that each field is loaded (scalar, from the constant cache) where it is
+  // used instead of staying live in scalar registers across the whole loop
   const KArgs LB_CONST* A = A_;
-#define P (CA ? *(const DevParams*)(&A->P) : Pv)
-#define S (CA ? *(const DevState*)(&A->S) : Sv)
+#define P (*(const DevParams*)(&A->P))
+#define S (*(const DevState*)(&A->S))
 
   constexpr int BLOCK = KMAX * LPB;
   constexpr int HS = 2 * KMAX;  // LDS hash slots for the current prefix keys
   constexpr int NW = BLOCK / 64;
   constexpr int NC = (kSep + LPB - 1) / LPB;  // extension slots per lane
   static_assert(LPB <= 16 && LPB * NC < 64, "a lane's slots stay below symbol 64");
+  static_assert(NC + 1 < 64, "a lane's candidates (its slots and the stay) fit the 64-bit sets sel_bits and bnd");
   constexpr int NPM = KMAX * kMaxSub;  // (completed word, sub-beam) pairs per frame, at most
   constexpr int NPL = NPM < 256 ? NPM : 256;  // pairs grouped at once
   constexpr int NEB = NPL / kMaxSub;          // completed words per batch
@@ -616,17 +616,14 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
   double* const sStL = reinterpret_cast<double*>(sSel + 8 * NPL);
   uint32_t* const sStH = reinterpret_cast<uint32_t*>(sStL + KMAX * kMaxSub);
   static_assert(DB || 8 * NPL + 12 * KMAX * kMaxSub <= UNI_BYTES, "write-back staging fits the shared scratch");
-  // the output (when this launch writes it) sorts in the shared scratch.  The
-  // instance with by-value arguments never writes it: the output pointers would
-  // stay live in scalar registers across the frame loop
-  constexpr bool kOut = CA;
+  // the output (when this launch writes it) sorts in the shared scratch
   auto output = [&](const DevParams& Pr, const DevState& Sr) {
     emit_output<BLOCK, KMAX>(Pr, Sr, b, lengths, out_fin, out_hyps, out_scores, reinterpret_cast<double*>(sSel),
                              reinterpret_cast<uint64_t*>(sSel + 8 * KMAX),
                              reinterpret_cast<uint32_t*>(sSel + 16 * KMAX), sScan);
   };
   if (tau0 >= tend) {  // no frames of this stream in the launch
-    if (kOut && out_hyps) output(P, S);
+    if (out_hyps) output(P, S);
     return;
   }
 
@@ -696,7 +693,7 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
     // live in registers across all frames)
     int tid = threadIdx.x;
     asm volatile("" : "+v"(tid));
-    if constexpr (CA) asm volatile("" : "+s"(A));
+    asm volatile("" : "+s"(A));
     const int lane = tid & 63;
     const int wave = tid >> 6;
     BeamLds<KMAX>& C = sBeam[DB ? cur : 0];        // the frame's hypotheses
@@ -918,13 +915,12 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
     // below it dropped; bnd marks this lane's candidates inside it (bit k: slot
     // k, bit NC: the stay)
     uint64_t sel_bits = 0;  // bit 0: the stay, bit k+1: slot k
-    uint32_t bnd = 0;
+    uint64_t bnd = 0;
+    // (branch-free: 0xFFFF, no candidate, is above every bin index; the two
+    // sets are updated separately so that they stay in registers)
     auto classify = [&](uint32_t bn, int bit, int bbit) {
-      if (bn == 0xFFFFu) return;
-      if (static_cast<int>(bn) < beta0)
-        sel_bits |= 1ull << bit;
-      else if (static_cast<int>(bn) == beta0)
-        bnd |= 1u << bbit;
+      sel_bits |= static_cast<uint64_t>(static_cast<int>(bn) < beta0) << bit;
+      bnd |= static_cast<uint64_t>(static_cast<int>(bn) == beta0) << bbit;
     };
     classify(bin_stay, 0, NC);
 #pragma unroll
@@ -933,8 +929,8 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
     // boundary bins of levels 1..L-1
     auto for_bnd = [&](int L, auto&& f) {
 #pragma unroll 1
-      for (uint32_t m = bnd; m; m &= m - 1) {
-        const int k = __ffs(m) - 1;
+      for (uint64_t m = bnd; m; m &= m - 1) {
+        const int k = __ffsll(static_cast<unsigned long long>(m)) - 1;
         const int v = k == NC ? 0 : 1 + ln + LPB * k;
         const double sc = k == NC ? c_stay : score_now(k);
         bool in = true;
@@ -997,8 +993,8 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
     // the boundary bin's candidates: the deeper levels, then the exact rank on
     // (score desc, key asc)
 #pragma unroll 1
-    for (uint32_t m = bnd; m; m &= m - 1) {
-      const int k = __ffs(m) - 1;
+    for (uint64_t m = bnd; m; m &= m - 1) {
+      const int k = __ffsll(static_cast<unsigned long long>(m)) - 1;
       const int v = k == NC ? 0 : 1 + ln + LPB * k;
       const double sc = k == NC ? c_stay : score_now(k);
       bool take = true;
@@ -1260,12 +1256,11 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
     }
     c_lookups += static_cast<uint64_t>(U);
     // the results go to LDS when they fit in the grouping keys freed above (the
-    // usual case), else to the stream's scratch in global memory (always in
-    // the two-per-CU K = 256 instance, where the LDS path costs registers)
+    // usual case), else to the stream's scratch in global memory
     constexpr int kLdsRes = 12 * NPL / 32;
     double* const sResL = reinterpret_cast<double*>(sSel);
     QState* const sResS = reinterpret_cast<QState*>(sSel + 8 * kLdsRes);
-    const bool res_lds = CA && U <= kLdsRes;
+    const bool res_lds = U <= kLdsRes;
     auto res_lp = [&](int u) -> double { return res_lds ? sResL[u] : scrL[u]; };
     auto res_st = [&](int u) -> QState { return res_lds ? sResS[u] : scrS[u]; };
     lds_barrier();
@@ -1750,7 +1745,7 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
     cn[kCntProbeLines] += sCnt[0];
     cn[kCntLookups] += c_lookups;
   }
-  if (kOut && out_hyps) {
+  if (out_hyps) {
     __syncthreads();  // the beam is back in global memory
     output(P, S);
   }
@@ -2127,46 +2122,42 @@ int cu_count() {
   return n;
 }
 
-hipError_t launch_decode(int K, const KArgs* args, const DevParams& P, const DevState& S, const float* logits,
-                         const int32_t* lengths, int32_t B, int32_t Tc, int32_t tau0, int32_t tau1, int32_t fin,
-                         int32_t* out_hyps, float* out_scores, bool* wrote_output, hipStream_t st) {
+hipError_t launch_decode(int K, const KArgs* args, const float* logits, const int32_t* lengths, int32_t B,
+                         int32_t Tc, int32_t tau0, int32_t tau1, int32_t fin, int32_t* out_hyps, float* out_scores,
+                         hipStream_t st) {
   const KArgs LB_CONST* A = (const KArgs LB_CONST*)args;
   // One workgroup per stream.  A batch that leaves CUs to spare gets more
   // lanes per hypothesis (up to 512 threads per stream, LPB <= 16); a batch
   // with more streams than one round of workgroups holds gets the instances
-  // that fit more workgroups per CU (fewer registers, at the price of some
-  // spilling): K = 64 with 4 per CU instead of 3, K = 256 with 2 per CU
-  // (one LDS buffer, by-value arguments: constant-memory loads there make the
-  // LDS waits coarser).
+  // that fit more workgroups per CU: K = 64 with 4 per CU instead of 3 (128
+  // registers, some spilling), K = 256 with 2 per CU (one in-place LDS beam
+  // buffer, one lane per hypothesis: 256 threads, so the registers need not
+  // be capped).
   const int cus = cu_count();
   const bool spare = B <= cus;
-  // (an instance writes the output iff it reads its arguments from constant memory)
-#define LB_DECODE(KM, LP, WP, DBUF, CARGS, THREADS)                                                            \
-  do {                                                                                                        \
-    *wrote_output = (CARGS) && out_hyps != nullptr;                                                           \
-    LB_LAUNCH((k_decode<KM, LP, WP, DBUF, CARGS>), dim3(B), dim3(THREADS), st, A, P, S, logits, lengths, Tc, tau0, \
-              tau1, fin, out_hyps, out_scores);                                                               \
-  } while (0)
+#define LB_DECODE(KM, LP, WP, DBUF, THREADS)                                                                  \
+  LB_LAUNCH((k_decode<KM, LP, WP, DBUF>), dim3(B), dim3(THREADS), st, A, logits, lengths, Tc, tau0, tau1, fin, \
+            out_hyps, out_scores)
   if (K <= 16 && spare)
-    LB_DECODE(16, 16, 1, true, true, 256);
+    LB_DECODE(16, 16, 1, true, 256);
   else if (K <= 16)
-    LB_DECODE(16, 4, 1, true, true, 64);
+    LB_DECODE(16, 4, 1, true, 64);
   else if (K <= 32 && spare)
-    LB_DECODE(32, 16, 1, true, true, 512);
+    LB_DECODE(32, 16, 1, true, 512);
   else if (K <= 32)
-    LB_DECODE(32, 4, 1, true, true, 128);
+    LB_DECODE(32, 4, 1, true, 128);
   else if (K <= 64 && spare)
-    LB_DECODE(64, 8, 1, true, true, 512);
+    LB_DECODE(64, 8, 1, true, 512);
   else if (K <= 64 && B > 3 * cus)
-    LB_DECODE(64, 4, 4, true, true, 256);
+    LB_DECODE(64, 4, 4, true, 256);
   else if (K <= 64)
-    LB_DECODE(64, 4, 1, true, true, 256);
+    LB_DECODE(64, 4, 1, true, 256);
   else if (K <= 128)
-    LB_DECODE(128, 4, 1, true, true, 512);
+    LB_DECODE(128, 4, 1, true, 512);
   else if (spare)
-    LB_DECODE(256, 2, 1, true, true, 512);
+    LB_DECODE(256, 2, 1, true, 512);
   else
-    LB_DECODE(256, 2, 4, false, false, 512);
+    LB_DECODE(256, 1, 2, false, 256);
 #undef LB_DECODE
   return hipGetLastError();
 }

@@ -15,13 +15,12 @@ hipError_t launch_build_order(int order, const int32_t* ids, const float* lp, co
                               int32_t vocab, NgramTable t2, NgramTable t3, NgramTable dst, uint32_t* flags,
                               uint32_t* ctx_out, hipStream_t st);
 hipError_t launch_begin(const DevParams& P, const DevState& S, int32_t B, hipStream_t st);
-// args: device copy of the decoder's parameters and state (the same as P and S).
-// out_hyps / out_scores non-null: the launch may also write the call's output
-// (fin: the end of an utterance), as launch_output would; *wrote_output says
-// whether it does (the kernel instance decides).
-hipError_t launch_decode(int K, const KArgs* args, const DevParams& P, const DevState& S, const float* logits,
-                         const int32_t* lengths, int32_t B, int32_t Tc, int32_t tau0, int32_t tau1, int32_t fin,
-                         int32_t* out_hyps, float* out_scores, bool* wrote_output, hipStream_t st);
+// args: device copy of the decoder's parameters and state.  out_hyps /
+// out_scores non-null: the launch also writes the call's output (fin: the end
+// of an utterance), as launch_output would.
+hipError_t launch_decode(int K, const KArgs* args, const float* logits, const int32_t* lengths, int32_t B,
+                         int32_t Tc, int32_t tau0, int32_t tau1, int32_t fin, int32_t* out_hyps, float* out_scores,
+                         hipStream_t st);
 hipError_t launch_fuse_select(int block, const DevParams& P, const DevState& S, const int32_t* flag, int32_t B,
                               hipStream_t st);
 hipError_t launch_fuse_export(int block, const DevParams& P, const DevState& S, int32_t* words, int32_t* n_words,
