@@ -872,9 +872,10 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
     // level-0 bin of each of the lane's candidates, kept packed 16 bits per slot
     // (0xFFFF: no candidate); exact scores are recomputed only inside the boundary bin
     uint32_t binp[(NC + 1) / 2];
-    // (the candidates' inputs are made opaque here so that their scores are
-    // recomputed below instead of being kept live across the block reduction)
-    asm volatile("" : "+v"(c_ab), "+v"(c_p), "+v"(c_L), "+v"(c_rel), "+v"(c_key));
+    // (with several lanes per hypothesis the candidates' inputs are made opaque
+    // here so that their scores are recomputed below instead of being kept live
+    // across the block reduction; the one-lane instance has the registers)
+    if constexpr (LPB > 1) asm volatile("" : "+v"(c_ab), "+v"(c_p), "+v"(c_L), "+v"(c_rel), "+v"(c_key));
     uint32_t bin_stay = 0xFFFFu;
     if (c_stay != kNegInf && c_stay >= thr) {
       bin_stay = static_cast<uint32_t>(bin0(0, c_stay));
