@@ -436,3 +436,41 @@ def test_end_of_sentence_marks(name):
     check_parity(d, out, range(B), name=f"{name}/eos", oracle_overrides=dict(eos_count=3, eos_ids=marks))
     ends = [ws[-1] for words, _ in out for ws in words if ws]
     assert ends and all(w in (d.lm.eos, d.lm.unk, 3) for w in ends)
+
+
+@pytest.mark.parametrize("finalize", [True, False], ids=["end", "live"])
+@pytest.mark.parametrize("name", ["t-c20k", "t-k256"])
+def test_output_in_decode_launch_equals_output_launch(name, finalize):
+    """The call's output is written by its decode launch when nothing follows
+    it, and by a launch of its own when the call has no frames: decoding all
+    frames and then ending with an empty call must give the bits of one call."""
+    import torch
+    d = load_workload(name)
+    B, T = d.logits.shape[:2]
+    say(f"[case] output paths {name} B={B} finalize={finalize}")
+    p = d.workload.params
+    flags_end = lbm.LB_END if finalize else 0
+    res = []
+    for split in (False, True):
+        lp = lbm.make_params(p, max_batch=B, max_frames=T, fusion_seed=d.fusion_seed)
+        dec = lbm.Decoder(d.lexicon, d.lm, lp)
+        dev = torch.device("cuda:0")
+        lg = torch.from_numpy(np.ascontiguousarray(d.logits)).to(dev)
+        ln = torch.from_numpy(d.lengths.astype(np.int32)).to(dev)
+        if split:
+            st, _, _ = dec.decode(lg, ln, lbm.LB_BEGIN)
+            assert st == lbm.LB_OK
+            empty = torch.empty((B, 0, lg.shape[2]), dtype=torch.float32, device=dev)
+            st, h, s = dec.decode(empty, torch.zeros(B, dtype=torch.int32, device=dev), flags_end)
+        else:
+            st, h, s = dec.decode(lg, ln, lbm.LB_BEGIN | flags_end)
+        assert st == lbm.LB_OK
+        torch.cuda.synchronize()
+        assert dec.status() == lbm.LB_OK, lbm.lb_last_error()
+        res.append((h.cpu().numpy(), s.cpu().numpy()))
+        dec.close()
+    (h1, s1), (h2, s2) = res
+    assert np.array_equal(h1, h2)
+    assert np.array_equal(s1, s2)
+    if not finalize:  # the whole beam is ranked
+        assert np.isfinite(s1[:, 0]).all()
