@@ -550,6 +550,9 @@ __device__ __forceinline__ void emit_output(const DevParams& P, const DevState& 
 //     word with a large fully looked-up group) survive lambda pruning and
 //     receive word-history nodes;
 //   * Eq. (2) with the synthetic scorer on fusion frames.
+// After the last frame the beam goes back to global memory, and, when out_hyps
+// is given, the workgroup also writes the stream's output (emit_output; out_fin:
+// the end of the utterance).
 // WPE: wavefronts per SIMD the register allocation aims for (four workgroups
 // of 256 threads per CU need 4).  DB: the hypotheses are double-buffered in
 // LDS; otherwise one buffer is rewritten in place (every source entry is read
