@@ -571,7 +571,10 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
 #define S (*(const DevState*)(&A->S))
 
   constexpr int BLOCK = KMAX * LPB;
-  constexpr int HS = 2 * KMAX;  // LDS hash slots for the current prefix keys
+  // LDS hash slots for the current prefix keys: a load of at most 1/4 keeps the
+  // linear probe chains short (at 1/2, a parent that is not in the beam took
+  // ~2.5 probes, and the whole frame 6 % longer)
+  constexpr int HS = 4 * KMAX;
   constexpr int NW = BLOCK / 64;
   constexpr int NC = (kSep + LPB - 1) / LPB;  // extension slots per lane
   static_assert(LPB <= 16 && LPB * NC < 64, "a lane's slots stay below symbol 64");
