@@ -557,9 +557,10 @@ __device__ __forceinline__ void emit_output(const DevParams& P, const DevState& 
 // of 256 threads per CU need 4).  DB: the hypotheses are double-buffered in
 // LDS; otherwise one buffer is rewritten in place (every source entry is read
 // before any new entry is written), which lets two K = 256 workgroups share a
-// CU.  The decoder's parameters and state (P, S) are read from their device
-// copy A_ in constant memory.
-template <int KMAX, int LPB, int WPE, bool DB>
+// CU.  HSF: LDS hash slots per hypothesis for the prefix keys (more slots,
+// shorter linear probe chains, more LDS).  The decoder's parameters and state
+// (P, S) are read from their device copy A_ in constant memory.
+template <int KMAX, int LPB, int WPE, bool DB, int HSF>
 __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE))) void k_decode(
     const KArgs LB_CONST* A_, const float* __restrict__ logits, const int32_t* __restrict__ lengths, int32_t Tc,
     int32_t tau0, int32_t tau1, int32_t out_fin, int32_t* __restrict__ out_hyps, float* __restrict__ out_scores) {
@@ -574,7 +575,8 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
   // LDS hash slots for the current prefix keys: a load of at most 1/4 keeps the
   // linear probe chains short (at 1/2, a parent that is not in the beam took
   // ~2.5 probes, and the whole frame 6 % longer)
-  constexpr int HS = 4 * KMAX;
+  constexpr int HS = HSF * KMAX;
+  static_assert(HSF >= 4 && (HSF & (HSF - 1)) == 0, "hash slots: a power of two, load at most 1/4");
   constexpr int NW = BLOCK / 64;
   constexpr int NC = (kSep + LPB - 1) / LPB;  // extension slots per lane
   static_assert(LPB <= 16 && LPB * NC < 64, "a lane's slots stay below symbol 64");
@@ -2142,29 +2144,32 @@ hipError_t launch_decode(int K, const KArgs* args, const float* logits, const in
   // be capped).
   const int cus = cu_count();
   const bool spare = B <= cus;
-#define LB_DECODE(KM, LP, WP, DBUF, THREADS)                                                                  \
-  LB_LAUNCH((k_decode<KM, LP, WP, DBUF>), dim3(B), dim3(THREADS), st, A, logits, lengths, Tc, tau0, tau1, fin, \
-            out_hyps, out_scores)
+  // (hash slots per hypothesis: 16 with one workgroup per CU and K <= 64, 8 at
+  // K = 256, where 16 would exceed the CU's LDS; 4 in the instances that share
+  // a CU, which keeps their LDS within their share)
+#define LB_DECODE(KM, LP, WP, DBUF, HSLOTS, THREADS)                                                         \
+  LB_LAUNCH((k_decode<KM, LP, WP, DBUF, HSLOTS>), dim3(B), dim3(THREADS), st, A, logits, lengths, Tc, tau0, tau1, \
+            fin, out_hyps, out_scores)
   if (K <= 16 && spare)
-    LB_DECODE(16, 16, 1, true, 256);
+    LB_DECODE(16, 16, 1, true, 16, 256);
   else if (K <= 16)
-    LB_DECODE(16, 4, 1, true, 64);
+    LB_DECODE(16, 4, 1, true, 4, 64);
   else if (K <= 32 && spare)
-    LB_DECODE(32, 16, 1, true, 512);
+    LB_DECODE(32, 16, 1, true, 16, 512);
   else if (K <= 32)
-    LB_DECODE(32, 4, 1, true, 128);
+    LB_DECODE(32, 4, 1, true, 4, 128);
   else if (K <= 64 && spare)
-    LB_DECODE(64, 8, 1, true, 512);
+    LB_DECODE(64, 8, 1, true, 16, 512);
   else if (K <= 64 && B > 3 * cus)
-    LB_DECODE(64, 4, 4, true, 256);
+    LB_DECODE(64, 4, 4, true, 4, 256);
   else if (K <= 64)
-    LB_DECODE(64, 4, 1, true, 256);
+    LB_DECODE(64, 4, 1, true, 4, 256);
   else if (K <= 128)
-    LB_DECODE(128, 4, 1, true, 512);
+    LB_DECODE(128, 4, 1, true, 4, 512);
   else if (spare)
-    LB_DECODE(256, 2, 1, true, 512);
+    LB_DECODE(256, 2, 1, true, 8, 512);
   else
-    LB_DECODE(256, 1, 2, false, 256);
+    LB_DECODE(256, 1, 2, false, 4, 256);
 #undef LB_DECODE
   return hipGetLastError();
 }
