@@ -2139,14 +2139,14 @@ hipError_t launch_decode(int K, const KArgs* args, const float* logits, const in
   // lanes per hypothesis (up to 512 threads per stream, LPB <= 16); a batch
   // with more streams than one round of workgroups holds gets the instances
   // that fit more workgroups per CU: K = 64 with 4 per CU instead of 3 (128
-  // registers, some spilling), K = 256 with 2 per CU (one in-place LDS beam
-  // buffer, one lane per hypothesis: 256 threads, so the registers need not
-  // be capped).
+  // registers, some spilling; one in-place LDS beam buffer), K = 256 with 2 per
+  // CU (one in-place LDS beam buffer, one lane per hypothesis: 256 threads, so
+  // the registers need not be capped).
   const int cus = cu_count();
   const bool spare = B <= cus;
   // (hash slots per hypothesis: 16 with one workgroup per CU and K <= 64, 8 at
-  // K = 256, where 16 would exceed the CU's LDS; 4 in the instances that share
-  // a CU, which keeps their LDS within their share)
+  // K = 256, where 16 would exceed the CU's LDS; in the instances that share a
+  // CU, 4, or 8 where the one in-place beam buffer leaves the LDS for it)
 #define LB_DECODE(KM, LP, WP, DBUF, HSLOTS, THREADS)                                                         \
   LB_LAUNCH((k_decode<KM, LP, WP, DBUF, HSLOTS>), dim3(B), dim3(THREADS), st, A, logits, lengths, Tc, tau0, tau1, \
             fin, out_hyps, out_scores)
@@ -2161,7 +2161,7 @@ hipError_t launch_decode(int K, const KArgs* args, const float* logits, const in
   else if (K <= 64 && spare)
     LB_DECODE(64, 8, 1, true, 16, 512);
   else if (K <= 64 && B > 3 * cus)
-    LB_DECODE(64, 4, 4, true, 4, 256);
+    LB_DECODE(64, 4, 4, false, 8, 256);
   else if (K <= 64)
     LB_DECODE(64, 4, 1, true, 4, 256);
   else if (K <= 128)
