@@ -783,6 +783,16 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
     }
     lds_barrier();
     hb ^= 1;
+    // Workgroups that share a CU: the CU's arbitration favours the older
+    // wavefronts, so the workgroup dispatched second (the later half of the
+    // grid, when workgroups are dispatched to the CUs in order) fell behind
+    // (c4: 9.8 against 11.1 ms on average) and the launch waited for it.  It
+    // gets the higher issue priority in 3 frames of 4, the first one in the
+    // 4th (c4: 12.3 -> 11.7 ms; alternating 1:1 gave 12.1).
+    if ((blockIdx.x >= gridDim.x / 2) ? (tau & 3) != 0 : (tau & 3) == 0)
+      __builtin_amdgcn_s_setprio(1);
+    else
+      __builtin_amdgcn_s_setprio(0);
 
     // ---- this lane's candidates: slot k is the extension by v = 1 + ln + LPB*k,
     // plus the merged stay on lane 0; scores are recomputed in every pass (same
