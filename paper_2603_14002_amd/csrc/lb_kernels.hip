@@ -577,6 +577,7 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
   // ~2.5 probes, and the whole frame 6 % longer)
   constexpr int HS = HSF * KMAX;
   static_assert(HSF >= 4 && (HSF & (HSF - 1)) == 0, "hash slots: a power of two, load at most 1/4");
+  static_assert(KMAX <= 256, "a hash slot holds its hypothesis in 8 bits");
   constexpr int NW = BLOCK / 64;
   constexpr int NC = (kSep + LPB - 1) / LPB;  // extension slots per lane
   static_assert(LPB <= 16 && LPB * NC < 64, "a lane's slots stay below symbol 64");
@@ -600,8 +601,13 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
   __shared__ double sAb2[KMAX], sAnb2[KMAX], sPt2[KMAX], sStay[KMAX];
   __shared__ uint64_t sMask[KMAX];
   // two tables: the one of this frame, and the next frame's, cleared meanwhile
-  __shared__ unsigned long long sHKey[2][HS];
-  __shared__ int32_t sHIdx[HS];
+  // two tables, the next frame's cleared during this one; or, in the one-buffer
+  // instances (whose LDS is scarcer), one table, cleared for the next frame once
+  // this frame's parent lookups are done (the frame's later barriers separate
+  // the clear from the next inserts)
+  constexpr int kHT = DB ? 2 : 1;
+  __shared__ unsigned long long sHKey[kHT][HS];
+  __shared__ uint8_t sHIdx[HS];  // the slot's hypothesis (KMAX <= 256)
   // top-K selection scratch; the LM step and the fusion sort reuse it
   __shared__ __align__(16) unsigned char sSel[UNI_BYTES];
   __shared__ double sLvHi[kMaxLevels], sLvInv[kMaxLevels];
@@ -669,7 +675,7 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
   if (tid < 3) sCnt[tid] = 0;
   uint32_t arena_n = S.arena_n[b];
   int cur = 0;  // the current buffer (DB)
-  int hb = 0;   // the current prefix-key table
+  int hb = 0;  // the current prefix-key table
   for (int q = tid; q < HS; q += BLOCK) sHKey[0][q] = kEmptyKey;
   uint32_t lines = 0, c_words = 0;  // per thread
   uint64_t c_queries = 0;
@@ -710,7 +716,8 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
     // the next frame's log-probs are loaded meanwhile
     if (tid < kClasses && tau + 1 < tend) dnext = logits[(static_cast<size_t>(b) * Tc + tau + 1) * kClasses + tid];
     unsigned long long* const hkey = sHKey[hb];
-    for (int s = tid; s < HS; s += BLOCK) sHKey[hb ^ 1][s] = kEmptyKey;
+    if constexpr (DB)
+      for (int s = tid; s < HS; s += BLOCK) sHKey[hb ^ 1][s] = kEmptyKey;
     for (int d = tid; d < kBins; d += BLOCK) sHisto[d] = 0;
     if (tid == 0) sBCount = 0;
 
@@ -726,7 +733,7 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
       for (;;) {
         const unsigned long long prev = atomicCAS(&hkey[s], kEmptyKey, my_key);
         if (prev == kEmptyKey) {
-          sHIdx[s] = tid;
+          sHIdx[s] = static_cast<uint8_t>(tid);
           break;
         }
         s = (s + 1) & (HS - 1);
@@ -746,7 +753,7 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
           const unsigned long long k = hkey[s];
           if (k == kEmptyKey) break;
           if (k == my_pkey) {
-            par = sHIdx[s];
+            par = static_cast<int>(sHIdx[s]);
             break;
           }
           s = (s + 1) & (HS - 1);
@@ -782,7 +789,10 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
       sStay[tid] = pt2 + C.Lw[tid * kMaxSub];
     }
     lds_barrier();
-    hb ^= 1;
+    if constexpr (DB)
+      hb ^= 1;
+    else
+      for (int s = tid; s < HS; s += BLOCK) sHKey[0][s] = kEmptyKey;  // for the next frame
     // Workgroups that share a CU: the CU's arbitration favours the older
     // wavefronts, so the workgroup dispatched second (the later half of the
     // grid, when workgroups are dispatched to the CUs in order) fell behind
@@ -2155,8 +2165,8 @@ hipError_t launch_decode(int K, const KArgs* args, const float* logits, const in
   const int cus = cu_count();
   const bool spare = B <= cus;
   // (hash slots per hypothesis: 16 with one workgroup per CU and K <= 64, 8 at
-  // K = 256, where 16 would exceed the CU's LDS; in the instances that share a
-  // CU, 4, or 8 where the one in-place beam buffer leaves the LDS for it)
+  // K = 256; where workgroups share a CU, 4 with two tables, 8 or 16 with one,
+  // as their LDS allows)
 #define LB_DECODE(KM, LP, WP, DBUF, HSLOTS, THREADS)                                                         \
   LB_LAUNCH((k_decode<KM, LP, WP, DBUF, HSLOTS>), dim3(B), dim3(THREADS), st, A, logits, lengths, Tc, tau0, tau1, \
             fin, out_hyps, out_scores)
@@ -2171,7 +2181,7 @@ hipError_t launch_decode(int K, const KArgs* args, const float* logits, const in
   else if (K <= 64 && spare)
     LB_DECODE(64, 8, 1, true, 16, 512);
   else if (K <= 64 && B > 3 * cus)
-    LB_DECODE(64, 4, 4, false, 8, 256);
+    LB_DECODE(64, 4, 4, false, 16, 256);
   else if (K <= 64)
     LB_DECODE(64, 4, 1, true, 4, 256);
   else if (K <= 128)
@@ -2179,7 +2189,7 @@ hipError_t launch_decode(int K, const KArgs* args, const float* logits, const in
   else if (spare)
     LB_DECODE(256, 2, 1, true, 8, 512);
   else
-    LB_DECODE(256, 1, 2, false, 4, 256);
+    LB_DECODE(256, 1, 2, false, 8, 256);
 #undef LB_DECODE
   return hipGetLastError();
 }
