@@ -75,12 +75,13 @@ def copy_calibration(mib: int) -> None:
 
 
 def kernel_source_hash() -> str:
-    """sha256 over the device sources with comments and blank space removed; a
-    traffic figure is valid only for the kernel code it was measured on."""
+    """sha256 over the device sources and the host code that lays out the
+    device tables, with comments and blank space removed; a traffic figure is
+    valid only for the code it was measured on."""
     import hashlib
     import re
     h = hashlib.sha256()
-    for f in ("lb_kernels.hip", "lb_device.h"):
+    for f in ("lb_kernels.hip", "lb_device.h", "lb_api.cpp"):
         with open(os.path.join(ROOT, "paper_2603_14002_amd", "csrc", f)) as fh:
             text = fh.read()
         text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)

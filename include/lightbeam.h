@@ -121,7 +121,7 @@ typedef struct lb_params {
   uint64_t fusion_seed;    /* synthetic scorer: Bg(a,b) = lo + (hi-lo) *         */
   double fusion_lo;        /*   (splitmix64(seed ^ (a<<32 | b)) >> 48) / 65536,   */
   double fusion_hi;        /*   S_fus(w1..wn) = sum_i Bg(w_{i-1}, w_i), w0 = <s>  */
-  double lm_load_factor;   /* n-gram hash-table load factor (0 = 0.5), <= 0.9     */
+  double lm_load_factor;   /* n-gram hash-table load factor (0 = 0.25), <= 0.9    */
   int64_t arena_nodes_per_stream; /* word-history capacity (0 = beam*subbeams*max_frames) */
   int32_t merge;           /* LB_MERGE_*                                          */
   int32_t input;           /* LB_INPUT_*                                          */

@@ -255,7 +255,7 @@ lb_status validate(const lb_lexicon_desc* lex, const lb_ngram_desc* lm, const lb
   for (int k = 0; k < p->eos_count; ++k)
     if (p->eos_ids[k] < 0 || p->eos_ids[k] >= lm->vocab_size)
       return fail(LB_ERR_INVALID_ARG, "eos_ids outside the LM vocabulary");
-  const double lf = p->lm_load_factor == 0.0 ? 0.5 : p->lm_load_factor;
+  const double lf = p->lm_load_factor == 0.0 ? 0.25 : p->lm_load_factor;
   if (!(lf > 0.0 && lf <= 0.9)) return fail(LB_ERR_INVALID_ARG, "lm_load_factor must be in (0, 0.9]");
   for (double x : {p->alpha, p->beta, p->gamma, p->omega, p->phi, p->theta, p->lambda, p->fusion_lo, p->fusion_hi})
     if (!std::isfinite(x)) return fail(LB_ERR_INVALID_ARG, "non-finite parameter");
@@ -513,7 +513,7 @@ lb_status lb_create(const lb_lexicon_desc* lex, const lb_ngram_desc* lm, const l
   if (!d) return fail(LB_ERR_OUT_OF_MEMORY, "host allocation failed");
   d->p = *params;
   const lb_params& p = d->p;
-  const double lf = p.lm_load_factor == 0.0 ? 0.5 : p.lm_load_factor;
+  const double lf = p.lm_load_factor == 0.0 ? 0.25 : p.lm_load_factor;
   const int K = p.beam, O = p.subbeams, B = p.max_batch;
   d->block = K <= 64 ? 64 : (K <= 128 ? 128 : 256);
   uint64_t cap = p.arena_nodes_per_stream > 0
