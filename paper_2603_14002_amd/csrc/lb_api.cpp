@@ -266,14 +266,14 @@ lb_status validate(const lb_lexicon_desc* lex, const lb_ngram_desc* lm, const lb
 
 // Explicit-continuation index of one order: entries (key = context id << 32 |
 // node word offset, homophone index) grouped by key into an open-addressing
-// table with the n-gram tables' bucket layout and probe order.
+// table with the n-gram tables' bucket layout, probe order and load factor.
 struct PresEntry {
   uint64_t key;
   uint32_t h;
   bool operator<(const PresEntry& o) const { return key != o.key ? key < o.key : h < o.h; }
 };
 
-lb_status upload_pres(lb_decoder* d, std::vector<PresEntry>& ent, PresTable* out) {
+lb_status upload_pres(lb_decoder* d, std::vector<PresEntry>& ent, double lf, PresTable* out) {
   lb_status st;
   std::sort(ent.begin(), ent.end());
   ent.erase(std::unique(ent.begin(), ent.end(),
@@ -281,7 +281,7 @@ lb_status upload_pres(lb_decoder* d, std::vector<PresEntry>& ent, PresTable* out
             ent.end());
   size_t nkeys = 0;
   for (size_t i = 0; i < ent.size(); ++i) nkeys += (i == 0 || ent[i].key != ent[i - 1].key) ? 1 : 0;
-  const uint64_t nb = buckets_for(static_cast<int64_t>(nkeys), 0.5);
+  const uint64_t nb = buckets_for(static_cast<int64_t>(nkeys), lf);
   std::vector<PresSlot> slots(nb * 4, PresSlot{kEmptyKey, 0, 0});
   std::vector<uint32_t> lists;
   for (size_t i = 0; i < ent.size();) {
@@ -452,7 +452,7 @@ lb_status build_tables(lb_decoder* d, const HostTrie& trie, const lb_ngram_desc*
   if (flags & kFlagBuildFull) return fail(LB_ERR_CAPACITY, "n-gram hash table full");
   PresTable* ptabs[3] = {&d->S.p2, &d->S.p3, &d->S.p4};
   for (int k = 0; k < 3; ++k) {
-    if ((st = upload_pres(d, pres[k], ptabs[k])) != LB_OK) return st;
+    if ((st = upload_pres(d, pres[k], lf, ptabs[k])) != LB_OK) return st;
     std::vector<PresEntry>().swap(pres[k]);
   }
 
