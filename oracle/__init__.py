@@ -75,7 +75,7 @@ def _load():
         lib.orc_last_error.restype = ctypes.c_char_p
         lib.orc_decode.restype = ctypes.c_int32
         lib.orc_decode.argtypes = [P, ctypes.POINTER(_Params), P, ctypes.c_int32, ctypes.c_int32,
-                                   ctypes.c_int32, ctypes.c_int32] + [P] * 10
+                                   ctypes.c_int32, ctypes.c_int32] + [P] * 10 + [ctypes.c_int32] + [P] * 4
         lib.orc_log10p.restype = ctypes.c_double
         lib.orc_log10p.argtypes = [P, P, ctypes.c_int32, ctypes.c_int32]
         lib.orc_fusion_score.restype = ctypes.c_double
@@ -102,6 +102,7 @@ class OracleResult:
     margins: dict               # min decision margins
     frame_lse: Optional[np.ndarray]
     stats: dict
+    subs: Optional[List[List[tuple]]] = None  # per hypothesis: [(Lw, words), ...] best first
 
     @property
     def min_margin(self) -> float:
@@ -169,7 +170,9 @@ class Oracle:
 
     def decode(self, logits: np.ndarray, params: _Params, max_hyps: int = 4096,
                max_words: int = 512, max_labels: int = 2048,
-               frame_lse: bool = False) -> OracleResult:
+               frame_lse: bool = False, max_subs: int = 0) -> OracleResult:
+        """Decodes one utterance.  With max_subs > 0 the result also lists up to
+        max_subs sub-beams (word-level score, words) of every hypothesis."""
         lg = np.ascontiguousarray(logits, dtype=np.float32)
         T = int(lg.shape[0])
         assert lg.ndim == 2 and lg.shape[1] == 41
@@ -183,10 +186,15 @@ class Oracle:
         margins = np.empty(6, np.float64)
         flse = np.empty(max(T, 1), np.float64) if frame_lse else None
         stats = np.empty(4, np.int64)
+        S = max(0, int(max_subs))
+        nsub = np.zeros(max_hyps, np.int32) if S else None
+        subL = np.empty((max_hyps, S), np.float64) if S else None
+        subnw = np.empty((max_hyps, S), np.int32) if S else None
+        subw = np.empty((max_hyps, S, max_words), np.int32) if S else None
         n = self.lib.orc_decode(self._h, ctypes.byref(params), _ptr(lg), T, max_hyps, max_words,
                                 max_labels, _ptr(words), _ptr(nwords), _ptr(tot), _ptr(ac),
                                 _ptr(labels), _ptr(nlabels), _ptr(keys), _ptr(margins),
-                                _ptr(flse), _ptr(stats))
+                                _ptr(flse), _ptr(stats), S, _ptr(nsub), _ptr(subL), _ptr(subnw), _ptr(subw))
         if n < 0:
             raise RuntimeError("oracle decode failed: " + self.lib.orc_last_error().decode())
         m = min(n, max_hyps)
@@ -198,7 +206,9 @@ class Oracle:
             margins=dict(zip(MARGIN_NAMES, margins.tolist())),
             frame_lse=None if flse is None else flse[:T].copy(),
             stats=dict(expansions=int(stats[0]), word_events=int(stats[1]),
-                       lm_queries=int(stats[2]), fused=int(stats[3])))
+                       lm_queries=int(stats[2]), fused=int(stats[3])),
+            subs=None if not S else [[(float(subL[i, j]), [int(x) for x in subw[i, j, :min(subnw[i, j], max_words)]])
+                                      for j in range(nsub[i])] for i in range(m)])
 
     def log10p(self, ctx, w: int) -> float:
         c = np.ascontiguousarray(list(ctx) or [0], dtype=np.int32)

@@ -624,11 +624,15 @@ static Params to_params(const orc_params* q) {
 //   out_margins [6]: min decision margins (top-K, theta, top-o, lambda, top-F, ranking)
 //   out_frame_lse [T] (optional): log-sum-exp of the beam's acoustic scores after each frame
 //   out_stats [4]: expansions, word events, LM queries, fused entries
+//   (optional, with max_subs > 0) every sub-beam of each hypothesis, best first:
+//   out_nsub [max_hyps], out_sub_L [max_hyps][max_subs] word-level scores,
+//   out_sub_nw [max_hyps][max_subs] and out_sub_words [max_hyps][max_subs][max_words]
 int32_t orc_decode(void* h, const orc_params* q, const float* logits, int32_t T, int32_t max_hyps,
                    int32_t max_words, int32_t max_labels, int32_t* out_words, int32_t* out_nwords,
                    double* out_total, double* out_acoustic, int32_t* out_labels,
                    int32_t* out_nlabels, uint64_t* out_keys, double* out_margins,
-                   double* out_frame_lse, int64_t* out_stats) {
+                   double* out_frame_lse, int64_t* out_stats, int32_t max_subs, int32_t* out_nsub,
+                   double* out_sub_L, int32_t* out_sub_nw, int32_t* out_sub_words) {
   if (!h || !q || !logits || T < 0 || q->beam < 1 || q->subbeams < 1 || q->fusion_mode < 0 ||
       q->fusion_mode > 2 || (q->fusion_mode == 2 && !q->scorer)) {
     g_err = "invalid argument";
@@ -653,6 +657,19 @@ int32_t orc_decode(void* h, const orc_params* q, const float* logits, int32_t T,
       for (int32_t k = 0; k < max_labels; ++k)
         out_labels[static_cast<int64_t>(i) * max_labels + k] = k < static_cast<int32_t>(x.y.size()) ? x.y[k] : -1;
     if (out_keys) out_keys[i] = prefix_key(x.y);
+    if (max_subs > 0 && out_nsub) {
+      const int32_t ns = std::min<int32_t>(max_subs, static_cast<int32_t>(x.subs.size()));
+      out_nsub[i] = ns;
+      for (int32_t j = 0; j < ns; ++j) {
+        const Sub& sb = x.subs[j];
+        const int64_t r = static_cast<int64_t>(i) * max_subs + j;
+        if (out_sub_L) out_sub_L[r] = sb.Lw;
+        if (out_sub_nw) out_sub_nw[r] = static_cast<int32_t>(sb.words.size());
+        if (out_sub_words)
+          for (int32_t k = 0; k < max_words; ++k)
+            out_sub_words[r * max_words + k] = k < static_cast<int32_t>(sb.words.size()) ? sb.words[k] : -1;
+      }
+    }
   }
   if (out_margins) {
     const double m[6] = {o.mg.topk, o.mg.theta, o.mg.homophone, o.mg.lam, o.mg.fusion, o.mg.ranking};
