@@ -75,19 +75,11 @@ def copy_calibration(mib: int) -> None:
 
 
 def kernel_source_hash() -> str:
-    """sha256 over the device sources and the host code that lays out the
-    device tables, with comments and blank space removed; a traffic figure is
-    valid only for the code it was measured on."""
-    import hashlib
-    import re
-    h = hashlib.sha256()
-    for f in ("lb_kernels.hip", "lb_device.h", "lb_api.cpp"):
-        with open(os.path.join(ROOT, "paper_2603_14002_amd", "csrc", f)) as fh:
-            text = fh.read()
-        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
-        text = re.sub(r"//[^\n]*", " ", text)
-        h.update(" ".join(text.split()).encode())
-    return h.hexdigest()
+    """The library's build id for the sources in this tree (sha256 over the
+    sources without comments and spacing, and the build flags); a committed
+    traffic or parity figure is valid only for the code it was measured on."""
+    from paper_2603_14002_amd.build import source_hash
+    return source_hash()
 
 
 def measured_traffic(workload: str):
@@ -114,15 +106,16 @@ def measured_traffic(workload: str):
 
 def algorithmic_bytes(s, B, T, p, lp):
     """Bytes the method itself moves in the counted work (all launches of the
-    pass): the logits once, a 16-B trie node per 41 expansions, the beam state
-    read and written once per call, the probed 64-B bucket lines (n-gram and
-    continuation-index tables), per lookup the unigram entry (8 B) and the word
-    id (4 B) (the queries of a stream-frame that share context and word are
-    looked up once; homophones that back off to their unigram are not looked
-    up), per completed word and sub-beam the context's 64-B history node
-    read and a 64-B history node written (at most o per completed word), and,
-    when the decode launch also writes the call's output (no separate output
-    launch), the output rows: B x K x (W word ids + a score), 4 B each."""
+    pass), per unit of work: a 164-B logit row per stream-frame, a 16-B trie
+    node per 41 expansions, the beam state read and written once per call
+    (it stays in LDS between frames), a 64-B line per probed hash-table bucket
+    (n-gram tables and continuation index) and per lookup the 64-B line of the
+    word's unigram entry (the queries of a stream-frame that share context
+    and word are looked up once; homophones that back off to their unigram are
+    not looked up), an 8-B history-node reference per completed word and
+    sub-beam, 8 B per fused sub-beam, and, when the decode launch also writes
+    the call's output (no separate output launch), the output rows: B x K x
+    (W word ids + a score), 4 B each."""
     state = 48 + 12 * p.subbeams          # key, pkey, a_b, a_nb, total, node, meta + o x (L, hist)
     calls = max(1, int(s.launches[0]))
     parts = {
@@ -130,8 +123,9 @@ def algorithmic_bytes(s, B, T, p, lp):
         "trie": float(s.expansions) * 16.0 / 41.0,
         "state": 2.0 * calls * B * p.beam * state,
         "ngram_lines": float(s.probe_lines) * LINE_BYTES,
-        "ngram_other": float(s.lm_lookups) * (8 + 4),
-        "history_nodes": float(s.word_events) * p.subbeams * 128.0,
+        "unigram_lines": float(s.lm_lookups) * LINE_BYTES,
+        "history_nodes": float(s.word_events) * p.subbeams * 8.0,
+        "fusion": float(s.fused) * p.subbeams * 8.0,
     }
     import paper_2603_14002_amd as lbm
     if int(s.launches[lbm.KIND_OUTPUT]) == 0:
@@ -140,14 +134,63 @@ def algorithmic_bytes(s, B, T, p, lp):
     return parts
 
 
+def copy_bandwidth(mib: int = 1024, reps: int = 5) -> float:
+    """GB/s (bytes read + written) of a plain device copy of `mib` MiB, best of `reps`."""
+    import torch
+    n = mib * (1 << 20) // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    best = float("inf")
+    for _ in range(reps):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        dst.copy_(src)
+        e1.record()
+        torch.cuda.synchronize()
+        best = min(best, e0.elapsed_time(e1))
+    del src, dst
+    torch.cuda.empty_cache()
+    return 2.0 * n * 4 / (best * 1e-3) / 1e9
+
+
+def committed_parity(workload: str):
+    """Parity counts of the full-batch GPU tests for this workload from the
+    committed summary, while the library sources hash to the ones they were
+    measured on (else None)."""
+    path = os.path.join(ROOT, "profiles", f"parity_{workload}.md")
+    if not os.path.exists(path):
+        return None
+    out, sha = {}, None
+    with open(path) as fh:
+        for line in fh:
+            if line.startswith("- kernel_source_sha256: "):
+                sha = line.split(": ", 1)[1].strip().strip("`")
+            if line.startswith("{") and '"mode"' in line:
+                r = json.loads(line)
+                out[r["mode"]] = {k: r[k] for k in ("utterances", "exact", "near_tie", "near_tie_excused",
+                                                    "tie_divergent", "mismatch", "empty", "hyps_compared")}
+    if sha != kernel_source_hash() or not out:
+        return None
+    return out
+
+
 def cpu_baseline(d, n_utts: int, threads: int):
     """The oracle, as it stands, on the first n_utts utterances (full length), one
-    utterance per host thread; returns expansions/s and the sample description."""
+    utterance per host thread; returns expansions/s and the sample description,
+    and the first utterance decoded alone on one core."""
     import oracle
     t0 = time.time()
     orc = oracle.Oracle(d.lexicon, d.lm)
     log(f"oracle loaded in {time.time() - t0:.1f}s")
     op = oracle.params_from(d.workload.params, fusion_seed=d.fusion_seed)
+    L0 = int(d.lengths[0])
+    t0 = time.time()
+    r0 = orc.decode(d.logits[0, :L0], op, max_hyps=d.workload.params.beam)
+    one = time.time() - t0
+    single = dict(seconds_per_utterance=one, expansions_per_s=r0.stats["expansions"] / one,
+                  rtf=one / (L0 * 0.08), sample=f"utterance 0 ({L0} frames) alone on one thread")
     exps = [0] * n_utts
     frames = [0] * n_utts
     nxt = [0]
@@ -176,7 +219,8 @@ def cpu_baseline(d, n_utts: int, threads: int):
     return dict(value=sum(exps) / wall, unit="beam-token expansions/s", cores=threads, kind="oracle",
                 sample=f"first {n_utts} utterances of {d.workload.name} (all frames), "
                        f"one per thread on {threads} threads, {wall:.1f}s wall",
-                audio_sec_per_wall_sec=sum(frames) * 0.08 / wall)
+                host_cpu_count=os.cpu_count(), audio_sec_per_wall_sec=sum(frames) * 0.08 / wall,
+                single_core=single)
 
 
 def main():
@@ -276,6 +320,7 @@ def main():
     value = exp_per_step / (ms / 1000.0)
     roof = None
     kern = {}
+    out_phase, roof_lookup = None, None
     if not args.no_profile:
         # (2) the same K steps with every kernel timed by events carried in its
         # own dispatch: k_decode's duration for the roofline, and the breakdown
@@ -297,6 +342,35 @@ def main():
                            "a second pass of the same steps",
                     wall_ms_per_step_in_that_pass=wall_p / args.steps)
         roof["frac"] = roof["achieved"] / HBM_PEAK_GBS
+        roof["copy_GBps"] = copy_bandwidth()
+        roof["frac_of_copy"] = roof["achieved"] / roof["copy_GBps"]
+        # (3) the same K steps with the decode kernel's phase counters on: each
+        # phase's share of the workgroups' cycles, and the n-gram lookup phase
+        # against the HBM roofline (its bytes over its share of the launch)
+        _, sph = timed_pass(lbm.LB_PROFILE_PHASES)
+        cyc = [float(x) for x in sph.phase_cycles]
+        tot = sum(cyc)
+        if tot > 0:
+            share = {n: c / tot for n, c in zip(lbm.PHASE_NAMES, cyc)}
+            nl3 = max(1, int(sph.launches[i]))
+            look_bytes = ((sph.probe_lines - sph.index_lines) * LINE_BYTES + sph.lm_lookups * LINE_BYTES) / nl3
+            look_s = share["ngram_lookup"] * avg_us * 1e-6
+            ach = look_bytes / look_s / 1e9 if look_s > 0 else None
+            out_phase = dict(share=share, cycles_per_stream_frame={n: c / max(1, sph.frames) for n, c in
+                                                                   zip(lbm.PHASE_NAMES, cyc)})
+            roof_lookup = dict(
+                kernel="k_decode n-gram lookup phase", bound="hbm", achieved=ach, peak=HBM_PEAK_GBS, unit="GB/s",
+                frac=None if ach is None else ach / HBM_PEAK_GBS,
+                frac_of_copy=None if ach is None else ach / roof["copy_GBps"],
+                traffic=None, bytes_per_launch=look_bytes,
+                lines_per_launch=(sph.probe_lines - sph.index_lines) / nl3,
+                lookups_per_launch=sph.lm_lookups / nl3,
+                phase_seconds_per_launch=look_s,
+                timing="the phase's share of the workgroups' clock cycles (s_memtime at its barriers) x the "
+                       "event-timed k_decode launch duration; bytes: a 64-B line per probed bucket of the "
+                       "n-gram tables and per lookup the unigram entry's line")
+        else:
+            out_phase, roof_lookup = None, None
     out = {
         "metric": METRIC,
         "value": value,
@@ -323,6 +397,9 @@ def main():
                      "probe_lines_per_step": s.probe_lines / args.steps},
         "kernels": kern,
         "roofline": roof,
+        "roofline_lookup_phase": roof_lookup,
+        "phases": out_phase,
+        "parity": committed_parity(wl.name),
     }
     if external:
         n = args.steps

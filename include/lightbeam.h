@@ -159,6 +159,16 @@ typedef struct lb_stats {
                            apply, [5] stream reset, [6..7] unused                */
   double  kernel_ms[8]; /* summed event-timed durations (when profiling is on)    */
   int64_t timed[8];     /* launches included in kernel_ms                         */
+  int64_t index_lines;  /* the part of probe_lines read from the explicit-
+                           continuation index                                     */
+  int64_t phase_cycles[8]; /* with LB_PROFILE_PHASES: clock cycles of the decode
+                           launches' workgroups, summed over streams, by phase:
+                           [0] recombination and stay scores, [1] top-K and theta,
+                           [2] new beam, [3] grouping of the n-gram queries and
+                           the continuation index, [4] n-gram lookups, [5]
+                           ranking of the completed words (top-o, lambda) and
+                           history nodes, [6] fusion and the rest of the frame,
+                           [7] beam load / write-back / output                  */
 } lb_stats;
 
 /* Builds a decoder: the lexicon trie (CSR) and the n-gram hash tables are
@@ -176,10 +186,13 @@ void lb_destroy(lb_decoder* dec);
  * per frame).
  *   logits      device float32 [batch][frames][41], log-softmax per frame
  *   lengths     device int32 [batch]: frames of this call valid for each stream
- *               (0..frames; the rest of the stream's rows are ignored)
+ *               (0..frames; the rest of the stream's rows are ignored; a value
+ *               outside 0..frames is clamped and reported by lb_get_status)
  *   flags       LB_BEGIN resets streams 0..batch-1 to the empty hypothesis;
  *               LB_END finalises them after the call's frames (final fusion over
- *               every hypothesis, hypotheses inside a word dropped)
+ *               every hypothesis; hypotheses inside a word are dropped when some
+ *               hypothesis ends at a word boundary, else all are ranked by
+ *               their completed words)
  *   out_hyps    device int32 [batch][beam][max_words_out]: word ids of the best
  *               sub-beam of each ranked hypothesis, -1 padded
  *   out_scores  device float32 [batch][beam]: total scores, -inf padded
@@ -213,9 +226,12 @@ lb_status lb_fusion_request(lb_decoder* dec, int32_t* words, int32_t* n_words, v
  * sub-beams are re-ranked.  LB_ERR_STATE if no fusion is pending. */
 lb_status lb_fusion_scores(lb_decoder* dec, const float* fusion_logprobs, void* stream);
 
-/* Synchronises `stream` and reports device-side overflow flags: LB_ERR_CAPACITY
- * if a word-history arena, an output buffer (words beyond max_words_out) or the
- * top-K selection's boundary buffer overflowed since lb_create. */
+/* Synchronises `stream` and reports device-side flags raised since lb_create:
+ * LB_ERR_CAPACITY if a word-history arena, an output buffer (words beyond
+ * max_words_out) or the top-K selection's boundary buffer overflowed (the
+ * writes past them were skipped), LB_ERR_INVALID_ARG if a decode call was
+ * given a length outside 0..frames (that stream was decoded, and its frame
+ * counter advanced, as if the length were clamped to that range). */
 lb_status lb_get_status(lb_decoder* dec, void* stream);
 
 /* Reads the counters (synchronises the device).  With profiling on (see
@@ -227,12 +243,19 @@ lb_status lb_reset_stats(lb_decoder* dec);
  * kind k (the index of lb_stats.launches); 0 disables timing and
  * LB_PROFILE_ALL times every launch.  The start / stop events are carried by
  * the kernel's own dispatch (hipExtLaunchKernel), so they time its execution
- * only. */
-enum { LB_PROFILE_ALL = 0xFFu };
+ * only.  LB_PROFILE_PHASES makes the decode kernel count the clock cycles of
+ * each phase of its frames (lb_stats.phase_cycles). */
+enum { LB_PROFILE_ALL = 0xFFu, LB_PROFILE_PHASES = 0x100u };
 lb_status lb_set_profiling(lb_decoder* dec, uint32_t kernel_mask);
 
 /* Thread-local description of the last error ("" if none). */
 const char* lb_last_error(void);
+
+/* Identity of the build: a hex sha256 over the library's source files
+ * (comments and spacing removed) and its compile flags, fixed at build time,
+ * so that a caller can check that the library in hand was built from the
+ * sources it expects ("unknown" if the build did not define it). */
+const char* lb_build_id(void);
 
 #ifdef __cplusplus
 }

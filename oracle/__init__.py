@@ -27,7 +27,11 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "oracle.cpp")
 _LIB = os.path.join(_HERE, "liboracle.so")
 
-MARGIN_NAMES = ("topk", "theta", "homophone", "lambda", "fusion", "ranking")
+# minimum decision margins over the decode (the K-th vs (K+1)-th candidate at
+# top-K, the distance to the theta cut, the o-th vs (o+1)-th homophone
+# candidate, the distance to the lambda cut, the F-th vs (F+1)-th fused
+# hypothesis, adjacent output ranks), and the last frame's top-K margin
+MARGIN_NAMES = ("topk", "theta", "homophone", "lambda", "fusion", "ranking", "last_topk")
 
 
 def build(force: bool = True) -> str:
@@ -106,7 +110,8 @@ class OracleResult:
 
     @property
     def min_margin(self) -> float:
-        return float(min(self.margins.values()))
+        """Smallest margin of any decision taken during the decode."""
+        return float(min(v for k, v in self.margins.items() if k != "last_topk"))
 
 
 def params_from(p, fusion_seed: int = 0, fusion_mode: int = 0, scorer=None, **overrides) -> _Params:
@@ -183,7 +188,7 @@ class Oracle:
         labels = np.empty((max_hyps, max_labels), np.int32)
         nlabels = np.empty(max_hyps, np.int32)
         keys = np.empty(max_hyps, np.uint64)
-        margins = np.empty(6, np.float64)
+        margins = np.empty(7, np.float64)
         flse = np.empty(max(T, 1), np.float64) if frame_lse else None
         stats = np.empty(4, np.int64)
         S = max(0, int(max_subs))

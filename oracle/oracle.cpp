@@ -27,7 +27,8 @@
 //  * Delayed fusion after frame t when t % I == 0 and t > 0 replaces every
 //    sub-beam score of the top-F entries by phi * S_fus(words), then re-sorts
 //    the sub-beams (stable); at the end a final fusion covers all entries,
-//    entries inside a word are dropped and the rest are ranked.
+//    entries inside a word are dropped if any entry ends at a word boundary
+//    (else all are kept, with their completed words) and the rest are ranked.
 //  * Ties are broken by a 64-bit key of the prefix (splitmix64 chain), and
 //    sub-beam ties by (parent sub-beam index, word id).
 //  * Options: recombination by max instead of log-sum-exp (the best alignment,
@@ -233,6 +234,7 @@ bool valid_extension(const Lexicon& lex, const std::vector<int>& P, int v) {
 
 struct Margins {
   double topk = kInf, theta = kInf, homophone = kInf, lam = kInf, fusion = kInf, ranking = kInf;
+  double last_topk = kInf;  // the K-th vs (K+1)-th candidate of the last frame
 };
 
 struct Stats {
@@ -456,6 +458,7 @@ Output decode(const Model& M, const Params& p, const float* logits, int T, bool 
     });
     size_t keep = std::min<size_t>(p.beam, ms.size());
     if (ms.size() > keep) out.mg.topk = std::min(out.mg.topk, ms[keep - 1].total - ms[keep].total);
+    out.mg.last_topk = ms.size() > keep ? ms[keep - 1].total - ms[keep].total : kInf;
     const double cut = ms.empty() ? kNegInf : ms[0].total - p.theta;
 
     std::vector<Hyp> next;
@@ -493,13 +496,17 @@ Output decode(const Model& M, const Params& p, const float* logits, int T, bool 
     }
   }
 
-  // End of the utterance: final fusion over every entry, drop entries that
-  // stop inside a word, rank the rest.  Without finalisation the live beam is
-  // ranked as it stands (the state a streaming decoder reports mid-stream).
+  // End of the utterance: final fusion over every entry; entries that stop
+  // inside a word are dropped when at least one entry ends at a word boundary
+  // (otherwise every entry is kept, with its completed words); the rest are
+  // ranked.  Without finalisation the live beam is ranked as it stands (the
+  // state a streaming decoder reports mid-stream).
   if (p.finalize && p.fusion_interval > 0) apply_fusion(M, p, beam, 0, out.mg, out.st, true);
+  bool any_complete = false;
+  for (const Hyp& h : beam) any_complete = any_complete || partial_word(h.y).empty();
   std::vector<Hyp> done;
   for (Hyp& h : beam)
-    if (!p.finalize || partial_word(h.y).empty()) done.push_back(std::move(h));
+    if (!p.finalize || !any_complete || partial_word(h.y).empty()) done.push_back(std::move(h));
   std::vector<Ranked> r = rank(done);
   for (size_t i = 0; i + 1 < r.size(); ++i)
     out.mg.ranking = std::min(out.mg.ranking, r[i].total - r[i + 1].total);
@@ -621,7 +628,8 @@ static Params to_params(const orc_params* q) {
 //   out_total, out_acoustic: total score and its acoustic part (fp64)
 //   out_labels [max_hyps][max_labels] / out_nlabels: collapsed symbol sequence
 //   out_keys: 64-bit prefix key of each hypothesis
-//   out_margins [6]: min decision margins (top-K, theta, top-o, lambda, top-F, ranking)
+//   out_margins [7]: min decision margins (top-K, theta, top-o, lambda, top-F, ranking)
+//                    and the last frame's top-K margin
 //   out_frame_lse [T] (optional): log-sum-exp of the beam's acoustic scores after each frame
 //   out_stats [4]: expansions, word events, LM queries, fused entries
 //   (optional, with max_subs > 0) every sub-beam of each hypothesis, best first:
@@ -672,7 +680,8 @@ int32_t orc_decode(void* h, const orc_params* q, const float* logits, int32_t T,
     }
   }
   if (out_margins) {
-    const double m[6] = {o.mg.topk, o.mg.theta, o.mg.homophone, o.mg.lam, o.mg.fusion, o.mg.ranking};
+    const double m[7] = {o.mg.topk, o.mg.theta, o.mg.homophone, o.mg.lam, o.mg.fusion, o.mg.ranking,
+                         o.mg.last_topk};
     std::memcpy(out_margins, m, sizeof(m));
   }
   if (out_frame_lse)

@@ -29,7 +29,8 @@ STATUS_NAMES = {0: "LB_OK", 1: "LB_ERR_INVALID_ARG", 2: "LB_ERR_STATE", 3: "LB_E
                 4: "LB_ERR_OUT_OF_MEMORY", 5: "LB_ERR_HIP", 6: "LB_NEED_FUSION"}
 
 EXPORTED = ("lb_create", "lb_destroy", "lb_decode_batch", "lb_fusion_request", "lb_fusion_scores",
-            "lb_get_status", "lb_get_stats", "lb_reset_stats", "lb_set_profiling", "lb_last_error")
+            "lb_get_status", "lb_get_stats", "lb_reset_stats", "lb_set_profiling", "lb_last_error",
+            "lb_build_id")
 
 
 class LBError(RuntimeError):
@@ -71,19 +72,29 @@ class lb_stats(ctypes.Structure):
                 ("lm_queries", ctypes.c_int64), ("fused", ctypes.c_int64), ("frames", ctypes.c_int64),
                 ("probe_lines", ctypes.c_int64), ("lm_lookups", ctypes.c_int64),
                 ("launches", ctypes.c_int64 * 8), ("kernel_ms", ctypes.c_double * 8),
-                ("timed", ctypes.c_int64 * 8)]
+                ("timed", ctypes.c_int64 * 8), ("index_lines", ctypes.c_int64),
+                ("phase_cycles", ctypes.c_int64 * 8)]
 
 
 _lib = None
 
 
 def lib():
-    """The loaded liblightbeam.so (raises if it has not been built)."""
+    """The loaded liblightbeam.so.  Raises if it has not been built, or if its
+    build id differs from the hash of the sources in this tree (a library built
+    from other sources is never used)."""
     global _lib
     if _lib is None:
         if not os.path.exists(LIB_PATH):
             raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2603_14002_amd.build`")
+        from .build import source_hash
         L = ctypes.CDLL(LIB_PATH)
+        L.lb_build_id.restype = ctypes.c_char_p
+        L.lb_build_id.argtypes = []
+        have, want = L.lb_build_id().decode(), source_hash()
+        if have != want:
+            raise ImportError(f"{LIB_PATH} was built from other sources (build id {have[:16]}, sources "
+                              f"{want[:16]}): rebuild it with `python -m paper_2603_14002_amd.build`")
         P = ctypes.c_void_p
         L.lb_create.restype = ctypes.c_int32
         L.lb_create.argtypes = [ctypes.POINTER(lb_lexicon_desc), ctypes.POINTER(lb_ngram_desc),
@@ -112,6 +123,10 @@ def lib():
 
 def lb_last_error() -> str:
     return lib().lb_last_error().decode()
+
+
+def lb_build_id() -> str:
+    return lib().lb_build_id().decode()
 
 
 def _check(st: int, allow=(LB_OK,)) -> int:
@@ -189,7 +204,9 @@ KIND_DECODE, KIND_OUTPUT, KIND_FUSE_SELECT, KIND_FUSE_EXPORT, KIND_FUSE_APPLY, K
 KIND_NAMES = ("decode", "output", "fuse_select", "fuse_export", "fuse_apply", "begin")
 LB_MERGE_LOGSUMEXP, LB_MERGE_MAX = 0, 1
 LB_INPUT_LOGPROBS, LB_INPUT_LOGITS = 0, 1
-LB_PROFILE_ALL = 0xFF
+LB_PROFILE_ALL, LB_PROFILE_PHASES = 0xFF, 0x100
+PHASE_NAMES = ("recombination", "top_k", "new_beam", "ngram_group", "ngram_lookup", "ngram_rank", "fusion_rest",
+               "load_writeback_output")
 
 
 def lb_set_profiling(dec: int, kernel_mask: int) -> None:

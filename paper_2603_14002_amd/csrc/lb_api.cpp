@@ -19,7 +19,7 @@ using namespace lb;
 static_assert(sizeof(lb_params) == 160, "lb_params layout");
 static_assert(sizeof(lb_ngram_desc) == 144, "lb_ngram_desc layout");
 static_assert(sizeof(lb_lexicon_desc) == 32, "lb_lexicon_desc layout");
-static_assert(sizeof(lb_stats) == 248, "lb_stats layout");
+static_assert(sizeof(lb_stats) == 320, "lb_stats layout");
 
 namespace {
 
@@ -143,7 +143,7 @@ struct lb_decoder {
   int block = 64;       // workgroup size of the fusion / output kernels (>= beam)
   std::vector<void*> allocs;
   int64_t launches[kKinds] = {};
-  uint32_t profile_mask = 0;  // kernel kinds timed with HIP events (bit k = kind k)
+  uint32_t profile_mask = 0;  // kernel kinds timed with HIP events (bit k = kind k), LB_PROFILE_PHASES
   std::vector<EventPair> pending;
   std::vector<hipEvent_t> pool;
   double kernel_ms[kKinds] = {};
@@ -192,6 +192,8 @@ struct lb_decoder {
       if (hipEventElapsedTime(&ms, ep.a, ep.b) == hipSuccess) {
         kernel_ms[ep.kind] += ms;
         timed[ep.kind] += 1;
+      } else {
+        (void)hipGetLastError();  // an unusable pair is skipped; leave no error behind for the caller
       }
       pool.push_back(ep.a);
       pool.push_back(ep.b);
@@ -502,6 +504,11 @@ extern "C" {
 
 const char* lb_last_error(void) { return g_err.c_str(); }
 
+#ifndef LB_BUILD_ID
+#define LB_BUILD_ID "unknown"
+#endif
+const char* lb_build_id(void) { return LB_BUILD_ID; }
+
 lb_status lb_create(const lb_lexicon_desc* lex, const lb_ngram_desc* lm, const lb_params* params,
                     lb_decoder** out) {
   g_err.clear();
@@ -680,7 +687,8 @@ lb_status lb_decode_batch(lb_decoder* d, const float* logits, const int32_t* len
   if (start < stop)
     LB_HIP(launch(kKindDecode, [&] {
       return launch_decode(P.K, d->dargs, logits, lengths, batch, frames, start, stop, out_here ? fin : 0,
-                           out_here ? out_hyps : nullptr, out_here ? out_scores : nullptr, st);
+                           out_here ? out_hyps : nullptr, out_here ? out_scores : nullptr,
+                           (d->profile_mask & LB_PROFILE_PHASES) ? kOptPhaseTimers : 0u, st);
     }));
   if (fuse_tau >= 0) {
     for (int32_t b = 0; b < batch; ++b) {
@@ -705,7 +713,7 @@ lb_status lb_decode_batch(lb_decoder* d, const float* logits, const int32_t* len
     return LB_NEED_FUSION;
   }
   if (!out_here)
-    LB_HIP(launch(kKindOutput, [&] { return launch_output(d->block, P, S, lengths, batch, fin, out_hyps, out_scores, st); }));
+    LB_HIP(launch(kKindOutput, [&] { return launch_output(d->block, P, S, lengths, batch, frames, fin, out_hyps, out_scores, st); }));
   if (external) {
     for (int32_t b = 0; b < batch; ++b) X.t0[b] += X.len[b];
     X.in_call = false;
@@ -751,6 +759,8 @@ lb_status lb_get_status(lb_decoder* d, void* stream) {
   if (flags & kFlagArena) return fail(LB_ERR_CAPACITY, "word-history arena overflow (raise arena_nodes_per_stream)");
   if (flags & kFlagWords) return fail(LB_ERR_CAPACITY, "hypothesis longer than max_words_out (output truncated)");
   if (flags & kFlagSelect) return fail(LB_ERR_CAPACITY, "internal top-K selection overflow");
+  if (flags & kFlagLength)
+    return fail(LB_ERR_INVALID_ARG, "a decode call's lengths were outside 0..frames (decoded and counted as clamped)");
   return LB_OK;
 }
 
@@ -769,6 +779,8 @@ lb_status lb_get_stats(lb_decoder* d, lb_stats* out) {
     out->frames += static_cast<int64_t>(x[kCntFrames]);
     out->probe_lines += static_cast<int64_t>(x[kCntProbeLines]);
     out->lm_lookups += static_cast<int64_t>(x[kCntLookups]);
+    out->index_lines += static_cast<int64_t>(x[kCntPresLines]);
+    for (int k = 0; k < kPhases; ++k) out->phase_cycles[k] += static_cast<int64_t>(x[kCntPhase0 + k]);
   }
   d->harvest();
   for (int k = 0; k < kKinds; ++k) {

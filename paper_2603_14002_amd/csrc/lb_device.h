@@ -55,10 +55,21 @@ constexpr uint32_t kFlagBuildRange = 8u;
 constexpr uint32_t kFlagBuildContext = 16u;
 constexpr uint32_t kFlagBuildDup = 32u;
 constexpr uint32_t kFlagBuildFull = 64u;
+constexpr uint32_t kFlagLength = 128u;  // a decode call's length outside 0..frames (clamped)
+
+// phases of a decode frame timed by the phase counters: recombination and stay
+// scores, top-K selection, new beam, grouping of the n-gram queries (with the
+// continuation index), the n-gram lookups, ranking of the completed words and
+// history nodes, the rest of the frame (fusion, trie-node store, next row);
+// kPhOther: beam load, write-back and output outside the frame loop
+enum { kPhRecomb = 0, kPhTopK = 1, kPhNewBeam = 2, kPhGroup = 3, kPhLookup = 4, kPhRank = 5, kPhFusion = 6,
+       kPhOther = 7, kPhases = 8 };
+constexpr uint32_t kOptPhaseTimers = 1u;  // k_decode option: per-phase clock cycles
 
 // per-stream counters (DevState::counters, [max_batch][kNumCounters])
 enum { kCntExpansions = 0, kCntWordEvents = 1, kCntLmQueries = 2, kCntFused = 3, kCntFrames = 4,
-       kCntProbeLines = 5, kCntLookups = 6, kNumCounters = 7 };
+       kCntProbeLines = 5, kCntLookups = 6, kCntPresLines = 7, kCntPhase0 = 8,
+       kNumCounters = kCntPhase0 + kPhases };
 
 struct TrieNode {
   uint64_t mask;

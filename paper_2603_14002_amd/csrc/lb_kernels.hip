@@ -528,9 +528,9 @@ struct BeamLds {
 };
 
 template <int NT, int N>
-__device__ __forceinline__ void emit_output(const DevParams& P, const DevState& S, int b, const int32_t* lengths, int32_t fin,
-                            int32_t* out_hyps, float* out_scores, double* sc, uint64_t* ky, uint32_t* ix,
-                            int32_t* sScan);
+__device__ __forceinline__ void emit_output(const DevParams& P, const DevState& S, int b, const int32_t* lengths,
+                                            int32_t Tc, int32_t fin, int32_t* out_hyps, float* out_scores, double* sc,
+                                            uint64_t* ky, uint32_t* ix, int32_t* sScan);
 
 // Frames [tau0, min(tau1, length)) of Alg. 1 for every stream: one workgroup
 // per stream, which keeps the stream's beam in LDS from frame to frame.  Each
@@ -559,11 +559,14 @@ __device__ __forceinline__ void emit_output(const DevParams& P, const DevState& 
 // before any new entry is written), which lets two K = 256 workgroups share a
 // CU.  HSF: LDS hash slots per hypothesis for the prefix keys (more slots,
 // shorter linear probe chains, more LDS).  The decoder's parameters and state
-// (P, S) are read from their device copy A_ in constant memory.
+// (P, S) are read from their device copy A_ in constant memory.  opts bit 0
+// (kOptPhaseTimers): thread 0 adds the clock cycles of each phase of the
+// frame to the stream's phase counters (kCntPhase0 + kPh*).
 template <int KMAX, int LPB, int WPE, bool DB, int HSF>
 __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE))) void k_decode(
     const KArgs LB_CONST* A_, const float* __restrict__ logits, const int32_t* __restrict__ lengths, int32_t Tc,
-    int32_t tau0, int32_t tau1, int32_t out_fin, int32_t* __restrict__ out_hyps, float* __restrict__ out_scores) {
+    int32_t tau0, int32_t tau1, int32_t out_fin, int32_t* __restrict__ out_hyps, float* __restrict__ out_scores,
+    uint32_t opts) {
   // P and S are read through a pointer that is made opaque in every frame, so
   // that each field is loaded (scalar, from the constant cache) where it is
   // used instead of staying live in scalar registers across the whole loop
@@ -620,7 +623,18 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
   __shared__ double sRed[2 * NW], sRedB[2 * NW];
   __shared__ int32_t sScan[NW], sScanB[NW], sScanC[NW], sScanD[NW];
   __shared__ int32_t sBucket, sAbove, sBucketCnt, sBCount;
-  __shared__ unsigned long long sCnt[3];  // probed lines, completed words, LM queries
+  __shared__ unsigned long long sCnt[4];  // probed lines, completed words, LM queries, index lines
+  // phase cycles of thread 0 (kPh*), and the last timestamp
+  __shared__ unsigned long long sPhase[kPhases + 1];
+  const bool timing = (opts & kOptPhaseTimers) != 0;
+  // closes the current phase as phase k (taken after the barrier that ends it)
+  auto mark = [&](int k) {
+    if (timing && threadIdx.x == 0) {
+      const unsigned long long now = __builtin_amdgcn_s_memtime();
+      sPhase[k] += now - sPhase[kPhases];
+      sPhase[kPhases] = now;
+    }
+  };
 
   uint32_t* const sHisto = reinterpret_cast<uint32_t*>(sSel);
   double* const sBScore = reinterpret_cast<double*>(sSel + kBins * 4);
@@ -632,7 +646,7 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
   static_assert(DB || 8 * NPL + 12 * KMAX * kMaxSub <= UNI_BYTES, "write-back staging fits the shared scratch");
   // the output (when this launch writes it) sorts in the shared scratch
   auto output = [&](const DevParams& Pr, const DevState& Sr) {
-    emit_output<BLOCK, KMAX>(Pr, Sr, b, lengths, out_fin, out_hyps, out_scores, reinterpret_cast<double*>(sSel),
+    emit_output<BLOCK, KMAX>(Pr, Sr, b, lengths, Tc, out_fin, out_hyps, out_scores, reinterpret_cast<double*>(sSel),
                              reinterpret_cast<uint64_t*>(sSel + 8 * KMAX),
                              reinterpret_cast<uint32_t*>(sSel + 16 * KMAX), sScan);
   };
@@ -672,12 +686,16 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
     B0.first[tid] = tn.first_child;
     B0.woff[tid] = tn.word_off;
   }
-  if (tid < 3) sCnt[tid] = 0;
+  if (tid < 4) sCnt[tid] = 0;
+  if (timing && tid == 0) {
+    for (int k = 0; k < kPhases; ++k) sPhase[k] = 0;
+    sPhase[kPhases] = __builtin_amdgcn_s_memtime();
+  }
   uint32_t arena_n = S.arena_n[b];
   int cur = 0;  // the current buffer (DB)
   int hb = 0;  // the current prefix-key table
   for (int q = tid; q < HS; q += BLOCK) sHKey[0][q] = kEmptyKey;
-  uint32_t lines = 0, c_words = 0;  // per thread
+  uint32_t lines = 0, plines = 0, c_words = 0;  // per thread
   uint64_t c_queries = 0;
   uint64_t c_exp = 0, c_fused = 0, c_lookups = 0;  // uniform
   double* const scrL = S.scrL + static_cast<size_t>(b) * S.scap;
@@ -700,6 +718,7 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
     set_row(P, lane < kClasses ? logits[(static_cast<size_t>(b) * Tc + tau0) * kClasses + lane] : 0.0f);
   float dnext = 0.0f;
   lds_barrier();
+  mark(kPhOther);
 
   for (int tau = tau0; tau < tend; ++tau) {
     // the thread index is made opaque to the optimizer in every frame so that
@@ -789,6 +808,7 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
       sStay[tid] = pt2 + C.Lw[tid * kMaxSub];
     }
     lds_barrier();
+    mark(kPhRecomb);
     if constexpr (DB)
       hb ^= 1;
     else
@@ -1056,6 +1076,7 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
       sSelSrc[wpos++] = static_cast<uint32_t>(hi_) | (v << 16);
     }
     lds_barrier();
+    mark(kPhTopK);
 
     // ---- the new hypotheses; an extension's trie node is fetched now and
     // stored after the LM step.  (The n-gram grouping table is cleared here:
@@ -1161,6 +1182,7 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
       sEvWoff[erank] = ev_woff;
       sEvH[erank] = ev_H;
     }
+    mark(kPhNewBeam);
 
     // ---- Eq. (1).  The queries (sub-beam j, homophone h) of the completed
     // words are scored once per distinct group (n-gram context, completed-word
@@ -1236,7 +1258,7 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
       uint32_t cnt = Hg;
       if (Hg >= P.heavy_min) {
         PresHit hit[3];
-        pres_lookup(S, sGctx[g], sGwoff[g], hit, &lines);
+        pres_lookup(S, sGctx[g], sGwoff[g], hit, &plines);
         const uint32_t ne = hit[0].n + hit[1].n + hit[2].n;
         if (ne <= static_cast<uint32_t>(kMaxExplicit)) {
           uint32_t* E = scrE + static_cast<size_t>(g) * kMaxExplicit;
@@ -1293,6 +1315,7 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
     auto res_lp = [&](int u) -> double { return res_lds ? sResL[u] : scrL[u]; };
     auto res_st = [&](int u) -> QState { return res_lds ? sResS[u] : scrS[u]; };
     lds_barrier();
+    mark(kPhGroup);
     for (int u = tid; u < U; u += BLOCK) {
       int lo = 0, hi = NG - 1;
       while (lo < hi) {
@@ -1315,6 +1338,7 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
       lds_barrier();
     else
       __syncthreads();  // the lookup results (global memory) are read by other threads
+    mark(kPhLookup);
     // each completed word: its top-o by (score desc, j*H + h asc), lambda
     // pruning, word-history nodes (o reserved per word, in order).  A
     // candidate's source: its lookup result in the scratch (>= 0), or, for a
@@ -1656,11 +1680,18 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
       if (lane < kept && room) write_node(e, lane, myL, ph, mys);
       if (lane == 0) close_event(e, kept, nsub);
     }
+    mark(kPhRank);
     }
-    arena_n += static_cast<uint32_t>(nev * O);
+    {
+      // nodes reserved this frame; past the capacity the count stays at cap + 1
+      // (every later word event then sees no room and raises the flag)
+      const uint64_t an = static_cast<uint64_t>(arena_n) + static_cast<uint64_t>(nev * O);
+      arena_n = static_cast<uint32_t>(an <= S.arena_cap ? an : S.arena_cap + 1);
+    }
     c_exp += static_cast<uint64_t>(n) * kClasses;
     n = nsel;
     __syncthreads();  // history nodes (global memory) are read by the fusion and the next frame
+    mark(kPhRank);
     if (tn_load) {
       N.tmask[r] = tn.mask;
       N.first[r] = tn.first_child;
@@ -1727,6 +1758,7 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
       c_fused += static_cast<uint64_t>(F);
     }
     lds_barrier();
+    mark(kPhFusion);
     if constexpr (DB) cur ^= 1;
   }
 
@@ -1753,6 +1785,7 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) {
     lines += __shfl_xor(lines, o, 64);
+    plines += __shfl_xor(plines, o, 64);
     c_words += __shfl_xor(c_words, o, 64);
     c_queries += __shfl_xor(c_queries, o, 64);
   }
@@ -1760,6 +1793,7 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
     atomicAdd(&sCnt[0], static_cast<unsigned long long>(lines));
     atomicAdd(&sCnt[1], static_cast<unsigned long long>(c_words));
     atomicAdd(&sCnt[2], static_cast<unsigned long long>(c_queries));
+    atomicAdd(&sCnt[3], static_cast<unsigned long long>(plines));
   }
   __syncthreads();
   if (tid == 0) {
@@ -1771,12 +1805,21 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
     cn[kCntWordEvents] += sCnt[1];
     cn[kCntLmQueries] += sCnt[2];
     cn[kCntFused] += c_fused;
-    cn[kCntProbeLines] += sCnt[0];
+    cn[kCntProbeLines] += sCnt[0] + sCnt[3];
+    cn[kCntPresLines] += sCnt[3];
     cn[kCntLookups] += c_lookups;
   }
   if (out_hyps) {
     __syncthreads();  // the beam is back in global memory
     output(P, S);
+  }
+  if (timing) {
+    __syncthreads();
+    mark(kPhOther);
+    if (tid == 0) {
+      unsigned long long* cn = S.counters + static_cast<size_t>(b) * kNumCounters;
+      for (int k = 0; k < kPhases; ++k) cn[kCntPhase0 + k] += sPhase[k];
+    }
   }
 }
 
@@ -2012,15 +2055,16 @@ __global__ __launch_bounds__(BLOCK) void k_fuse_apply(const DevParams P, const D
 // ------------------------------------------------------------------ output
 
 // One stream's output: at the end of an utterance the final synthetic fusion
-// over all hypotheses and the mid-word filter; then the hypotheses ranked by
+// over all hypotheses and the mid-word filter (when some hypothesis ends at a
+// word boundary); then the hypotheses ranked by
 // (total desc, key asc), each one's words traced back from its best sub-beam,
 // rows padded with -1.  Run by a whole workgroup of NT threads; the sort covers
 // N >= K entries (N a power of two, N <= NT) in sc / ky / ix; sScan holds
 // NT / 64 entries.
 template <int NT, int N>
-__device__ __forceinline__ void emit_output(const DevParams& P, const DevState& S, int b, const int32_t* lengths, int32_t fin,
-                            int32_t* out_hyps, float* out_scores, double* sc, uint64_t* ky, uint32_t* ix,
-                            int32_t* sScan) {
+__device__ __forceinline__ void emit_output(const DevParams& P, const DevState& S, int b, const int32_t* lengths,
+                                            int32_t Tc, int32_t fin, int32_t* out_hyps, float* out_scores, double* sc,
+                                            uint64_t* ky, uint32_t* ix, int32_t* sScan) {
   const int tid = threadIdx.x;
   if (fin && P.fusion_source == 1 && P.fusion_interval > 0) {
     select_fused<N>(P, S, b, 0, sc, ky, ix);
@@ -2028,9 +2072,17 @@ __device__ __forceinline__ void emit_output(const DevParams& P, const DevState& 
   }
   const int n = S.nbeam[b];
   const size_t gb = static_cast<size_t>(b) * P.K;
+  // at the end of an utterance, hypotheses inside a word are dropped when at
+  // least one hypothesis ends at a word boundary; otherwise all are ranked
+  int nroot = 0;
+  bool root = false;
+  if (fin) {
+    root = tid < n && S.node[gb + tid] == kRootNode;
+    (void)block_scan<NT>(root ? 1 : 0, sScan, &nroot);
+  }
   bool ok = false;
   if (tid < n) {
-    ok = !fin || S.node[gb + tid] == kRootNode;
+    ok = !fin || root || nroot == 0;
     sc[tid] = ok ? S.pt[gb + tid] + S.Lw[(gb + tid) * P.O] : kNegInf;
     ky[tid] = ok ? S.key[gb + tid] : ~0ull;
     ix[tid] = tid;
@@ -2042,7 +2094,14 @@ __device__ __forceinline__ void emit_output(const DevParams& P, const DevState& 
   int m = 0;
   (void)block_scan<NT>(ok ? 1 : 0, sScan, &m);
   bitonic_sort<N>(sc, ky, ix);
-  if (tid == 0) S.t0[b] += lengths[b];
+  if (tid == 0) {
+    // the stream's frame counter advances by the frames decoded in this call:
+    // a length outside 0..Tc is clamped (the decode did the same) and flagged
+    const int32_t len = lengths[b];
+    const int32_t adv = len < 0 ? 0 : (len > Tc ? Tc : len);
+    if (adv != len) atomicOr(S.flags, kFlagLength);
+    S.t0[b] += adv;
+  }
   int32_t* const sLen = reinterpret_cast<int32_t*>(ky);  // words written per rank (the keys are read)
   __syncthreads();
   for (int r = tid; r < P.K; r += NT) {
@@ -2077,14 +2136,14 @@ __device__ __forceinline__ void emit_output(const DevParams& P, const DevState& 
 // not write it).
 template <int BLOCK>
 __global__ __launch_bounds__(BLOCK) void k_output(const DevParams P, const DevState S,
-                                                  const int32_t* __restrict__ lengths, int32_t fin,
+                                                  const int32_t* __restrict__ lengths, int32_t Tc, int32_t fin,
                                                   int32_t* __restrict__ out_hyps,
                                                   float* __restrict__ out_scores) {
   __shared__ double sc[BLOCK];
   __shared__ uint64_t ky[BLOCK];
   __shared__ uint32_t ix[BLOCK];
   __shared__ int32_t sScan[BLOCK / 64];
-  emit_output<BLOCK, BLOCK>(P, S, blockIdx.x, lengths, fin, out_hyps, out_scores, sc, ky, ix, sScan);
+  emit_output<BLOCK, BLOCK>(P, S, blockIdx.x, lengths, Tc, fin, out_hyps, out_scores, sc, ky, ix, sScan);
 }
 
 }  // namespace
@@ -2122,7 +2181,7 @@ hipError_t launch_build_order(int order, const int32_t* ids, const float* lp, co
 }
 
 hipError_t launch_begin(const DevParams& P, const DevState& S, int32_t B, hipStream_t st) {
-  hipLaunchKernelGGL(k_begin, dim3((B + 255) / 256), dim3(256), 0, st, P, S, B);
+  LB_LAUNCH(k_begin, dim3((B + 255) / 256), dim3(256), st, P, S, B);
   return hipGetLastError();
 }
 
@@ -2153,7 +2212,7 @@ int cu_count() {
 
 hipError_t launch_decode(int K, const KArgs* args, const float* logits, const int32_t* lengths, int32_t B,
                          int32_t Tc, int32_t tau0, int32_t tau1, int32_t fin, int32_t* out_hyps, float* out_scores,
-                         hipStream_t st) {
+                         uint32_t opts, hipStream_t st) {
   const KArgs LB_CONST* A = (const KArgs LB_CONST*)args;
   // One workgroup per stream.  A batch that leaves CUs to spare gets more
   // lanes per hypothesis (up to 512 threads per stream, LPB <= 16); a batch
@@ -2169,7 +2228,7 @@ hipError_t launch_decode(int K, const KArgs* args, const float* logits, const in
   // as their LDS allows)
 #define LB_DECODE(KM, LP, WP, DBUF, HSLOTS, THREADS)                                                         \
   LB_LAUNCH((k_decode<KM, LP, WP, DBUF, HSLOTS>), dim3(B), dim3(THREADS), st, A, logits, lengths, Tc, tau0, tau1, \
-            fin, out_hyps, out_scores)
+            fin, out_hyps, out_scores, opts)
   if (K <= 16 && spare)
     LB_DECODE(16, 16, 1, true, 16, 256);
   else if (K <= 16)
@@ -2213,8 +2272,8 @@ hipError_t launch_fuse_apply(int block, const DevParams& P, const DevState& S, c
 }
 
 hipError_t launch_output(int block, const DevParams& P, const DevState& S, const int32_t* lengths, int32_t B,
-                         int32_t fin, int32_t* out_hyps, float* out_scores, hipStream_t st) {
-  LB_DISPATCH_BLOCK(block, k_output, B, P, S, lengths, fin, out_hyps, out_scores);
+                         int32_t Tc, int32_t fin, int32_t* out_hyps, float* out_scores, hipStream_t st) {
+  LB_DISPATCH_BLOCK(block, k_output, B, P, S, lengths, Tc, fin, out_hyps, out_scores);
   return hipGetLastError();
 }
 

@@ -3,20 +3,16 @@ compare its ranked outputs with the oracle's, utterance by utterance."""
 
 from __future__ import annotations
 
-import math
 import sys
 import time
-from dataclasses import dataclass, field
-from typing import List, Optional
+from typing import Optional
 
 import numpy as np
 
 import oracle
 import paper_2603_14002_amd as lbm
 
-SCORE_TOL = 1e-4       # fp32 hypothesis scores, absolute
-NEAR_TIE = 1e-4        # decision margins below this are counted as near-ties
-EXCUSE_TOL = 1e-9      # a mismatch is excused only at a margin below this (both sides are fp64)
+from tests.parity import Expected, Parity  # noqa: F401  (the comparison protocol)
 
 
 def say(msg: str) -> None:
@@ -98,52 +94,15 @@ def check_padding(H: np.ndarray, S: np.ndarray) -> None:
     assert np.all(H[empty] == -1), "ranks without a hypothesis not all -1"
 
 
-@dataclass
-class Parity:
-    exact: int = 0
-    near_tie: int = 0          # utterances with a decision margin < NEAR_TIE (reported)
-    excused: int = 0           # differs, at a decision margin < EXCUSE_TOL
-    mismatch: List[str] = field(default_factory=list)
-    max_score_err: float = 0.0
-    n_hyps: int = 0
-
-    def report(self, name: str) -> str:
-        return (f"[parity] {name}: exact={self.exact} near_tie={self.near_tie} excused={self.excused} "
-                f"mismatch={len(self.mismatch)} hyps={self.n_hyps} max|dscore|={self.max_score_err:.2e}")
-
-
-def compare(par: Parity, b: int, gpu, orc: oracle.OracleResult, K: int) -> None:
-    gw, gs = gpu
-    if orc.min_margin < NEAR_TIE:
-        par.near_tie += 1
-    ow = [[int(x) for x in w] for w in orc.words[:K]]
-    ot = orc.total[:K]
-    same = gw == ow and len(gs) == len(ot)
-    err = float(np.max(np.abs(gs.astype(np.float64) - ot))) if same and len(ot) else 0.0
-    if same and err <= SCORE_TOL:
-        par.exact += 1
-        par.max_score_err = max(par.max_score_err, err)
-        par.n_hyps += len(ot)
-        return
-    if orc.min_margin < EXCUSE_TOL:
-        par.excused += 1
-        return
-    # locate the first difference for the message
-    k = 0
-    while k < min(len(gw), len(ow)) and gw[k] == ow[k] and abs(float(gs[k]) - ot[k]) <= SCORE_TOL:
-        k += 1
-    detail = (f"utt {b}: first difference at rank {k}: gpu={gw[k] if k < len(gw) else None} "
-              f"{float(gs[k]) if k < len(gs) else None} oracle={ow[k] if k < len(ow) else None} "
-              f"{ot[k] if k < len(ot) else None}; n gpu={len(gw)} oracle={len(ow)} margins={orc.margins}")
-    par.mismatch.append(detail)
-
-
 def oracle_for(d):
     return oracle.Oracle(d.lexicon, d.lm)
 
 
 def check_parity(d, gpu_out, utts, params=None, orc=None, name="", max_mismatch=0, finalize=True,
-                 logits: Optional[np.ndarray] = None, oracle_overrides=None):
+                 logits: Optional[np.ndarray] = None, oracle_overrides=None, min_hyps=1):
+    """The oracle decodes utterances `utts` one by one and each is classified
+    against the decoder's output (tests.parity); no mismatch is allowed and at
+    least `min_hyps` hypotheses must have been compared."""
     p = params or d.workload.params
     orc = orc or oracle_for(d)
     op = oracle.params_from(p, fusion_seed=d.fusion_seed, finalize=1 if finalize else 0,
@@ -153,7 +112,9 @@ def check_parity(d, gpu_out, utts, params=None, orc=None, name="", max_mismatch=
     t0 = time.time()
     for b in utts:
         res = orc.decode(src[b, :d.lengths[b]], op)
-        compare(par, b, gpu_out[b], res, p.beam)
+        gw, gs = gpu_out[b]
+        par.add(b, gw, gs, Expected.from_oracle(res, p.beam))
     say(par.report(name) + f" oracle {time.time() - t0:.1f}s")
     assert len(par.mismatch) <= max_mismatch, "\n".join(par.mismatch[:5])
+    assert par.n_hyps >= min_hyps, f"{name}: only {par.n_hyps} hypotheses compared"
     return par

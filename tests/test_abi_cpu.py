@@ -34,7 +34,7 @@ def test_struct_sizes_match_header_layout():
     assert ctypes.sizeof(lbm.lb_params) == 160
     assert ctypes.sizeof(lbm.lb_ngram_desc) == 144
     assert ctypes.sizeof(lbm.lb_lexicon_desc) == 32
-    assert ctypes.sizeof(lbm.lb_stats) == 248
+    assert ctypes.sizeof(lbm.lb_stats) == 320
 
 
 def _descs():
@@ -91,3 +91,15 @@ def test_null_arguments():
     assert L.lb_fusion_request(None, None, None, None) == lbm.LB_ERR_INVALID_ARG
     assert L.lb_get_status(None, None) == lbm.LB_ERR_INVALID_ARG
     L.lb_destroy(None)
+
+
+def test_library_built_from_other_sources_is_refused(monkeypatch):
+    """lib() loads the library only when its build id equals the hash of the
+    sources in this tree."""
+    import paper_2603_14002_amd.build as bld
+    L = lbm.lib()
+    assert L.lb_build_id().decode() == bld.source_hash()
+    monkeypatch.setattr(lbm, "_lib", None)
+    monkeypatch.setattr(bld, "source_hash", lambda: "0" * 64)
+    with pytest.raises(ImportError, match="built from other sources"):
+        lbm.lib()

@@ -264,3 +264,25 @@ def test_equal_candidates_order_by_parent_subbeam_then_word():
     # after the first word alone: [a0, a1]
     r1 = run(orc, lg[:2], omega=1.0, subbeams=2, lam=100.0)
     assert r1.subs[0] == [(LN10 * -1.0, [0]), (LN10 * -1.0, [1])]
+
+
+# ------------------------------------------------------------------ end of the utterance
+
+def test_end_keeps_word_boundaries_else_every_hypothesis(four_words):
+    # ONE_FRAME with finalisation: () is the only entry at a word boundary, so
+    # it alone is output (total -1.0, no words); (1)..(4) stop inside a word.
+    fin = run(four_words, ONE_FRAME, finalize=1, beam=5)
+    assert labels(fin) == [()] and fin.total.tolist() == [-1.0] and fin.words == [[]]
+    # without a blank the empty prefix dies: no entry ends at a word boundary,
+    # so every entry is ranked with its completed words (none yet)
+    lg = frames({1: -0.5, 2: -1.5, 3: -2.5, 4: -3.0})
+    fin = run(four_words, lg, finalize=1, beam=5)
+    assert labels(fin) == [(1,), (2,), (3,), (4,)]
+    assert fin.total.tolist() == [0.0, -1.0, -2.0, -2.5] and fin.words == [[], [], [], []]
+    # two frames, separator then phoneme: (1 40 2) and (1 40 3) are inside
+    # their second word and keep their first, completed word w0
+    lg2 = frames({1: -0.5}, {40: -0.5}, {2: -0.5, 3: -1.0})
+    fin2 = run(four_words, lg2, finalize=1, beam=5)
+    assert labels(fin2) == [(1, 40, 2), (1, 40, 3)] and fin2.words == [[0], [0]]
+    # (-0.5 + 0.5) + (-0.5 + 0.25) + (-0.5 + 0.5) = -0.25 and -0.75 (omega = 0)
+    assert fin2.total.tolist() == [-0.25, -0.75]
