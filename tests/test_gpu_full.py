@@ -51,6 +51,8 @@ def check_properties(d, out):
 @pytest.mark.parametrize("mode", ["end", "live"])
 @pytest.mark.parametrize("name", ["c2", "c3", "c4", "c5"])
 def test_full_batch_parity(name, mode):
+    if not os.path.exists(golden.path_of(name, mode)):
+        pytest.skip(f"no stored oracle results for {name}/{mode}: run tests/golden/full_parity.py")
     exp, meta = golden.load(name, mode)
     d = workload(name)
     B = d.logits.shape[0]
