@@ -207,6 +207,24 @@ lb_status lb_decode_batch(lb_decoder* dec, const float* logits, const int32_t* l
                           int32_t batch, int32_t frames, uint32_t flags, void* stream,
                           int32_t* out_hyps, float* out_scores);
 
+/* lb_decode_batch for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, hosts that forbid allocation): the
+ * same decode with the same arguments and results, whose n-gram lookup scratch
+ * is a fixed array of 64 MiB per device (held until the process ends) instead
+ * of memory of the decoder; it calls no allocating routine and creates no
+ * events (lb_set_profiling's event timing does not apply; the phase counters
+ * do).  The scratch holds batch x (K * subbeams * H * 32 B + K * 256 B), H the
+ * largest homophone set of the lexicon, rounded up per region: a batch that
+ * needs more returns LB_ERR_CAPACITY (and decodes nothing).  Every such call
+ * on a device shares that device's array: calls that overlap in time on one
+ * device (other streams, other threads, other decoders) race on it and must be
+ * serialised by the caller.  Nothing in the array needs to start at zero (each
+ * frame writes what it reads).  Decoders with LB_FUSION_EXTERNAL are refused
+ * (LB_ERR_INVALID_ARG): their round trip reads the lengths to the host. */
+lb_status lb_decode_batch_noalloc(lb_decoder* dec, const float* logits, const int32_t* lengths, int32_t batch,
+                                  int32_t frames, uint32_t flags, void* stream, int32_t* out_hyps,
+                                  float* out_scores);
+
 /* Exports the word sequences of a pending fusion event (after LB_NEED_FUSION).
  * Entry [b][r][j] is sub-beam j of the stream's r-th fused hypothesis; the
  * fused hypotheses are the top fusion_top_f (all when 0) by total score at a

@@ -30,7 +30,7 @@ STATUS_NAMES = {0: "LB_OK", 1: "LB_ERR_INVALID_ARG", 2: "LB_ERR_STATE", 3: "LB_E
 
 EXPORTED = ("lb_create", "lb_destroy", "lb_decode_batch", "lb_fusion_request", "lb_fusion_scores",
             "lb_get_status", "lb_get_stats", "lb_reset_stats", "lb_set_profiling", "lb_last_error",
-            "lb_build_id")
+            "lb_build_id", "lb_decode_batch_noalloc")
 
 
 class LBError(RuntimeError):
@@ -103,6 +103,8 @@ def lib():
         L.lb_destroy.argtypes = [P]
         L.lb_decode_batch.restype = ctypes.c_int32
         L.lb_decode_batch.argtypes = [P, P, P, ctypes.c_int32, ctypes.c_int32, ctypes.c_uint32, P, P, P]
+        L.lb_decode_batch_noalloc.restype = ctypes.c_int32
+        L.lb_decode_batch_noalloc.argtypes = [P, P, P, ctypes.c_int32, ctypes.c_int32, ctypes.c_uint32, P, P, P]
         L.lb_fusion_request.restype = ctypes.c_int32
         L.lb_fusion_request.argtypes = [P, P, P, P]
         L.lb_fusion_scores.restype = ctypes.c_int32
@@ -175,6 +177,12 @@ def lb_decode_batch(dec: int, logits, lengths, batch: int, frames: int, flags: i
     return _check(lib().lb_decode_batch(dec, _dev_ptr(logits), _dev_ptr(lengths), batch, frames, flags,
                                         _stream_ptr(stream), _dev_ptr(out_hyps), _dev_ptr(out_scores)),
                   allow=(LB_OK, LB_NEED_FUSION))
+
+
+def lb_decode_batch_noalloc(dec: int, logits, lengths, batch: int, frames: int, flags: int, stream,
+                            out_hyps, out_scores) -> int:
+    return _check(lib().lb_decode_batch_noalloc(dec, _dev_ptr(logits), _dev_ptr(lengths), batch, frames, flags,
+                                                _stream_ptr(stream), _dev_ptr(out_hyps), _dev_ptr(out_scores)))
 
 
 def lb_fusion_request(dec: int, words, n_words, stream) -> int:

@@ -140,6 +140,7 @@ struct lb_decoder {
   DevParams P{};
   DevState S{};
   KArgs* dargs = nullptr;  // device copy of P and S for the decode kernel
+  void* static_scratch = nullptr;  // this device's static lookup scratch (lb_decode_batch_noalloc)
   int block = 64;       // workgroup size of the fusion / output kernels (>= beam)
   std::vector<void*> allocs;
   int64_t launches[kKinds] = {};
@@ -617,6 +618,12 @@ lb_status lb_create(const lb_lexicon_desc* lex, const lb_ngram_desc* lm, const l
       return fail(st != LB_OK ? st : LB_ERR_HIP, msg);
     }
   }
+  // the device address of this device's static lookup scratch, for the calls
+  // that allocate nothing (a failure here only disables those calls)
+  if (static_scratch_address(&d->static_scratch) != hipSuccess) {
+    d->static_scratch = nullptr;
+    (void)hipGetLastError();
+  }
   *out = d;
   return LB_OK;
 }
@@ -688,7 +695,7 @@ lb_status lb_decode_batch(lb_decoder* d, const float* logits, const int32_t* len
     LB_HIP(launch(kKindDecode, [&] {
       return launch_decode(P.K, d->dargs, logits, lengths, batch, frames, start, stop, out_here ? fin : 0,
                            out_here ? out_hyps : nullptr, out_here ? out_scores : nullptr,
-                           (d->profile_mask & LB_PROFILE_PHASES) ? kOptPhaseTimers : 0u, st);
+                           (d->profile_mask & LB_PROFILE_PHASES) ? kOptPhaseTimers : 0u, nullptr, st);
     }));
   if (fuse_tau >= 0) {
     for (int32_t b = 0; b < batch; ++b) {
@@ -717,6 +724,46 @@ lb_status lb_decode_batch(lb_decoder* d, const float* logits, const int32_t* len
   if (external) {
     for (int32_t b = 0; b < batch; ++b) X.t0[b] += X.len[b];
     X.in_call = false;
+  }
+  return LB_OK;
+}
+
+lb_status lb_decode_batch_noalloc(lb_decoder* d, const float* logits, const int32_t* lengths, int32_t batch,
+                                  int32_t frames, uint32_t flags, void* stream, int32_t* out_hyps,
+                                  float* out_scores) {
+  g_err.clear();
+  if (!d) return fail(LB_ERR_INVALID_ARG, "decoder is null");
+  if (batch < 1 || batch > d->p.max_batch) return fail(LB_ERR_INVALID_ARG, "batch must be in 1..max_batch");
+  if (frames < 0) return fail(LB_ERR_INVALID_ARG, "frames < 0");
+  if ((frames > 0 && !logits) || !lengths || !out_hyps || !out_scores)
+    return fail(LB_ERR_INVALID_ARG, "null device pointer");
+  if (flags & ~static_cast<uint32_t>(LB_BEGIN | LB_END)) return fail(LB_ERR_INVALID_ARG, "unknown flags");
+  const DevParams& P = d->P;
+  const DevState& S = d->S;
+  if (P.fusion_source == LB_FUSION_EXTERNAL)
+    return fail(LB_ERR_INVALID_ARG, "lb_decode_batch_noalloc does not run the external fusion round trip "
+                                    "(it reads the lengths to the host); use lb_decode_batch");
+  const size_t need = scratch_layout(static_cast<size_t>(batch), S.scap, static_cast<size_t>(P.K)).bytes;
+  if (need > kStaticScratchBytes)
+    return fail(LB_ERR_CAPACITY, "lb_decode_batch_noalloc: " + std::to_string(batch) + " streams need " +
+                                     std::to_string(need) + " B of lookup scratch, the static scratch holds " +
+                                     std::to_string(kStaticScratchBytes) +
+                                     " B; decode fewer streams per call or use lb_decode_batch");
+  if (!d->static_scratch) return fail(LB_ERR_HIP, "the static lookup scratch has no device address on this device");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  // the same launches as lb_decode_batch, without event timing (which creates events)
+  if (flags & LB_BEGIN) {
+    LB_HIP(launch_begin(P, S, batch, st));
+    d->launches[kKindBegin]++;
+  }
+  const int32_t fin = (flags & LB_END) ? 1 : 0;
+  if (frames > 0) {
+    LB_HIP(launch_decode(P.K, d->dargs, logits, lengths, batch, frames, 0, frames, fin, out_hyps, out_scores,
+                         (d->profile_mask & LB_PROFILE_PHASES) ? kOptPhaseTimers : 0u, d->static_scratch, st));
+    d->launches[kKindDecode]++;
+  } else {
+    LB_HIP(launch_output(d->block, P, S, lengths, batch, frames, fin, out_hyps, out_scores, st));
+    d->launches[kKindOutput]++;
   }
   return LB_OK;
 }

@@ -200,6 +200,22 @@ struct DevState {
   uint32_t* scrE;
 };
 
+// Layout of the n-gram lookup scratch of a decode call over nb streams, when it
+// is one contiguous buffer: nb x scap lookup results (f64 log10 P), then nb x
+// scap n-gram states (QState), then nb x K*kMaxSub*kMaxExplicit explicit
+// homophone indices (u32); each region starts on a 256-B boundary.
+struct ScratchLayout {
+  size_t off_state, off_explicit, bytes;
+};
+__host__ __device__ inline ScratchLayout scratch_layout(size_t nb, size_t scap, size_t K) {
+  auto up = [](size_t x) { return (x + 255) & ~static_cast<size_t>(255); };
+  ScratchLayout l;
+  l.off_state = up(nb * scap * sizeof(double));
+  l.off_explicit = l.off_state + up(nb * scap * sizeof(QState));
+  l.bytes = l.off_explicit + up(nb * K * kMaxSub * kMaxExplicit * sizeof(uint32_t));
+  return l;
+}
+
 // The decode kernel's parameters and state, kept in device memory (written
 // once by lb_create) and read through a constant-memory pointer.
 struct KArgs {

@@ -13,6 +13,8 @@
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
+#include <mutex>
+
 #include "lb_device.h"
 #include "lb_launch.h"
 
@@ -561,12 +563,14 @@ __device__ __forceinline__ void emit_output(const DevParams& P, const DevState& 
 // shorter linear probe chains, more LDS).  The decoder's parameters and state
 // (P, S) are read from their device copy A_ in constant memory.  opts bit 0
 // (kOptPhaseTimers): thread 0 adds the clock cycles of each phase of the
-// frame to the stream's phase counters (kCntPhase0 + kPh*).
+// frame to the stream's phase counters (kCntPhase0 + kPh*).  scratch: when
+// given, the n-gram lookup scratch of the call's streams (scratch_layout)
+// instead of the decoder's own buffers.
 template <int KMAX, int LPB, int WPE, bool DB, int HSF>
 __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE))) void k_decode(
     const KArgs LB_CONST* A_, const float* __restrict__ logits, const int32_t* __restrict__ lengths, int32_t Tc,
     int32_t tau0, int32_t tau1, int32_t out_fin, int32_t* __restrict__ out_hyps, float* __restrict__ out_scores,
-    uint32_t opts) {
+    uint32_t opts, unsigned char* __restrict__ scratch) {
   // P and S are read through a pointer that is made opaque in every frame, so
   // that each field is loaded (scalar, from the constant cache) where it is
   // used instead of staying live in scalar registers across the whole loop
@@ -698,8 +702,12 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
   uint32_t lines = 0, plines = 0, c_words = 0;  // per thread
   uint64_t c_queries = 0;
   uint64_t c_exp = 0, c_fused = 0, c_lookups = 0;  // uniform
-  double* const scrL = S.scrL + static_cast<size_t>(b) * S.scap;
-  QState* const scrS = S.scrS + static_cast<size_t>(b) * S.scap;
+  const ScratchLayout slay = scratch_layout(gridDim.x, S.scap, P.K);
+  double* const scrL = (scratch ? reinterpret_cast<double*>(scratch) : S.scrL) + static_cast<size_t>(b) * S.scap;
+  QState* const scrS =
+      (scratch ? reinterpret_cast<QState*>(scratch + slay.off_state) : S.scrS) + static_cast<size_t>(b) * S.scap;
+  uint32_t* const scrE = (scratch ? reinterpret_cast<uint32_t*>(scratch + slay.off_explicit) : S.scrE) +
+                         static_cast<size_t>(b) * P.K * kMaxSub * kMaxExplicit;
   // D = alpha * log-probs of a frame into sD, by wavefront 0 (every lane):
   // raw scores are first normalised by a log-softmax over the 41 classes
   auto set_row = [&](const DevParams& Pr, float xin) {
@@ -1251,7 +1259,6 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
     // n-gram for the group's context, from the continuation index; the others
     // back off to their unigrams and are not looked up.  A group with more than
     // kMaxExplicit of them is looked up in full.
-    uint32_t* const scrE = S.scrE + static_cast<size_t>(b) * P.K * kMaxSub * kMaxExplicit;
     const bool heavy_frame = sHeavy != 0;
     for (int g = tid; g < NG; g += BLOCK) {
       const uint32_t Hg = sGH[g];
@@ -2212,7 +2219,8 @@ int cu_count() {
 
 hipError_t launch_decode(int K, const KArgs* args, const float* logits, const int32_t* lengths, int32_t B,
                          int32_t Tc, int32_t tau0, int32_t tau1, int32_t fin, int32_t* out_hyps, float* out_scores,
-                         uint32_t opts, hipStream_t st) {
+                         uint32_t opts, void* scratch, hipStream_t st) {
+  unsigned char* const scr = static_cast<unsigned char*>(scratch);
   const KArgs LB_CONST* A = (const KArgs LB_CONST*)args;
   // One workgroup per stream.  A batch that leaves CUs to spare gets more
   // lanes per hypothesis (up to 512 threads per stream, LPB <= 16); a batch
@@ -2228,7 +2236,7 @@ hipError_t launch_decode(int K, const KArgs* args, const float* logits, const in
   // as their LDS allows)
 #define LB_DECODE(KM, LP, WP, DBUF, HSLOTS, THREADS)                                                         \
   LB_LAUNCH((k_decode<KM, LP, WP, DBUF, HSLOTS>), dim3(B), dim3(THREADS), st, A, logits, lengths, Tc, tau0, tau1, \
-            fin, out_hyps, out_scores, opts)
+            fin, out_hyps, out_scores, opts, scr)
   if (K <= 16 && spare)
     LB_DECODE(16, 16, 1, true, 16, 256);
   else if (K <= 16)
@@ -2275,6 +2283,36 @@ hipError_t launch_output(int block, const DevParams& P, const DevState& S, const
                          int32_t Tc, int32_t fin, int32_t* out_hyps, float* out_scores, hipStream_t st) {
   LB_DISPATCH_BLOCK(block, k_output, B, P, S, lengths, Tc, fin, out_hyps, out_scores);
   return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ static lookup scratch
+
+// The n-gram lookup scratch of the decode calls that allocate nothing
+// (lb_decode_batch_noalloc): one array per device, held until the process
+// ends, shared by every such call on that device.  Host code never uses the
+// name itself as an address (on the host it stands for the symbol, not for the
+// device memory): static_scratch_address() returns the device address, found
+// with hipGetSymbolAddress once per device, with that device current.
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+
+static std::mutex g_scratch_mu;
+static void* g_scratch_addr[kMaxDevices] = {};
+
+hipError_t static_scratch_address(void** out) {
+  *out = nullptr;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_addr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_scratch_addr[dev] = p;
+  }
+  *out = g_scratch_addr[dev];
+  return hipSuccess;
 }
 
 }  // namespace lb

@@ -17,10 +17,11 @@ hipError_t launch_build_order(int order, const int32_t* ids, const float* lp, co
 hipError_t launch_begin(const DevParams& P, const DevState& S, int32_t B, hipStream_t st);
 // args: device copy of the decoder's parameters and state.  out_hyps /
 // out_scores non-null: the launch also writes the call's output (fin: the end
-// of an utterance), as launch_output would.  opts: kOptPhaseTimers.
+// of an utterance), as launch_output would.  opts: kOptPhaseTimers.  scratch:
+// null (the decoder's lookup scratch) or a buffer laid out by scratch_layout.
 hipError_t launch_decode(int K, const KArgs* args, const float* logits, const int32_t* lengths, int32_t B,
                          int32_t Tc, int32_t tau0, int32_t tau1, int32_t fin, int32_t* out_hyps, float* out_scores,
-                         uint32_t opts, hipStream_t st);
+                         uint32_t opts, void* scratch, hipStream_t st);
 hipError_t launch_fuse_select(int block, const DevParams& P, const DevState& S, const int32_t* flag, int32_t B,
                               hipStream_t st);
 hipError_t launch_fuse_export(int block, const DevParams& P, const DevState& S, int32_t* words, int32_t* n_words,
@@ -29,5 +30,11 @@ hipError_t launch_fuse_apply(int block, const DevParams& P, const DevState& S, c
                              hipStream_t st);
 hipError_t launch_output(int block, const DevParams& P, const DevState& S, const int32_t* lengths, int32_t B,
                          int32_t Tc, int32_t fin, int32_t* out_hyps, float* out_scores, hipStream_t st);
+
+// Capacity of the per-device static lookup scratch, and its device address on
+// the current device (looked up once per device).
+constexpr size_t kStaticScratchBytes = size_t{64} << 20;
+constexpr int kMaxDevices = 64;
+hipError_t static_scratch_address(void** out);
 
 }  // namespace lb
