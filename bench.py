@@ -49,6 +49,11 @@ def parse():
     ap.add_argument("--fusion-scorer", choices=("synthetic", "lm"), default="synthetic",
                     help="lm: fusion scores come back through the external round trip from a small "
                          "randomly initialised causal word LM (the LLM stand-in)")
+    ap.add_argument("--gather-ceiling", type=float, default=0.0, metavar="GB",
+                    help="only time random 64-B line gathers (index_select of rows of 16 floats) from a table "
+                         "of GB gigabytes, the access pattern of the n-gram lookups, and exit")
+    ap.add_argument("--gather-lines", type=int, default=4_500_000,
+                    help="lines gathered per pass in --gather-ceiling (default: about one c4 decode's lookups)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (reads and writes MIB MiB) and exit; "
                          "its FETCH_SIZE / WRITE_SIZE counters calibrate the HBM traffic figures")
@@ -72,6 +77,35 @@ def copy_calibration(mib: int) -> None:
     ms = ev0.elapsed_time(ev1)
     print(json.dumps({"copy_calibration_mib": mib, "bytes_read": n * 4, "bytes_written": n * 4,
                       "ms": ms, "GBps_read_plus_write": 2 * n * 4 / (ms * 1e-3) / 1e9}), flush=True)
+
+
+def gather_ceiling(gb: float, lines: int, reps: int = 5) -> None:
+    """Random 64-B line gathers from an HBM table of `gb` GB (the n-gram lookups'
+    access pattern: one line per probe, uniformly random over the tables), as
+    rows of 16 float32 gathered by index_select into a dense output; prints the
+    best of `reps` passes as read (64 B per line) and read + write GB/s."""
+    import torch
+    n_rows = int(gb * 1e9) // 64
+    table = torch.empty((n_rows, 16), dtype=torch.float32, device="cuda:0")
+    table[:: max(1, n_rows // 1024)].fill_(1.0)
+    g = torch.Generator(device="cuda:0")
+    g.manual_seed(260314002)
+    idx = torch.randint(0, n_rows, (lines,), device="cuda:0", generator=g)
+    out = torch.empty((lines, 16), dtype=torch.float32, device="cuda:0")
+    torch.index_select(table, 0, idx, out=out)
+    best = float("inf")
+    for _ in range(reps):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        torch.index_select(table, 0, idx, out=out)
+        e1.record()
+        torch.cuda.synchronize()
+        best = min(best, e0.elapsed_time(e1))
+    rd = lines * 64.0
+    print(json.dumps({"gather_ceiling_table_GB": n_rows * 64 / 1e9, "lines": lines, "ms": best,
+                      "read_GBps": rd / (best * 1e-3) / 1e9, "read_plus_write_GBps": 2 * rd / (best * 1e-3) / 1e9,
+                      "kernel": "torch index_select, rows of 16 float32 (64 B)"}), flush=True)
 
 
 def kernel_source_hash() -> str:
@@ -227,6 +261,9 @@ def main():
     args = parse()
     if args.copy_calibration:
         copy_calibration(args.copy_calibration)
+        return
+    if args.gather_ceiling:
+        gather_ceiling(args.gather_ceiling, args.gather_lines)
         return
     if args.gpus != 1:
         print(json.dumps({"error": "this decoder runs on one GPU; --gpus N>1 is not supported "

@@ -855,10 +855,13 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
     }
     // the slot of the separator on this lane (-1: none)
     const int c_sep = ((kSep - 1 - ln) % LPB) == 0 ? (kSep - 1 - ln) / LPB : -1;
+    // (the bonuses are read once here: inside the slot loops a constant-memory
+    // load per slot would wait together with the LDS loads)
+    const double bon_ph = P.beta, bon_sep = P.gamma;
     auto score_now = [&](int k) -> double {
       const bool valid = (c_rel >> (LPB * k)) & 1ull;
       const double base = (c_rep == LPB * k) ? c_ab : c_p;
-      const double sc = ((base + sD[1 + ln + LPB * k]) + (k == c_sep ? P.gamma : P.beta)) + c_L;
+      const double sc = ((base + sD[1 + ln + LPB * k]) + (k == c_sep ? bon_sep : bon_ph)) + c_L;
       return valid ? sc : kNegInf;
     };
     auto key_of = [&](int v) -> uint64_t { return v == 0 ? c_key : prefix_step(c_key, v); };
@@ -933,17 +936,17 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
     // across the block reduction; the one-lane instance has the registers)
     if constexpr (LPB > 1) asm volatile("" : "+v"(c_ab), "+v"(c_p), "+v"(c_L), "+v"(c_rel), "+v"(c_key));
     uint32_t bin_stay = 0xFFFFu;
-    if (c_stay != kNegInf && c_stay >= thr) {
-      bin_stay = static_cast<uint32_t>(bin0(0, c_stay));
-      atomicAdd(&sHisto[bin_stay], 1u);
-    }
+    if (c_stay != kNegInf && c_stay >= thr) bin_stay = static_cast<uint32_t>(bin0(0, c_stay));
+    // the bins first, then the histogram: with no LDS write among them, the
+    // slots' log-prob loads are issued together instead of each waiting behind
+    // the previous slot's atomic
     if (shift0 < 0) {
 #pragma unroll
       for (int k = 0; k < NC; ++k) {
         const double sc = score_now(k);
         const bool in = sc >= thr;  // -inf (no candidate) is below any threshold
-        const uint32_t bn = in ? static_cast<uint32_t>(bin_score(best, inv0, sc)) : 0xFFFFu;
-        if (in) atomicAdd(&sHisto[bn], 1u);
+        // branch-free: the bin of an in-range score (best for the others), then a select
+        const uint32_t bn = in ? static_cast<uint32_t>(bin_score(best, inv0, in ? sc : best)) : 0xFFFFu;
         if (k & 1)
           binp[k >> 1] |= bn << 16;
         else
@@ -956,12 +959,17 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
         const double sc = score_now(k);
         const bool in = sc >= thr;
         const uint32_t bn = in ? static_cast<uint32_t>(bin0(1 + ln + LPB * k, sc)) : 0xFFFFu;
-        if (in) atomicAdd(&sHisto[bn], 1u);
         if (k & 1)
           binp[k >> 1] |= bn << 16;
         else
           binp[k >> 1] = bn;
       }
+    }
+    if (bin_stay != 0xFFFFu) atomicAdd(&sHisto[bin_stay], 1u);
+#pragma unroll
+    for (int k = 0; k < NC; ++k) {
+      const uint32_t bn = (binp[k >> 1] >> ((k & 1) * 16)) & 0xFFFFu;
+      if (bn != 0xFFFFu) atomicAdd(&sHisto[bn], 1u);
     }
     lds_barrier();
     const int nvalid = find_bin(P.K);
