@@ -80,6 +80,15 @@ __device__ __forceinline__ void wave_minmax(double* mx, double* mn) {
   *mn = fmin(fmin(readlane_f64(c, 0), readlane_f64(c, 16)), fmin(readlane_f64(c, 32), readlane_f64(c, 48)));
 }
 
+// Wavefront maximum of x, in every lane.
+__device__ __forceinline__ double wave_max(double x) {
+  x = fmax(x, dpp_f64<kDppXor1>(x, -HUGE_VAL));
+  x = fmax(x, dpp_f64<kDppXor2>(x, -HUGE_VAL));
+  x = fmax(x, dpp_f64<kDppHalfMirror>(x, -HUGE_VAL));
+  x = fmax(x, dpp_f64<kDppMirror>(x, -HUGE_VAL));
+  return fmax(fmax(readlane_f64(x, 0), readlane_f64(x, 16)), fmax(readlane_f64(x, 32), readlane_f64(x, 48)));
+}
+
 // Wavefront sum of x, in every lane.
 __device__ __forceinline__ double wave_sum(double x) {
   x += dpp_f64<kDppXor1>(x, 0.0);
@@ -587,6 +596,10 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
   static_assert(KMAX <= 256, "a hash slot holds its hypothesis in 8 bits");
   constexpr int NW = BLOCK / 64;
   constexpr int NC = (kSep + LPB - 1) / LPB;  // extension slots per lane
+  // top-K in one pass over the slots, with the bin range from bounds taken in
+  // the recombination phase, where a lane owns many slots; with few slots per
+  // lane a first pass for the exact range costs less than the bounds
+  constexpr bool kOnePass = NC >= 20;
   static_assert(LPB <= 16 && LPB * NC < 64, "a lane's slots stay below symbol 64");
   static_assert(NC + 1 < 64, "a lane's candidates (its slots and the stay) fit the 64-bit sets sel_bits and bnd");
   constexpr int NPM = KMAX * kMaxSub;  // (completed word, sub-beam) pairs per frame, at most
@@ -605,15 +618,14 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
 
   __shared__ BeamLds<KMAX> sBeam[DB ? 2 : 1];
   __shared__ double sD[64];  // classes 0..40; 41..63 are zero (slots past the separator)
+  __shared__ double sDmax;   // the largest of sD[1..40]
   __shared__ double sAb2[KMAX], sAnb2[KMAX], sPt2[KMAX], sStay[KMAX];
   __shared__ uint64_t sMask[KMAX];
-  // two tables: the one of this frame, and the next frame's, cleared meanwhile
-  // two tables, the next frame's cleared during this one; or, in the one-buffer
-  // instances (whose LDS is scarcer), one table, cleared for the next frame once
-  // this frame's parent lookups are done (the frame's later barriers separate
-  // the clear from the next inserts)
-  constexpr int kHT = DB ? 2 : 1;
-  __shared__ unsigned long long sHKey[kHT][HS];
+  // the prefix keys of the frame's hypotheses: inserted when the hypotheses
+  // are written (in the previous frame, or when the beam is loaded), cleared
+  // once this frame's parent lookups are done (the frame's later barriers
+  // separate the clear from the next inserts)
+  __shared__ unsigned long long sHKey[HS];
   __shared__ uint8_t sHIdx[HS];  // the slot's hypothesis (KMAX <= 256)
   // top-K selection scratch; the LM step and the fusion sort reuse it
   __shared__ __align__(16) unsigned char sSel[UNI_BYTES];
@@ -626,8 +638,11 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
   __shared__ int32_t sLarge[KMAX];  // completed words ranked by a whole wavefront
   __shared__ double sRed[2 * NW], sRedB[2 * NW];
   __shared__ int32_t sScan[NW], sScanB[NW], sScanC[NW], sScanD[NW];
-  __shared__ int32_t sBucket, sAbove, sBucketCnt, sBCount;
-  __shared__ unsigned long long sCnt[4];  // probed lines, completed words, LM queries, index lines
+  __shared__ int32_t sBucket, sAbove, sBucketCnt, sBCount, sAthr;
+  // counters: probed lines, completed words, LM queries, index lines (summed over
+  // the threads at the end), expansions, fused hypotheses, lookups (added by
+  // thread 0 as they occur: kept here, not in every thread's registers)
+  __shared__ unsigned long long sCnt[7];
   // phase cycles of thread 0 (kPh*), and the last timestamp
   __shared__ unsigned long long sPhase[kPhases + 1];
   const bool timing = (opts & kOptPhaseTimers) != 0;
@@ -690,18 +705,28 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
     B0.first[tid] = tn.first_child;
     B0.woff[tid] = tn.word_off;
   }
-  if (tid < 4) sCnt[tid] = 0;
+  if (tid < 7) sCnt[tid] = 0;
   if (timing && tid == 0) {
     for (int k = 0; k < kPhases; ++k) sPhase[k] = 0;
     sPhase[kPhases] = __builtin_amdgcn_s_memtime();
   }
   uint32_t arena_n = S.arena_n[b];
   int cur = 0;  // the current buffer (DB)
-  int hb = 0;  // the current prefix-key table
-  for (int q = tid; q < HS; q += BLOCK) sHKey[0][q] = kEmptyKey;
+  for (int q = tid; q < HS; q += BLOCK) sHKey[q] = kEmptyKey;
+  // a new hypothesis' prefix key into the hash table, with its index r
+  auto insert_key = [&](uint64_t key, int r) {
+    uint32_t s = static_cast<uint32_t>(key) & (HS - 1);
+    for (;;) {
+      const unsigned long long prev = atomicCAS(&sHKey[s], kEmptyKey, key);
+      if (prev == kEmptyKey) {
+        sHIdx[s] = static_cast<uint8_t>(r);
+        break;
+      }
+      s = (s + 1) & (HS - 1);
+    }
+  };
   uint32_t lines = 0, plines = 0, c_words = 0;  // per thread
   uint64_t c_queries = 0;
-  uint64_t c_exp = 0, c_fused = 0, c_lookups = 0;  // uniform
   const ScratchLayout slay = scratch_layout(gridDim.x, S.scap, P.K);
   double* const scrL = (scratch ? reinterpret_cast<double*>(scratch) : S.scrL) + static_cast<size_t>(b) * S.scap;
   QState* const scrS =
@@ -718,13 +743,22 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
       const double sum = wave_sum(lane < kClasses ? exp(x - m) : 0.0);
       x = (x - m) - log(sum);
     }
-    sD[lane] = lane < kClasses ? Pr.alpha * x : 0.0;
+    const double dv = lane < kClasses ? Pr.alpha * x : 0.0;
+    sD[lane] = dv;
+    const double dm = wave_max(lane >= 1 && lane < kClasses ? dv : kNegInf);
+    if (lane == 0) sDmax = dm;
   };
   // the first frame's row now; each frame loads the next frame's row early and
   // writes it to sD after the frame's last global wait
   if (wave == 0)
     set_row(P, lane < kClasses ? logits[(static_cast<size_t>(b) * Tc + tau0) * kClasses + lane] : 0.0f);
   float dnext = 0.0f;
+  lds_barrier();
+  // the loaded hypotheses' keys and trie masks for the first frame
+  if (tid < n) {
+    insert_key(sBeam[0].key[tid], tid);
+    sMask[tid] = sBeam[0].tmask[tid];
+  }
   lds_barrier();
   mark(kPhOther);
 
@@ -742,36 +776,21 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
 
     // the next frame's log-probs are loaded meanwhile
     if (tid < kClasses && tau + 1 < tend) dnext = logits[(static_cast<size_t>(b) * Tc + tau + 1) * kClasses + tid];
-    unsigned long long* const hkey = sHKey[hb];
-    if constexpr (DB)
-      for (int s = tid; s < HS; s += BLOCK) sHKey[hb ^ 1][s] = kEmptyKey;
+    unsigned long long* const hkey = sHKey;  // the frame's prefix keys (inserted with the hypotheses)
     for (int d = tid; d < kBins; d += BLOCK) sHisto[d] = 0;
     if (tid == 0) sBCount = 0;
-
-    // ---- prefix keys into an LDS hash table (cleared during the last frame)
     uint64_t my_pkey = kNoParent;
     uint32_t my_meta = 0;
     if (tid < n) {
-      const uint64_t my_key = C.key[tid];
       my_pkey = C.pkey[tid];
       my_meta = C.meta[tid];
-      sMask[tid] = C.tmask[tid];
-      uint32_t s = static_cast<uint32_t>(my_key) & (HS - 1);
-      for (;;) {
-        const unsigned long long prev = atomicCAS(&hkey[s], kEmptyKey, my_key);
-        if (prev == kEmptyKey) {
-          sHIdx[s] = static_cast<uint8_t>(tid);
-          break;
-        }
-        s = (s + 1) & (HS - 1);
-      }
     }
-    lds_barrier();
 
     // ---- recombination: a hypothesis whose parent prefix is also live receives
     // the parent's extension by its last symbol; that extension is removed from
     // the parent's fan-out.  Stay candidates: blank-stay, repeat-stay, merged
     // parent extension.
+    double st = kNegInf, up = kNegInf;  // this hypothesis' stay score and extension bound
     if (tid < n) {
       int par = -1;
       if (my_pkey != kNoParent) {
@@ -813,14 +832,25 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
       sAb2[tid] = ab2;
       sAnb2[tid] = anb2;
       sPt2[tid] = pt2;
-      sStay[tid] = pt2 + C.Lw[tid * kMaxSub];
+      st = pt2 + C.Lw[tid * kMaxSub];
+      sStay[tid] = st;
+      // no extension of this hypothesis scores above this (each of the additions
+      // rounds monotonically, base <= pt, log-prob <= sDmax, bonus <= the larger)
+      if constexpr (kOnePass) up = ((C.pt[tid] + sDmax) + fmax(P.beta, P.gamma)) + C.Lw[tid * kMaxSub];
+    }
+    if constexpr (kOnePass) {
+      // per wavefront: an upper bound of every candidate (sRedB[w]) and the best
+      // stay (sRedB[NW + w]), for the top-K's bin range
+      double hi = fmax(st, up), nlo = -st;
+      wave_minmax(&hi, &nlo);
+      if (lane == 0) {
+        sRedB[wave] = hi;
+        sRedB[NW + wave] = -nlo;
+      }
     }
     lds_barrier();
     mark(kPhRecomb);
-    if constexpr (DB)
-      hb ^= 1;
-    else
-      for (int s = tid; s < HS; s += BLOCK) sHKey[0][s] = kEmptyKey;  // for the next frame
+    for (int s = tid; s < HS; s += BLOCK) sHKey[s] = kEmptyKey;  // for the new hypotheses' keys
     // Workgroups that share a CU: the CU's arbitration favours the older
     // wavefronts, so the workgroup dispatched second (the later half of the
     // grid, when workgroups are dispatched to the CUs in order) fell behind
@@ -866,32 +896,58 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
     };
     auto key_of = [&](int v) -> uint64_t { return v == 0 ? c_key : prefix_step(c_key, v); };
 
-    double mx = c_stay, mn = c_stay != kNegInf ? c_stay : HUGE_VAL;
+    // ---- top-K and the theta cut.  Level 0 bins the candidates at or above L0
+    // by (U - score) over [L0, U] into kBins, where U is at least every
+    // candidate's score and L0 at most the cut (best - theta); the map is
+    // monotone, so bins above the one holding the K-th candidate are taken
+    // whole, and the bins above the cut's bin hold only candidates above the
+    // cut.  U and L0 come from the recombination phase's bounds (U: the stays
+    // and each hypothesis' extension bound; L0: the best stay - theta), so one
+    // pass over the slots bins them and finds the exact best; the members of
+    // the cut's bin are tested against the cut exactly.  Without a finite stay
+    // a first pass finds best and the lowest candidate: U = best, L0 =
+    // max(best - theta, lowest).  The bin holding the K-th candidate is
+    // resolved exactly by rank on (score desc, key asc) when it holds at most
+    // kBoundaryCap candidates; otherwise it is re-binned over its own score
+    // range (deeper levels), and when its scores are all equal, by the bits of
+    // the key (smaller key first).
+    const double theta = P.theta;
+    double U = kNegInf, Bst = kNegInf;
+    if constexpr (kOnePass) {
+      U = sRedB[0];
+      Bst = sRedB[NW];
 #pragma unroll
-    for (int k = 0; k < NC; ++k) {
-      const double sc = score_now(k);
-      mx = fmax(mx, sc);
-      mn = fmin(mn, sc != kNegInf ? sc : HUGE_VAL);
+      for (int w = 1; w < NW; ++w) {
+        U = fmax(U, sRedB[w]);
+        Bst = fmax(Bst, sRedB[NW + w]);
+      }
     }
-    double best, lowest;
-    block_minmax<BLOCK, false>(mx, mn, sRed, &best, &lowest);
-    const double thr = best - P.theta;
-
-    // ---- top-K.  Level 0 bins (best - score) over [max(thr, lowest), best] into
-    // kBins; the map is monotone, so bins above the one holding the K-th
-    // candidate are taken whole.  That bin is resolved exactly by rank on
-    // (score desc, key asc) when it holds at most kBoundaryCap candidates;
-    // otherwise it is re-binned over its own score range (deeper levels), and
-    // when its scores are all equal, by the bits of the key (smaller key first).
-    const double lo0 = fmax(thr, lowest);
-    const double inv0 = best > lo0 ? static_cast<double>(kBins) / (best - lo0) : 0.0;
-    const int shift0 = best > lo0 ? -1 : 64 - 10;
+    double L0 = Bst - theta;
+    // with a first pass the best is exact before the binning (and every binned
+    // candidate is at or above the cut)
+    const bool first_pass = Bst == kNegInf;  // no bounds, or no finite stay (uniform)
+    double best = kNegInf;
+    if (first_pass) {
+      double mx = c_stay, mn = c_stay != kNegInf ? c_stay : HUGE_VAL;
+#pragma unroll
+      for (int k = 0; k < NC; ++k) {
+        const double sc = score_now(k);
+        mx = fmax(mx, sc);
+        mn = fmin(mn, sc != kNegInf ? sc : HUGE_VAL);
+      }
+      double lowest;
+      block_minmax<BLOCK, false>(mx, mn, sRed, &best, &lowest);
+      U = best;
+      L0 = fmax(best - theta, lowest);
+    }
+    const double inv0 = U > L0 ? static_cast<double>(kBins) / (U - L0) : 0.0;
+    const int shift0 = U > L0 ? -1 : 64 - 10;
     auto bin_score = [&](double hi, double inv, double s) -> int {
       const double x = (hi - s) * inv;
       return x >= static_cast<double>(kBins - 1) ? kBins - 1 : static_cast<int>(x);
     };
     auto bin0 = [&](int v, double s) -> int {
-      return shift0 < 0 ? bin_score(best, inv0, s) : static_cast<int>((key_of(v) >> shift0) & (kBins - 1));
+      return shift0 < 0 ? bin_score(U, inv0, s) : static_cast<int>((key_of(v) >> shift0) & (kBins - 1));
     };
     // deeper levels (rare): parameters in LDS
     auto bin_at = [&](int l, int v, double s) -> int {
@@ -899,8 +955,10 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
       if (sh >= 0) return static_cast<int>((key_of(v) >> sh) & (kBins - 1));
       return bin_score(sLvHi[l], sLvInv[l], s);
     };
-    // finds the bin holding the need-th candidate of sHisto; returns via sBucket/sAbove/sBucketCnt
-    auto find_bin = [&](int need_in) -> int {
+    // finds the bin holding the need-th candidate of sHisto (sBucket, sAbove,
+    // sBucketCnt) and, for bthr < kBins, the number of candidates in the bins
+    // above bin bthr (sAthr); returns the number of binned candidates
+    auto find_bin = [&](int need_in, int bthr) -> int {
       constexpr int PER = (kBins + BLOCK - 1) / BLOCK;
       int local = 0;
 #pragma unroll
@@ -924,6 +982,11 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
           acc += h;
         }
       }
+      if (bthr < kBins && tid == bthr / PER) {
+        int acc = before;
+        for (int d = tid * PER; d < bthr; ++d) acc += static_cast<int>(sHisto[d]);
+        sAthr = acc;
+      }
       lds_barrier();
       return tot;
     };
@@ -935,8 +998,9 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
     // here so that their scores are recomputed below instead of being kept live
     // across the block reduction; the one-lane instance has the registers)
     if constexpr (LPB > 1) asm volatile("" : "+v"(c_ab), "+v"(c_p), "+v"(c_L), "+v"(c_rel), "+v"(c_key));
+    double mxl = c_stay;  // the lane's best candidate
     uint32_t bin_stay = 0xFFFFu;
-    if (c_stay != kNegInf && c_stay >= thr) bin_stay = static_cast<uint32_t>(bin0(0, c_stay));
+    if (c_stay >= L0) bin_stay = static_cast<uint32_t>(bin0(0, c_stay));  // (-inf: no stay)
     // the bins first, then the histogram: with no LDS write among them, the
     // slots' log-prob loads are issued together instead of each waiting behind
     // the previous slot's atomic
@@ -944,9 +1008,10 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
 #pragma unroll
       for (int k = 0; k < NC; ++k) {
         const double sc = score_now(k);
-        const bool in = sc >= thr;  // -inf (no candidate) is below any threshold
-        // branch-free: the bin of an in-range score (best for the others), then a select
-        const uint32_t bn = in ? static_cast<uint32_t>(bin_score(best, inv0, in ? sc : best)) : 0xFFFFu;
+        if constexpr (kOnePass) mxl = fmax(mxl, sc);
+        const bool in = sc >= L0;  // -inf (no candidate) is below any bound
+        // branch-free: the bin of an in-range score (U for the others), then a select
+        const uint32_t bn = in ? static_cast<uint32_t>(bin_score(U, inv0, in ? sc : U)) : 0xFFFFu;
         if (k & 1)
           binp[k >> 1] |= bn << 16;
         else
@@ -957,13 +1022,18 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
 #pragma unroll
       for (int k = 0; k < NC; ++k) {
         const double sc = score_now(k);
-        const bool in = sc >= thr;
+        if constexpr (kOnePass) mxl = fmax(mxl, sc);
+        const bool in = sc >= L0;
         const uint32_t bn = in ? static_cast<uint32_t>(bin0(1 + ln + LPB * k, sc)) : 0xFFFFu;
         if (k & 1)
           binp[k >> 1] |= bn << 16;
         else
           binp[k >> 1] = bn;
       }
+    }
+    if (!first_pass) {
+      const double mxw = wave_max(mxl);  // the exact best, read after the barrier
+      if (lane == 0) sRed[wave] = mxw;
     }
     if (bin_stay != 0xFFFFu) atomicAdd(&sHisto[bin_stay], 1u);
 #pragma unroll
@@ -972,10 +1042,30 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
       if (bn != 0xFFFFu) atomicAdd(&sHisto[bn], 1u);
     }
     lds_barrier();
-    const int nvalid = find_bin(P.K);
-    const bool select_all = nvalid <= P.K;
-    int beta0 = select_all ? kBins : sBucket, nlev = 1, need = P.K, nbc = 0;
-    bool all_bin = false;
+    if (!first_pass) {
+      best = sRed[0];
+#pragma unroll
+      for (int w = 1; w < NW; ++w) best = fmax(best, sRed[w]);
+    }
+    const double thr = best - theta;
+    // the cut's bin (kBins: every binned candidate is at or above the cut)
+    const int bthr = (shift0 < 0 && thr > L0) ? bin_score(U, inv0, thr) : kBins;
+    const int nbinned = find_bin(P.K, bthr);
+    // three cases: the K-th candidate lies above the cut's bin (resolve its
+    // bin); every candidate is selected; or the cut's bin decides (its members
+    // at or above the cut, as many as are still needed)
+    int beta0 = kBins, nlev = 1, need = 0, nbc = 0, cntb = 0;
+    bool all_bin = false, resolve = false, cutbin = false;
+    if (nbinned >= P.K && sBucket < bthr) {
+      beta0 = sBucket;
+      need = P.K - sAbove;
+      cntb = sBucketCnt;
+      resolve = true;
+    } else if (bthr < kBins) {
+      beta0 = bthr;
+      need = P.K - sAthr;
+      cutbin = true;
+    }
     // level 0 decides every candidate outside the boundary bin: above it taken,
     // below it dropped; bnd marks this lane's candidates inside it (bit k: slot
     // k, bit NC: the stay)
@@ -990,6 +1080,39 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
     classify(bin_stay, 0, NC);
 #pragma unroll
     for (int k = 0; k < NC; ++k) classify((binp[k >> 1] >> ((k & 1) * 16)) & 0xFFFFu, k + 1, k);
+    if (cutbin) {
+      // the cut's bin: members below the cut are no candidates.  When the bin
+      // is small (the usual case) its members at or above the cut go straight
+      // to the exact rank, whose list also counts them; otherwise they are
+      // counted first and the bin is refined like any boundary bin.
+      const bool small = static_cast<int>(sHisto[bthr]) <= kBoundaryCap;  // (uniform)
+#pragma unroll 1
+      for (uint64_t m = bnd; m; m &= m - 1) {
+        const int k = __ffsll(static_cast<unsigned long long>(m)) - 1;
+        const double sc = k == NC ? c_stay : score_now(k);
+        if (!(sc >= thr)) {
+          bnd &= ~(1ull << k);
+        } else if (small) {
+          const int slot = atomicAdd(&sBCount, 1);
+          sBScore[slot] = sc;
+          sBKey[slot] = key_of(k == NC ? 0 : 1 + ln + LPB * k);
+        }
+      }
+      if (small) {
+        lds_barrier();
+        nbc = sBCount;
+        cntb = nbc;
+        all_bin = cntb <= need;  // else: ranked exactly below
+      } else {
+        int cnt = 0;
+        (void)block_scan<BLOCK>(__popcll(bnd), sScanD, &cnt);
+        cntb = cnt;
+        if (cntb <= need)
+          all_bin = true;
+        else
+          resolve = true;
+      }
+    }
     // the lane's boundary-bin candidates (v, exact score) that also lie in the
     // boundary bins of levels 1..L-1
     auto for_bnd = [&](int L, auto&& f) {
@@ -1003,9 +1126,7 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
         if (in) f(k, v, sc);
       }
     };
-    if (!select_all) {
-      need -= sAbove;
-      int cntb = sBucketCnt;
+    if (resolve) {
       int key_shift = shift0 >= 0 ? shift0 - 10 : 64 - 10;
       bool key_level = shift0 >= 0;
       int last_shift = shift0;  // shift of the deepest level (-1: score bins)
@@ -1031,7 +1152,7 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
         if (key_level) key_shift -= 10;
         for_bnd(L, [&](int, int v, double sc) { atomicAdd(&sHisto[bin_at(L, v, sc)], 1u); });
         lds_barrier();
-        (void)find_bin(need);
+        (void)find_bin(need, kBins);
         if (tid == 0) sLvBeta[L] = sBucket;
         need -= sAbove;
         cntb = sBucketCnt;
@@ -1171,6 +1292,7 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
     }
     if constexpr (!DB) lds_barrier();  // every source entry has been read
     if (r < nsel) {
+      insert_key(w_key, r);  // for the next frame's parent lookups
       N.key[r] = w_key;
       N.pkey[r] = w_pkey;
       N.ab[r] = w_ab;
@@ -1180,6 +1302,7 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
       N.meta[r] = w_meta;
       if (!tn_load) {
         N.tmask[r] = w_tmask;
+        sMask[r] = w_tmask;
         N.first[r] = w_first;
         N.woff[r] = w_woff;
       }
@@ -1320,7 +1443,7 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
       if (tid == 0) atomicOr(S.flags, kFlagSelect);
       U = 0;
     }
-    c_lookups += static_cast<uint64_t>(U);
+    if (tid == 0) sCnt[6] += static_cast<unsigned long long>(U);
     // the results go to LDS when they fit in the grouping keys freed above (the
     // usual case), else to the stream's scratch in global memory
     constexpr int kLdsRes = 12 * NPL / 32;
@@ -1703,12 +1826,13 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
       const uint64_t an = static_cast<uint64_t>(arena_n) + static_cast<uint64_t>(nev * O);
       arena_n = static_cast<uint32_t>(an <= S.arena_cap ? an : S.arena_cap + 1);
     }
-    c_exp += static_cast<uint64_t>(n) * kClasses;
+    if (tid == 0) sCnt[4] += static_cast<unsigned long long>(n) * kClasses;
     n = nsel;
     __syncthreads();  // history nodes (global memory) are read by the fusion and the next frame
     mark(kPhRank);
     if (tn_load) {
       N.tmask[r] = tn.mask;
+      sMask[r] = tn.mask;
       N.first[r] = tn.first_child;
       N.woff[r] = tn.word_off;
     }
@@ -1770,7 +1894,7 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
           }
         }
       }
-      c_fused += static_cast<uint64_t>(F);
+      if (tid == 0) sCnt[5] += static_cast<unsigned long long>(F);
     }
     lds_barrier();
     mark(kPhFusion);
@@ -1815,14 +1939,14 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
     S.nbeam[b] = n;
     S.arena_n[b] = arena_n;
     unsigned long long* cn = S.counters + static_cast<size_t>(b) * kNumCounters;
-    cn[kCntExpansions] += c_exp;
+    cn[kCntExpansions] += sCnt[4];
     cn[kCntFrames] += static_cast<unsigned long long>(tend - tau0);
     cn[kCntWordEvents] += sCnt[1];
     cn[kCntLmQueries] += sCnt[2];
-    cn[kCntFused] += c_fused;
+    cn[kCntFused] += sCnt[5];
     cn[kCntProbeLines] += sCnt[0] + sCnt[3];
     cn[kCntPresLines] += sCnt[3];
-    cn[kCntLookups] += c_lookups;
+    cn[kCntLookups] += sCnt[6];
   }
   if (out_hyps) {
     __syncthreads();  // the beam is back in global memory
