@@ -79,33 +79,36 @@ def copy_calibration(mib: int) -> None:
                       "ms": ms, "GBps_read_plus_write": 2 * n * 4 / (ms * 1e-3) / 1e9}), flush=True)
 
 
-def gather_ceiling(gb: float, lines: int, reps: int = 5) -> None:
-    """Random 64-B line gathers from an HBM table of `gb` GB (the n-gram lookups'
-    access pattern: one line per probe, uniformly random over the tables), as
-    rows of 16 float32 gathered by index_select into a dense output; prints the
-    best of `reps` passes as read (64 B per line) and read + write GB/s."""
+def gather_bandwidth(gb: float, lines: int, reps: int = 5) -> dict:
+    """Random 64-B line gathers (lb_measure_gather) from a device table of `gb`
+    GB: the n-gram probes' access pattern (one line per probe, uniformly random
+    over the tables).  Best of `reps` passes, timed with events on the stream
+    of the gathers."""
     import torch
-    n_rows = int(gb * 1e9) // 64
-    table = torch.empty((n_rows, 16), dtype=torch.float32, device="cuda:0")
-    table[:: max(1, n_rows // 1024)].fill_(1.0)
-    g = torch.Generator(device="cuda:0")
-    g.manual_seed(260314002)
-    idx = torch.randint(0, n_rows, (lines,), device="cuda:0", generator=g)
-    out = torch.empty((lines, 16), dtype=torch.float32, device="cuda:0")
-    torch.index_select(table, 0, idx, out=out)
+    import paper_2603_14002_amd as lbm
+    n_lines = max(1, int(gb * 1e9) // 64)
+    table = torch.empty(n_lines * 16, dtype=torch.float32, device="cuda:0")
+    threads = (lines + 7) // 8
+    out = torch.empty(threads, dtype=torch.int32, device="cuda:0")
+    stream = torch.cuda.current_stream()
+    lbm.lb_measure_gather(table, n_lines, lines, 260314002, out, threads, stream)
     best = float("inf")
-    for _ in range(reps):
+    for r in range(reps):
         e0 = torch.cuda.Event(enable_timing=True)
         e1 = torch.cuda.Event(enable_timing=True)
-        e0.record()
-        torch.index_select(table, 0, idx, out=out)
-        e1.record()
+        e0.record(stream)
+        lbm.lb_measure_gather(table, n_lines, lines, 260314002 + r + 1, out, threads, stream)
+        e1.record(stream)
         torch.cuda.synchronize()
         best = min(best, e0.elapsed_time(e1))
-    rd = lines * 64.0
-    print(json.dumps({"gather_ceiling_table_GB": n_rows * 64 / 1e9, "lines": lines, "ms": best,
-                      "read_GBps": rd / (best * 1e-3) / 1e9, "read_plus_write_GBps": 2 * rd / (best * 1e-3) / 1e9,
-                      "kernel": "torch index_select, rows of 16 float32 (64 B)"}), flush=True)
+    del table, out
+    torch.cuda.empty_cache()
+    return {"table_GB": n_lines * 64 / 1e9, "lines": lines, "ms": best,
+            "GBps": lines * 64.0 / (best * 1e-3) / 1e9, "kernel": "k_gather_probe (lb_measure_gather)"}
+
+
+def gather_ceiling(gb: float, lines: int) -> None:
+    print(json.dumps(gather_bandwidth(gb, lines)), flush=True)
 
 
 def kernel_source_hash() -> str:
@@ -395,10 +398,16 @@ def main():
             ach = look_bytes / look_s / 1e9 if look_s > 0 else None
             out_phase = dict(share=share, cycles_per_stream_frame={n: c / max(1, sph.frames) for n, c in
                                                                    zip(lbm.PHASE_NAMES, cyc)})
+            # the random 64-B gather ceiling over a table as large as the workload's n-gram tables
+            lf = lp.lm_load_factor if lp.lm_load_factor > 0 else 0.25
+            table_gb = sum(d.lm.counts[1:]) / lf * 16 / 1e9
+            ceil = gather_bandwidth(table_gb, max(4_000_000, int(look_bytes // LINE_BYTES)))
             roof_lookup = dict(
                 kernel="k_decode n-gram lookup phase", bound="hbm", achieved=ach, peak=HBM_PEAK_GBS, unit="GB/s",
                 frac=None if ach is None else ach / HBM_PEAK_GBS,
                 frac_of_copy=None if ach is None else ach / roof["copy_GBps"],
+                gather_ceiling=ceil,
+                frac_of_gather_ceiling=None if ach is None else ach / ceil["GBps"],
                 traffic=None, bytes_per_launch=look_bytes,
                 lines_per_launch=(sph.probe_lines - sph.index_lines) / nl3,
                 lookups_per_launch=sph.lm_lookups / nl3,

@@ -269,6 +269,18 @@ lb_status lb_set_profiling(lb_decoder* dec, uint32_t kernel_mask);
 /* Thread-local description of the last error ("" if none). */
 const char* lb_last_error(void);
 
+/* Measurement: the random-gather ceiling of the n-gram probes' access
+ * pattern (one 64-B bucket line per probe, at random positions of tables far
+ * larger than the caches).  Reads n_lines lines of 64 B from the device table
+ * `table` (table_lines lines, 16-B aligned) at pseudo-random line indices
+ * (the multiply-high of splitmix64(seed + i) and table_lines, for i =
+ * 0..n_lines-1), 8 independent lines per thread, and writes each thread's XOR
+ * of what it read to out (device uint32, out_len >= ceil(n_lines / 8)).
+ * Asynchronous on `stream`; the caller times it.  LB_ERR_INVALID_ARG for
+ * null pointers, zero sizes or a short out. */
+lb_status lb_measure_gather(const void* table, uint64_t table_lines, uint64_t n_lines, uint64_t seed,
+                            uint32_t* out, uint64_t out_len, void* stream);
+
 /* Identity of the build: a hex sha256 over the library's source files
  * (comments and spacing removed) and its compile flags, fixed at build time,
  * so that a caller can check that the library in hand was built from the

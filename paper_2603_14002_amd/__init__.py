@@ -30,7 +30,7 @@ STATUS_NAMES = {0: "LB_OK", 1: "LB_ERR_INVALID_ARG", 2: "LB_ERR_STATE", 3: "LB_E
 
 EXPORTED = ("lb_create", "lb_destroy", "lb_decode_batch", "lb_fusion_request", "lb_fusion_scores",
             "lb_get_status", "lb_get_stats", "lb_reset_stats", "lb_set_profiling", "lb_last_error",
-            "lb_build_id", "lb_decode_batch_noalloc")
+            "lb_build_id", "lb_decode_batch_noalloc", "lb_measure_gather")
 
 
 class LBError(RuntimeError):
@@ -105,6 +105,8 @@ def lib():
         L.lb_decode_batch.argtypes = [P, P, P, ctypes.c_int32, ctypes.c_int32, ctypes.c_uint32, P, P, P]
         L.lb_decode_batch_noalloc.restype = ctypes.c_int32
         L.lb_decode_batch_noalloc.argtypes = [P, P, P, ctypes.c_int32, ctypes.c_int32, ctypes.c_uint32, P, P, P]
+        L.lb_measure_gather.restype = ctypes.c_int32
+        L.lb_measure_gather.argtypes = [P, ctypes.c_uint64, ctypes.c_uint64, ctypes.c_uint64, P, ctypes.c_uint64, P]
         L.lb_fusion_request.restype = ctypes.c_int32
         L.lb_fusion_request.argtypes = [P, P, P, P]
         L.lb_fusion_scores.restype = ctypes.c_int32
@@ -183,6 +185,11 @@ def lb_decode_batch_noalloc(dec: int, logits, lengths, batch: int, frames: int, 
                             out_hyps, out_scores) -> int:
     return _check(lib().lb_decode_batch_noalloc(dec, _dev_ptr(logits), _dev_ptr(lengths), batch, frames, flags,
                                                 _stream_ptr(stream), _dev_ptr(out_hyps), _dev_ptr(out_scores)))
+
+
+def lb_measure_gather(table, table_lines: int, n_lines: int, seed: int, out, out_len: int, stream) -> int:
+    return _check(lib().lb_measure_gather(_dev_ptr(table), table_lines, n_lines, seed & (2**64 - 1), _dev_ptr(out),
+                                          out_len, _stream_ptr(stream)))
 
 
 def lb_fusion_request(dec: int, words, n_words, stream) -> int:

@@ -798,6 +798,17 @@ lb_status lb_fusion_scores(lb_decoder* d, const float* fusion_logprobs, void* st
   return LB_OK;
 }
 
+lb_status lb_measure_gather(const void* table, uint64_t table_lines, uint64_t n_lines, uint64_t seed,
+                            uint32_t* out, uint64_t out_len, void* stream) {
+  g_err.clear();
+  if (!table || !out) return fail(LB_ERR_INVALID_ARG, "null device pointer");
+  if (table_lines < 1 || n_lines < 1) return fail(LB_ERR_INVALID_ARG, "table_lines and n_lines must be >= 1");
+  if (out_len < gather_probe_threads(n_lines))
+    return fail(LB_ERR_INVALID_ARG, "out needs " + std::to_string(gather_probe_threads(n_lines)) + " entries");
+  LB_HIP(launch_gather_probe(table, table_lines, n_lines, seed, out, static_cast<hipStream_t>(stream)));
+  return LB_OK;
+}
+
 lb_status lb_get_status(lb_decoder* d, void* stream) {
   if (!d) return fail(LB_ERR_INVALID_ARG, "decoder is null");
   LB_HIP(hipStreamSynchronize(static_cast<hipStream_t>(stream)));

@@ -2285,6 +2285,33 @@ __global__ __launch_bounds__(BLOCK) void k_output(const DevParams P, const DevSt
   emit_output<BLOCK, BLOCK>(P, S, blockIdx.x, lengths, Tc, fin, out_hyps, out_scores, sc, ky, ix, sScan);
 }
 
+// ------------------------------------------------------------------ gather ceiling
+
+// Reads kGatherPerThread random 64-B lines of a table per thread (line index:
+// the multiply-high of splitmix64(seed + i) and the line count, i the global
+// gather number), all loads issued before any is used, and writes each thread's
+// XOR of what it read so that no load is optimised away: the access pattern of
+// the n-gram probes, one 64-B bucket line per probe, as independent threads.
+constexpr int kGatherPerThread = 8;
+__global__ __launch_bounds__(256) void k_gather_probe(const uint4* __restrict__ table, uint64_t lines, uint64_t n,
+                                                      uint64_t seed, uint32_t* __restrict__ out) {
+  const uint64_t t = static_cast<uint64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  uint4 v[kGatherPerThread][4];
+#pragma unroll
+  for (int g = 0; g < kGatherPerThread; ++g) {
+    const uint64_t i = t * kGatherPerThread + g;
+    const uint64_t line = i < n ? __umul64hi(splitmix64(seed + i), lines) : 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) v[g][q] = i < n ? table[line * 4 + q] : make_uint4(0, 0, 0, 0);
+  }
+  uint32_t x = 0;
+#pragma unroll
+  for (int g = 0; g < kGatherPerThread; ++g)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) x ^= v[g][q].x ^ v[g][q].y ^ v[g][q].z ^ v[g][q].w;
+  if (t * kGatherPerThread < n) out[t] = x;
+}
+
 }  // namespace
 
 // ------------------------------------------------------------------ launchers
@@ -2316,6 +2343,19 @@ hipError_t launch_build_order(int order, const int32_t* ids, const float* lp, co
   const int grid = static_cast<int>(blocks < 65536 ? blocks : 65536);
   hipLaunchKernelGGL(k_build_order, dim3(grid), dim3(256), 0, st, order, ids, lp, bo, count, vocab, t2, t3,
                      dst, flags, ctx_out);
+  return hipGetLastError();
+}
+
+uint64_t gather_probe_threads(uint64_t n) { return (n + kGatherPerThread - 1) / kGatherPerThread; }
+
+hipError_t launch_gather_probe(const void* table, uint64_t lines, uint64_t n, uint64_t seed, uint32_t* out,
+                               hipStream_t st) {
+  const uint64_t threads = gather_probe_threads(n);
+  const uint64_t blocks = (threads + 255) / 256;
+  if (blocks == 0) return hipSuccess;
+  if (blocks > 0x7FFFFFFFull) return hipErrorInvalidValue;
+  LB_LAUNCH(k_gather_probe, dim3(static_cast<unsigned>(blocks)), dim3(256), st, static_cast<const uint4*>(table), lines,
+            n, seed, out);
   return hipGetLastError();
 }
 

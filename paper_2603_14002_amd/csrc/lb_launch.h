@@ -15,6 +15,11 @@ hipError_t launch_build_order(int order, const int32_t* ids, const float* lp, co
                               int32_t vocab, NgramTable t2, NgramTable t3, NgramTable dst, uint32_t* flags,
                               uint32_t* ctx_out, hipStream_t st);
 hipError_t launch_begin(const DevParams& P, const DevState& S, int32_t B, hipStream_t st);
+// The random 64-B line gather of lb_measure_gather, and the number of threads
+// (= out entries) it runs for n gathers.
+uint64_t gather_probe_threads(uint64_t n);
+hipError_t launch_gather_probe(const void* table, uint64_t lines, uint64_t n, uint64_t seed, uint32_t* out,
+                               hipStream_t st);
 // args: device copy of the decoder's parameters and state.  out_hyps /
 // out_scores non-null: the launch also writes the call's output (fin: the end
 // of an utterance), as launch_output would.  opts: kOptPhaseTimers.  scratch:

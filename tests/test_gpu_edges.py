@@ -273,3 +273,32 @@ def test_profiling_changes_nothing_and_leaves_no_error(name):
     for b in range(B):
         n = len(plain[b][0])
         assert np.array_equal(Sn[b, :n], plain[b][1])
+
+
+# ------------------------------------------------------------------ gather ceiling probe
+
+def test_gather_probe_reads_the_lines_it_names():
+    """lb_measure_gather reads line mulhi(splitmix64(seed + i), lines) for
+    gather i, 8 per thread, and writes each thread's XOR of the 16 words it
+    read: the same XOR computed here from the table's contents."""
+    import torch
+    lines, n, seed = 1000, 8 * 37 + 5, 12345
+    rng = np.random.default_rng(4)
+    host = rng.integers(0, 2**32, size=(lines, 16), dtype=np.uint64).astype(np.uint32)
+    table = torch.from_numpy(host.view(np.int32)).to("cuda:0")
+    threads = (n + 7) // 8
+    out = torch.full((threads,), -1, dtype=torch.int32, device="cuda:0")
+    lbm.lb_measure_gather(table, lines, n, seed, out, threads, None)
+    torch.cuda.synchronize()
+    got = out.cpu().numpy().view(np.uint32)
+    for t in range(threads):
+        x = 0
+        for g in range(8):
+            i = t * 8 + g
+            if i < n:
+                line = (pins.splitmix64((seed + i) & pins.M64) * lines) >> 64
+                for w in host[line]:
+                    x ^= int(w)
+        assert int(got[t]) == x, t
+    with pytest.raises(lbm.LBError):
+        lbm.lb_measure_gather(table, lines, n, seed, out, threads - 1, None)
