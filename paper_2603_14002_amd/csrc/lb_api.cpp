@@ -145,6 +145,8 @@ struct lb_decoder {
   std::vector<void*> allocs;
   int64_t launches[kKinds] = {};
   uint32_t profile_mask = 0;  // kernel kinds timed with HIP events (bit k = kind k), LB_PROFILE_PHASES
+  // the decode kernel's options
+  uint32_t decode_opts() const { return (profile_mask & LB_PROFILE_PHASES) ? kOptPhaseTimers : 0u; }
   std::vector<EventPair> pending;
   std::vector<hipEvent_t> pool;
   double kernel_ms[kKinds] = {};
@@ -695,7 +697,7 @@ lb_status lb_decode_batch(lb_decoder* d, const float* logits, const int32_t* len
     LB_HIP(launch(kKindDecode, [&] {
       return launch_decode(P.K, d->dargs, logits, lengths, batch, frames, start, stop, out_here ? fin : 0,
                            out_here ? out_hyps : nullptr, out_here ? out_scores : nullptr,
-                           (d->profile_mask & LB_PROFILE_PHASES) ? kOptPhaseTimers : 0u, nullptr, st);
+                           d->decode_opts(), nullptr, st);
     }));
   if (fuse_tau >= 0) {
     for (int32_t b = 0; b < batch; ++b) {
@@ -759,7 +761,7 @@ lb_status lb_decode_batch_noalloc(lb_decoder* d, const float* logits, const int3
   const int32_t fin = (flags & LB_END) ? 1 : 0;
   if (frames > 0) {
     LB_HIP(launch_decode(P.K, d->dargs, logits, lengths, batch, frames, 0, frames, fin, out_hyps, out_scores,
-                         (d->profile_mask & LB_PROFILE_PHASES) ? kOptPhaseTimers : 0u, d->static_scratch, st));
+                         d->decode_opts(), d->static_scratch, st));
     d->launches[kKindDecode]++;
   } else {
     LB_HIP(launch_output(d->block, P, S, lengths, batch, frames, fin, out_hyps, out_scores, st));

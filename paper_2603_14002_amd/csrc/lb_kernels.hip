@@ -601,7 +601,7 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
   // lane a first pass for the exact range costs less than the bounds
   constexpr bool kOnePass = NC >= 20;
   static_assert(LPB <= 16 && LPB * NC < 64, "a lane's slots stay below symbol 64");
-  static_assert(NC + 1 < 64, "a lane's candidates (its slots and the stay) fit the 64-bit sets sel_bits and bnd");
+  static_assert(NC + 2 < 64, "a lane's candidates (its slots, the stay and the repeat) fit the 64-bit sets sel_bits and bnd");
   constexpr int NPM = KMAX * kMaxSub;  // (completed word, sub-beam) pairs per frame, at most
   constexpr int NPL = NPM < 256 ? NPM : 256;  // pairs grouped at once
   constexpr int NEB = NPL / kMaxSub;          // completed words per batch
@@ -888,13 +888,25 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
     // (the bonuses are read once here: inside the slot loops a constant-memory
     // load per slot would wait together with the LDS loads)
     const double bon_ph = P.beta, bon_sep = P.gamma;
+    // the repeat extension (the hypothesis' last symbol again, from its
+    // blank-ending part) is a candidate of its own, position NC + 1, and its
+    // slot is left out of the slot loops, whose extensions all start from pt
+    int c_rk = -1;            // its slot on this lane (-1: not on this lane, or invalid)
+    double c_rps = kNegInf;   // its score
+    if (c_rep >= 0 && c_rep % LPB == 0 && ((c_rel >> c_rep) & 1ull)) {
+      c_rk = c_rep / LPB;
+      c_rps = ((c_ab + sD[1 + ln + c_rep]) + (c_rk == c_sep ? bon_sep : bon_ph)) + c_L;
+      c_rel &= ~(1ull << c_rep);
+    }
     auto score_now = [&](int k) -> double {
       const bool valid = (c_rel >> (LPB * k)) & 1ull;
-      const double base = (c_rep == LPB * k) ? c_ab : c_p;
-      const double sc = ((base + sD[1 + ln + LPB * k]) + (k == c_sep ? bon_sep : bon_ph)) + c_L;
+      const double sc = ((c_p + sD[1 + ln + LPB * k]) + (k == c_sep ? bon_sep : bon_ph)) + c_L;
       return valid ? sc : kNegInf;
     };
     auto key_of = [&](int v) -> uint64_t { return v == 0 ? c_key : prefix_step(c_key, v); };
+    // position k of the lane: slot k (k < NC), the stay (NC), the repeat (NC + 1)
+    auto pos_v = [&](int k) -> int { return k == NC ? 0 : 1 + ln + LPB * (k == NC + 1 ? c_rk : k); };
+    auto pos_score = [&](int k) -> double { return k == NC ? c_stay : (k == NC + 1 ? c_rps : score_now(k)); };
 
     // ---- top-K and the theta cut.  Level 0 bins the candidates at or above L0
     // by (U - score) over [L0, U] into kBins, where U is at least every
@@ -928,7 +940,8 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
     const bool first_pass = Bst == kNegInf;  // no bounds, or no finite stay (uniform)
     double best = kNegInf;
     if (first_pass) {
-      double mx = c_stay, mn = c_stay != kNegInf ? c_stay : HUGE_VAL;
+      double mx = fmax(c_stay, c_rps);
+      double mn = fmin(c_stay != kNegInf ? c_stay : HUGE_VAL, c_rps != kNegInf ? c_rps : HUGE_VAL);
 #pragma unroll
       for (int k = 0; k < NC; ++k) {
         const double sc = score_now(k);
@@ -946,8 +959,15 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
       const double x = (hi - s) * inv;
       return x >= static_cast<double>(kBins - 1) ? kBins - 1 : static_cast<int>(x);
     };
+    // level 0: (U - s) * inv0 as one fused multiply-add of s, clamped to the
+    // bins; each step rounds monotonically, so a higher score never takes a
+    // higher bin (U bounds every candidate, so the value is at least about 0)
+    const double ninv0 = -inv0, uinv0 = U * inv0;
+    auto bin_lv0 = [&](double s) -> int {
+      return static_cast<int>(fmax(fmin(fma(s, ninv0, uinv0), static_cast<double>(kBins - 1)), 0.0));
+    };
     auto bin0 = [&](int v, double s) -> int {
-      return shift0 < 0 ? bin_score(U, inv0, s) : static_cast<int>((key_of(v) >> shift0) & (kBins - 1));
+      return shift0 < 0 ? bin_lv0(s) : static_cast<int>((key_of(v) >> shift0) & (kBins - 1));
     };
     // deeper levels (rare): parameters in LDS
     auto bin_at = [&](int l, int v, double s) -> int {
@@ -998,20 +1018,21 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
     // here so that their scores are recomputed below instead of being kept live
     // across the block reduction; the one-lane instance has the registers)
     if constexpr (LPB > 1) asm volatile("" : "+v"(c_ab), "+v"(c_p), "+v"(c_L), "+v"(c_rel), "+v"(c_key));
-    double mxl = c_stay;  // the lane's best candidate
-    uint32_t bin_stay = 0xFFFFu;
+    uint32_t bin_stay = 0xFFFFu, bin_rep = 0xFFFFu;
     if (c_stay >= L0) bin_stay = static_cast<uint32_t>(bin0(0, c_stay));  // (-inf: no stay)
+    if (c_rps >= L0) bin_rep = static_cast<uint32_t>(bin0(pos_v(NC + 1), c_rps));
     // the bins first, then the histogram: with no LDS write among them, the
     // slots' log-prob loads are issued together instead of each waiting behind
     // the previous slot's atomic
     if (shift0 < 0) {
 #pragma unroll
       for (int k = 0; k < NC; ++k) {
-        const double sc = score_now(k);
-        if constexpr (kOnePass) mxl = fmax(mxl, sc);
-        const bool in = sc >= L0;  // -inf (no candidate) is below any bound
-        // branch-free: the bin of an in-range score (U for the others), then a select
-        const uint32_t bn = in ? static_cast<uint32_t>(bin_score(U, inv0, in ? sc : U)) : 0xFFFFu;
+        // branch-free: the score and bin of the slot, valid or not (a bin in
+        // range either way), then a select
+        const bool valid = (c_rel >> (LPB * k)) & 1ull;
+        const double sc = ((c_p + sD[1 + ln + LPB * k]) + (k == c_sep ? bon_sep : bon_ph)) + c_L;
+        const bool in = valid && sc >= L0;
+        const uint32_t bn = in ? static_cast<uint32_t>(bin_lv0(sc)) : 0xFFFFu;
         if (k & 1)
           binp[k >> 1] |= bn << 16;
         else
@@ -1022,7 +1043,6 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
 #pragma unroll
       for (int k = 0; k < NC; ++k) {
         const double sc = score_now(k);
-        if constexpr (kOnePass) mxl = fmax(mxl, sc);
         const bool in = sc >= L0;
         const uint32_t bn = in ? static_cast<uint32_t>(bin0(1 + ln + LPB * k, sc)) : 0xFFFFu;
         if (k & 1)
@@ -1031,26 +1051,37 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
           binp[k >> 1] = bn;
       }
     }
-    if (!first_pass) {
-      const double mxw = wave_max(mxl);  // the exact best, read after the barrier
-      if (lane == 0) sRed[wave] = mxw;
-    }
     if (bin_stay != 0xFFFFu) atomicAdd(&sHisto[bin_stay], 1u);
+    if (bin_rep != 0xFFFFu) atomicAdd(&sHisto[bin_rep], 1u);
 #pragma unroll
     for (int k = 0; k < NC; ++k) {
       const uint32_t bn = (binp[k >> 1] >> ((k & 1) * 16)) & 0xFFFFu;
       if (bn != 0xFFFFu) atomicAdd(&sHisto[bn], 1u);
     }
     lds_barrier();
+    // With bounds, the exact best is needed only if the K-th candidate may lie
+    // at or below U - theta (>= best - theta): when it lies in a bin above that
+    // value's, every candidate up to it is above the cut, which cannot bind.
+    int nbinned = 0, bthr = kBins;
+    bool exact_cut = first_pass;
     if (!first_pass) {
-      best = sRed[0];
+      const double thr_hi = U - theta;
+      const int bhi = (shift0 < 0 && thr_hi > L0) ? bin_lv0(thr_hi) : kBins;
+      nbinned = find_bin(P.K, kBins);
+      if (!(nbinned >= P.K && sBucket < bhi)) {
+        double mx = fmax(c_stay, c_rps);
 #pragma unroll
-      for (int w = 1; w < NW; ++w) best = fmax(best, sRed[w]);
+        for (int k = 0; k < NC; ++k) mx = fmax(mx, score_now(k));
+        best = block_max<BLOCK>(mx, sRed);
+        exact_cut = true;
+      }
     }
-    const double thr = best - theta;
-    // the cut's bin (kBins: every binned candidate is at or above the cut)
-    const int bthr = (shift0 < 0 && thr > L0) ? bin_score(U, inv0, thr) : kBins;
-    const int nbinned = find_bin(P.K, bthr);
+    const double thr = best - theta;  // (read only with exact_cut)
+    if (exact_cut) {
+      // the cut's bin (kBins: every binned candidate is at or above the cut)
+      bthr = (shift0 < 0 && thr > L0) ? bin_lv0(thr) : kBins;
+      nbinned = find_bin(P.K, bthr);
+    }
     // three cases: the K-th candidate lies above the cut's bin (resolve its
     // bin); every candidate is selected; or the cut's bin decides (its members
     // at or above the cut, as many as are still needed)
@@ -1078,6 +1109,7 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
       bnd |= static_cast<uint64_t>(static_cast<int>(bn) == beta0) << bbit;
     };
     classify(bin_stay, 0, NC);
+    classify(bin_rep, NC + 1, NC + 1);
 #pragma unroll
     for (int k = 0; k < NC; ++k) classify((binp[k >> 1] >> ((k & 1) * 16)) & 0xFFFFu, k + 1, k);
     if (cutbin) {
@@ -1089,13 +1121,13 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
 #pragma unroll 1
       for (uint64_t m = bnd; m; m &= m - 1) {
         const int k = __ffsll(static_cast<unsigned long long>(m)) - 1;
-        const double sc = k == NC ? c_stay : score_now(k);
+        const double sc = pos_score(k);
         if (!(sc >= thr)) {
           bnd &= ~(1ull << k);
         } else if (small) {
           const int slot = atomicAdd(&sBCount, 1);
           sBScore[slot] = sc;
-          sBKey[slot] = key_of(k == NC ? 0 : 1 + ln + LPB * k);
+          sBKey[slot] = key_of(pos_v(k));
         }
       }
       if (small) {
@@ -1119,8 +1151,8 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
 #pragma unroll 1
       for (uint64_t m = bnd; m; m &= m - 1) {
         const int k = __ffsll(static_cast<unsigned long long>(m)) - 1;
-        const int v = k == NC ? 0 : 1 + ln + LPB * k;
-        const double sc = k == NC ? c_stay : score_now(k);
+        const int v = pos_v(k);
+        const double sc = pos_score(k);
         bool in = true;
         for (int l = 1; l < L && in; ++l) in = bin_at(l, v, sc) == sLvBeta[l];
         if (in) f(k, v, sc);
@@ -1181,8 +1213,8 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
 #pragma unroll 1
     for (uint64_t m = bnd; m; m &= m - 1) {
       const int k = __ffsll(static_cast<unsigned long long>(m)) - 1;
-      const int v = k == NC ? 0 : 1 + ln + LPB * k;
-      const double sc = k == NC ? c_stay : score_now(k);
+      const int v = pos_v(k);
+      const double sc = pos_score(k);
       bool take = true;
       bool decided = false;
       for (int l = 1; l < nlev && !decided; ++l) {
@@ -1198,7 +1230,7 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
         for (int u = 0; u < nbc; ++u) rank += ranks_before(sBScore[u], sBKey[u], sc, key);
         take = rank < need;
       }
-      if (take) sel_bits |= 1ull << (k == NC ? 0 : k + 1);
+      if (take) sel_bits |= 1ull << (k == NC ? 0 : (k == NC + 1 ? NC + 1 : k + 1));
     }
     int nsel = 0;
     int wpos = block_scan<BLOCK, false>(__popcll(sel_bits), sScanB, &nsel);
@@ -1209,7 +1241,7 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
 #pragma unroll 1
     for (uint64_t m = sel_bits; m && wpos < nsel; m &= m - 1) {
       const int bit = __ffsll(static_cast<unsigned long long>(m)) - 1;
-      const uint32_t v = bit == 0 ? 0u : static_cast<uint32_t>(1 + ln + LPB * (bit - 1));
+      const uint32_t v = static_cast<uint32_t>(pos_v(bit == 0 ? NC : (bit == NC + 1 ? NC + 1 : bit - 1)));
       sSelSrc[wpos++] = static_cast<uint32_t>(hi_) | (v << 16);
     }
     lds_barrier();
@@ -2399,8 +2431,8 @@ hipError_t launch_decode(int K, const KArgs* args, const float* logits, const in
   // with more streams than one round of workgroups holds gets the instances
   // that fit more workgroups per CU: K = 64 with 4 per CU instead of 3 (128
   // registers, some spilling; one in-place LDS beam buffer), K = 256 with 2 per
-  // CU (one in-place LDS beam buffer, one lane per hypothesis: 256 threads, so
-  // the registers need not be capped).
+  // CU (one in-place LDS beam buffer; two lanes per hypothesis, 512 threads,
+  // so 128 registers).
   const int cus = cu_count();
   const bool spare = B <= cus;
   // (hash slots per hypothesis: 16 with one workgroup per CU and K <= 64, 8 at
@@ -2428,7 +2460,7 @@ hipError_t launch_decode(int K, const KArgs* args, const float* logits, const in
   else if (spare)
     LB_DECODE(256, 2, 1, true, 8, 512);
   else
-    LB_DECODE(256, 1, 2, false, 8, 256);
+    LB_DECODE(256, 2, 4, false, 8, 512);
 #undef LB_DECODE
   return hipGetLastError();
 }

@@ -277,6 +277,30 @@ def test_profiling_changes_nothing_and_leaves_no_error(name):
 
 # ------------------------------------------------------------------ gather ceiling probe
 
+@pytest.mark.parametrize("theta", [4.0, 1.5])
+def test_k256_theta_cut_matches_oracle(theta):
+    """A theta small enough to bind inside the beam-256 selection (the cut's
+    bin tested exactly against best - theta), in the instance for small
+    batches (two lanes per hypothesis) and the one for batches beyond the CU
+    count (one lane per hypothesis): the oracle's beams, and every copy of a
+    tiled batch decoded like the original."""
+    d = load_workload("t-k256")
+    p = DecodeParams(**{**d.workload.params.__dict__, "theta": theta})
+    n = d.logits.shape[0]
+    say(f"[case] k256 theta={theta}: B={n}")
+    small = gpu_decode(d, params=p)
+    check_parity(d, small, range(n), params=p, name=f"t-k256 theta={theta}")
+    big = 300
+    reps = (big + n - 1) // n
+    tile = lambda a: np.concatenate([a] * reps)[:big]
+    db = WorkloadData(d.workload, d.lexicon, d.lm, tile(d.logits), tile(d.lengths), tile(d.targets),
+                      (d.words * reps)[:big], d.fusion_seed)
+    say(f"[case] k256 theta={theta}: B={big}")
+    out = gpu_decode(db, params=p)
+    for b in range(big):
+        assert out[b][0] == small[b % n][0] and np.array_equal(out[b][1], small[b % n][1]), b
+
+
 def test_gather_probe_reads_the_lines_it_names():
     """lb_measure_gather reads line mulhi(splitmix64(seed + i), lines) for
     gather i, 8 per thread, and writes each thread's XOR of the 16 words it
