@@ -214,7 +214,9 @@ def test_heavy_walk_edges(case):
 def test_crowded_boundary_bins(sigma):
     """Uniform (or nearly uniform) log-probs make thousands of candidates share
     the boundary score bin: exact ties are ordered by key bits, clustered
-    scores by refined score bins; both must match the oracle."""
+    scores by refined score bins; both must match the oracle, in the beam-256
+    kernel for small batches and, for a tiled batch of 300, in the one for
+    batches beyond the CU count."""
     base = load_workload("t-k256")
     rng = np.random.default_rng(11)
     B, T = 2, 7
@@ -225,11 +227,19 @@ def test_crowded_boundary_bins(sigma):
     d = WorkloadData(wl, base.lexicon, base.lm, lg, np.full(B, T, np.int32), np.zeros((B, T), np.int32),
                      [[], []], base.fusion_seed)
     say(f"[case] crowded bins sigma={sigma}")
+    big = 300  # more streams than CUs: the other beam-256 kernel
+    tile = lambda a: np.concatenate([a] * (big // B))
+    db = WorkloadData(wl, base.lexicon, base.lm, tile(lg), np.full(big, T, np.int32), np.zeros((big, T), np.int32),
+                      [[]] * big, base.fusion_seed)
     for fin in (False, True):
         out = gpu_decode(d, params=p, finalize=fin)
         par = check_parity(d, out, range(B), params=p, name=f"crowded/{sigma}", finalize=fin)
         if not fin:
             assert par.n_hyps == B * 256
+        say(f"[case] crowded bins sigma={sigma} B={big} fin={fin}")
+        outb = gpu_decode(db, params=p, finalize=fin)
+        for b in range(big):
+            assert outb[b][0] == out[b % B][0] and np.array_equal(outb[b][1], out[b % B][1]), b
 
 
 @pytest.mark.parametrize("name", ["t-c20k", "t-c125k"])
