@@ -915,10 +915,11 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
     // whole, and the bins above the cut's bin hold only candidates above the
     // cut.  U and L0 come from the recombination phase's bounds (U: the stays
     // and each hypothesis' extension bound; L0: the best stay - theta), so one
-    // pass over the slots bins them and finds the exact best; the members of
-    // the cut's bin are tested against the cut exactly.  Without a finite stay
-    // a first pass finds best and the lowest candidate: U = best, L0 =
-    // max(best - theta, lowest).  The bin holding the K-th candidate is
+    // pass over the slots bins them; the exact best is taken only where the
+    // cut might bind (below), and then the members of the cut's bin are tested
+    // against the cut exactly.  Without a finite stay (and in the instances
+    // without bounds) a first pass finds best and the lowest candidate: U =
+    // best, L0 = max(best - theta, lowest).  The bin holding the K-th candidate is
     // resolved exactly by rank on (score desc, key asc) when it holds at most
     // kBoundaryCap candidates; otherwise it is re-binned over its own score
     // range (deeper levels), and when its scores are all equal, by the bits of
