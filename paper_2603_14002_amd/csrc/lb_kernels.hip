@@ -164,16 +164,10 @@ __device__ inline void block_minmax(double mx, double mn, double* red, double* o
   *out_min = c;
 }
 
-// Exclusive prefix sum over the block; *total receives the block sum.  With
-// SYNC = false the trailing barrier is left out: `red` must then not be
-// written again before the next barrier.
-template <int BLOCK, bool SYNC = true>
-__device__ inline int block_scan(int v, int* red, int* total) {
-  const int lane = threadIdx.x & 63;
-  const int w = threadIdx.x >> 6;
-  // inclusive wavefront scan: shifts by 1, 2, 4, 8 inside each row of 16 lanes
-  // (lanes shifted in from outside the row add 0), then rows 1 and 3 add the
-  // last lane of the row before them, and rows 2 and 3 add lane 31
+// Inclusive prefix sum over the wavefront: shifts by 1, 2, 4, 8 inside each
+// row of 16 lanes (lanes shifted in from outside the row add 0), then rows 1
+// and 3 add the last lane of the row before them, and rows 2 and 3 add lane 31.
+__device__ __forceinline__ int wave_scan_incl(int v) {
   int x = v;
   x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xF, 0xF, true);
   x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xF, 0xF, true);
@@ -181,6 +175,17 @@ __device__ inline int block_scan(int v, int* red, int* total) {
   x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xF, 0xF, true);
   x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xA, 0xF, false);
   x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xC, 0xF, false);
+  return x;
+}
+
+// Exclusive prefix sum over the block; *total receives the block sum.  With
+// SYNC = false the trailing barrier is left out: `red` must then not be
+// written again before the next barrier.
+template <int BLOCK, bool SYNC = true>
+__device__ inline int block_scan(int v, int* red, int* total) {
+  const int lane = threadIdx.x & 63;
+  const int w = threadIdx.x >> 6;
+  const int x = wave_scan_incl(v);
   if (lane == 63) red[w] = x;
   lds_barrier();
   int base = 0, tot = 0;
@@ -638,7 +643,7 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
   __shared__ int32_t sLarge[KMAX];  // completed words ranked by a whole wavefront
   __shared__ double sRed[2 * NW], sRedB[2 * NW];
   __shared__ int32_t sScan[NW], sScanB[NW], sScanC[NW], sScanD[NW];
-  __shared__ int32_t sBucket, sAbove, sBucketCnt, sBCount, sAthr;
+  __shared__ int32_t sBucket, sAbove, sBucketCnt, sBCount, sAthr, sNBinned;
   // counters: probed lines, completed words, LM queries, index lines (summed over
   // the threads at the end), expansions, fused hypotheses, lookups (added by
   // thread 0 as they occur: kept here, not in every thread's registers)
@@ -978,38 +983,51 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
     };
     // finds the bin holding the need-th candidate of sHisto (sBucket, sAbove,
     // sBucketCnt) and, for bthr < kBins, the number of candidates in the bins
-    // above bin bthr (sAthr); returns the number of binned candidates
+    // above bin bthr (sAthr); returns the number of binned candidates.  The
+    // first wavefront scans the bins, 16 per lane, so one barrier ends it.
     auto find_bin = [&](int need_in, int bthr) -> int {
-      constexpr int PER = (kBins + BLOCK - 1) / BLOCK;
-      int local = 0;
+      constexpr int PERW = kBins / 64;
+      static_assert(PERW % 4 == 0, "bins per lane in 16-B loads");
+      if (wave == 0) {
+        int h[PERW];
+        const uint4* hp = reinterpret_cast<const uint4*>(sHisto + lane * PERW);
 #pragma unroll
-      for (int q = 0; q < PER; ++q) {
-        const int d = tid * PER + q;
-        local += d < kBins ? static_cast<int>(sHisto[d]) : 0;
-      }
-      int tot = 0;
-      const int before = block_scan<BLOCK, false>(local, sScan, &tot);
-      if (need_in > 0 && before < need_in && before + local >= need_in) {
-        int acc = before;
-        for (int q = 0; q < PER; ++q) {
-          const int d = tid * PER + q;
-          const int h = static_cast<int>(sHisto[d]);
-          if (acc + h >= need_in) {
-            sBucket = d;
-            sAbove = acc;
-            sBucketCnt = h;
-            break;
+        for (int q = 0; q < PERW / 4; ++q) {
+          const uint4 x4 = hp[q];
+          h[4 * q] = static_cast<int>(x4.x);
+          h[4 * q + 1] = static_cast<int>(x4.y);
+          h[4 * q + 2] = static_cast<int>(x4.z);
+          h[4 * q + 3] = static_cast<int>(x4.w);
+        }
+        int local = 0;
+#pragma unroll
+        for (int q = 0; q < PERW; ++q) local += h[q];
+        const int incl = wave_scan_incl(local);
+        const int before = incl - local;
+        if (lane == 63) sNBinned = incl;
+        if (need_in > 0 && before < need_in && incl >= need_in) {
+          int acc = before;
+          bool found = false;
+#pragma unroll
+          for (int q = 0; q < PERW; ++q) {
+            if (!found && acc + h[q] >= need_in) {
+              sBucket = lane * PERW + q;
+              sAbove = acc;
+              sBucketCnt = h[q];
+              found = true;
+            }
+            acc += h[q];
           }
-          acc += h;
+        }
+        if (bthr < kBins && lane == bthr / PERW) {
+          int acc = before;
+#pragma unroll
+          for (int q = 0; q < PERW; ++q) acc += (lane * PERW + q < bthr) ? h[q] : 0;
+          sAthr = acc;
         }
       }
-      if (bthr < kBins && tid == bthr / PER) {
-        int acc = before;
-        for (int d = tid * PER; d < bthr; ++d) acc += static_cast<int>(sHisto[d]);
-        sAthr = acc;
-      }
       lds_barrier();
-      return tot;
+      return sNBinned;
     };
 
     // level-0 bin of each of the lane's candidates, kept packed 16 bits per slot
