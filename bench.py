@@ -50,8 +50,8 @@ def parse():
                     help="lm: fusion scores come back through the external round trip from a small "
                          "randomly initialised causal word LM (the LLM stand-in)")
     ap.add_argument("--gather-ceiling", type=float, default=0.0, metavar="GB",
-                    help="only time random 64-B line gathers (index_select of rows of 16 floats) from a table "
-                         "of GB gigabytes, the access pattern of the n-gram lookups, and exit")
+                    help="only time random 64-B line gathers (lb_measure_gather) from a device table of GB "
+                         "gigabytes, the access pattern of the n-gram lookups, and exit")
     ap.add_argument("--gather-lines", type=int, default=4_500_000,
                     help="lines gathered per pass in --gather-ceiling (default: about one c4 decode's lookups)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
