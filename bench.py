@@ -1,6 +1,6 @@
 """Throughput of the MI355X LightBeam decoding path on one GPU.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c4] [--fusion-scorer lm]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload c4] [--fusion-scorer lm] [--merge max]
 
 One step decodes one whole batch of the workload (LB_BEGIN | LB_END over all
 frames; streaming workloads are fed chunk by chunk) with the inputs already in
@@ -46,6 +46,10 @@ def parse():
                     help="utterances decoded by the CPU oracle (0 = four per host thread, at most 16 threads)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true", help="skip per-kernel event timing")
+    ap.add_argument("--merge", choices=("lse", "max"), default="lse",
+                    help="max: paths into one prefix recombined by their maximum (the best alignment, App. E.1) "
+                         "instead of log-sum-exp; the committed traffic and parity figures are for log-sum-exp, "
+                         "so the line reports them as null")
     ap.add_argument("--fusion-scorer", choices=("synthetic", "lm"), default="synthetic",
                     help="lm: fusion scores come back through the external round trip from a small "
                          "randomly initialised causal word LM (the LLM stand-in)")
@@ -213,7 +217,7 @@ def committed_parity(workload: str):
     return out
 
 
-def cpu_baseline(d, n_utts: int, threads: int):
+def cpu_baseline(d, n_utts: int, threads: int, merge_max: bool = False):
     """The oracle, as it stands, on the first n_utts utterances (full length), one
     utterance per host thread; returns expansions/s and the sample description,
     and the first utterance decoded alone on one core."""
@@ -221,7 +225,7 @@ def cpu_baseline(d, n_utts: int, threads: int):
     t0 = time.time()
     orc = oracle.Oracle(d.lexicon, d.lm)
     log(f"oracle loaded in {time.time() - t0:.1f}s")
-    op = oracle.params_from(d.workload.params, fusion_seed=d.fusion_seed)
+    op = oracle.params_from(d.workload.params, fusion_seed=d.fusion_seed, merge_max=1 if merge_max else 0)
     L0 = int(d.lengths[0])
     t0 = time.time()
     r0 = orc.decode(d.logits[0, :L0], op, max_hyps=d.workload.params.beam)
@@ -288,7 +292,8 @@ def main():
     if external and p.fusion_interval <= 0:
         raise SystemExit(f"workload {wl.name} has no fusion")
     lp = lbm.make_params(p, max_batch=B, max_frames=T, fusion_seed=d.fusion_seed,
-                         fusion_source=lbm.LB_FUSION_EXTERNAL if external else None)
+                         fusion_source=lbm.LB_FUSION_EXTERNAL if external else None,
+                         merge=lbm.LB_MERGE_MAX if args.merge == "max" else lbm.LB_MERGE_LOGSUMEXP)
     dec = lbm.Decoder(d.lexicon, d.lm, lp)
     log(f"lb_create {time.time() - t0:.1f}s")
     dev = torch.device("cuda:0")
@@ -376,7 +381,8 @@ def main():
         avg_us = 1000.0 * sp.kernel_ms[i] / max(1, sp.timed[i])
         alg = {k: v / nl for k, v in algorithmic_bytes(sp, B, T, p, lp).items()}
         roof = dict(kernel="k_decode", bound="hbm", achieved=alg["total"] / (avg_us * 1e-6) / 1e9,
-                    peak=HBM_PEAK_GBS, unit="GB/s", frac=None, traffic=measured_traffic(wl.name),
+                    peak=HBM_PEAK_GBS, unit="GB/s", frac=None,
+                    traffic=measured_traffic(wl.name) if args.merge == "lse" else None,
                     bytes_per_launch=alg, avg_launch_us=avg_us, launches=nl,
                     timing="start/stop events carried by each k_decode dispatch (hipExtLaunchKernel), "
                            "a second pass of the same steps",
@@ -433,7 +439,7 @@ def main():
         "config": {"workload": wl.name, "batch": B, "frames": T, "beam": p.beam, "subbeams": p.subbeams,
                    "lexicon_words": d.lexicon.n_words, "ngrams": int(sum(d.lm.counts)),
                    "fusion_interval": p.fusion_interval, "fusion_top_f": p.fusion_top_f,
-                   "chunk": chunk, "parallelism": "none (1 GPU)"},
+                   "chunk": chunk, "merge": args.merge, "parallelism": "none (1 GPU)"},
         "audio_sec_per_wall_sec": audio / (ms / 1000.0),
         "rtf_per_stream": (ms / 1000.0) / (T * FRAME_SECONDS) if chunk == 0
         else (ms / 1000.0) / len(chunks) / (chunk * FRAME_SECONDS),
@@ -445,7 +451,7 @@ def main():
         "roofline": roof,
         "roofline_lookup_phase": roof_lookup,
         "phases": out_phase,
-        "parity": committed_parity(wl.name),
+        "parity": committed_parity(wl.name) if args.merge == "lse" else None,
     }
     if external:
         n = args.steps
@@ -466,7 +472,7 @@ def main():
     if not args.no_cpu_baseline:
         threads = min(os.cpu_count() or 1, 16)
         n = args.cpu_sample or 4 * threads
-        out["cpu_baseline"] = cpu_baseline(d, min(n, B), threads)
+        out["cpu_baseline"] = cpu_baseline(d, min(n, B), threads, merge_max=args.merge == "max")
     dec.close()
     print(json.dumps(out), flush=True)
 
