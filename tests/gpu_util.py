@@ -20,6 +20,28 @@ def say(msg: str) -> None:
     sys.stdout.flush()
 
 
+def read_outputs(hyps, scores):
+    """The ranked outputs of a decode call (device tensors [B, K, W] and [B, K],
+    already synchronised) as (words per rank, fp32 scores) per utterance; the
+    rows' padding is checked on the way."""
+    H = hyps.cpu().numpy()
+    S = scores.cpu().numpy()
+    check_padding(H, S)
+    B, K, W = H.shape
+    out = []
+    for b in range(B):
+        words, sc = [], []
+        for r in range(K):
+            if not np.isfinite(S[b, r]):
+                break
+            row = H[b, r]
+            n = int(np.argmax(row < 0)) if (row < 0).any() else W
+            words.append([int(x) for x in row[:n]])
+            sc.append(S[b, r])
+        out.append((words, np.array(sc, dtype=np.float32)))
+    return out
+
+
 def gpu_decode(d, params=None, chunk: int = 0, batch: Optional[int] = None, fusion_source=None,
                profiling=False, max_words: Optional[int] = None, arena_nodes_per_stream: int = 0,
                return_decoder=False, finalize=True, logits: Optional[np.ndarray] = None, lb_overrides=None):
@@ -63,20 +85,7 @@ def gpu_decode(d, params=None, chunk: int = 0, batch: Optional[int] = None, fusi
     torch.cuda.synchronize()
     st = dec.status()
     assert st == lbm.LB_OK, lbm.lb_last_error()
-    H = hyps.cpu().numpy()
-    S = scores.cpu().numpy()
-    check_padding(H, S)
-    out = []
-    for b in range(B):
-        words, sc = [], []
-        for r in range(K):
-            if not np.isfinite(S[b, r]):
-                break
-            row = H[b, r]
-            n = int(np.argmax(row < 0)) if (row < 0).any() else W
-            words.append([int(x) for x in row[:n]])
-            sc.append(S[b, r])
-        out.append((words, np.array(sc, dtype=np.float32)))
+    out = read_outputs(hyps, scores)
     if return_decoder:
         return out, dec
     dec.close()

@@ -10,7 +10,7 @@ import pytest
 
 import paper_2603_14002_amd as lbm
 from tests import test_oracle_pruning_pins as pins
-from tests.gpu_util import check_parity, gpu_decode, say
+from tests.gpu_util import check_parity, gpu_decode, read_outputs, say
 from tests.tinylm import lexicon_from, lm_from_entries, peaked_logits
 from workloads import DecodeParams, load_workload
 from workloads.gen import WorkloadData
@@ -299,6 +299,51 @@ def test_k256_theta_cut_matches_oracle(theta):
     out = gpu_decode(db, params=p)
     for b in range(big):
         assert out[b][0] == small[b % n][0] and np.array_equal(out[b][1], small[b % n][1]), b
+
+
+def test_two_decoders_on_two_streams():
+    """Two decoders (a 20k-word workload and a beam-256 one) fed 10-frame
+    chunks, their calls interleaved, each on a stream of its own: both decode
+    exactly as they do alone (decoders share no state)."""
+    import torch
+    ds = [load_workload("t-c20k"), load_workload("t-k256")]
+    chunk = 10
+    solo = [gpu_decode(d, chunk=chunk) for d in ds]
+    dev = torch.device("cuda:0")
+    runs = []
+    for d in ds:
+        p = d.workload.params
+        B, T = d.logits.shape[:2]
+        lp = lbm.make_params(p, max_batch=B, max_frames=T, fusion_seed=d.fusion_seed)
+        dec = lbm.Decoder(d.lexicon, d.lm, lp)
+        lg = torch.from_numpy(np.ascontiguousarray(d.logits)).to(dev)
+        nch = (T + chunk - 1) // chunk
+        parts = []
+        for c in range(nch):
+            lo, hi = c * chunk, min(T, (c + 1) * chunk)
+            ln = np.clip(d.lengths - lo, 0, hi - lo).astype(np.int32)
+            parts.append((lg[:, lo:hi].contiguous(), torch.from_numpy(ln).to(dev)))
+        hyps = torch.empty((B, lp.beam, lp.max_words_out), dtype=torch.int32, device=dev)
+        scores = torch.empty((B, lp.beam), dtype=torch.float32, device=dev)
+        runs.append(dict(dec=dec, parts=parts, hyps=hyps, scores=scores, stream=torch.cuda.Stream()))
+    torch.cuda.synchronize()  # the inputs are in place before either stream starts
+    say("[case] two decoders on two streams: t-c20k and t-k256, 10-frame chunks")
+    for c in range(max(len(r["parts"]) for r in runs)):
+        for r in runs:
+            n = len(r["parts"])
+            if c < n:
+                fl = (lbm.LB_BEGIN if c == 0 else 0) | (lbm.LB_END if c == n - 1 else 0)
+                st, _, _ = r["dec"].decode(r["parts"][c][0], r["parts"][c][1], fl, stream=r["stream"],
+                                           out_hyps=r["hyps"], out_scores=r["scores"])
+                assert st == lbm.LB_OK
+    torch.cuda.synchronize()
+    for r, ref in zip(runs, solo):
+        assert r["dec"].status(r["stream"]) == lbm.LB_OK, lbm.lb_last_error()
+        out = read_outputs(r["hyps"], r["scores"])
+        assert len(out) == len(ref)
+        for b, (got, want) in enumerate(zip(out, ref)):
+            assert got[0] == want[0] and np.array_equal(got[1], want[1]), b
+        r["dec"].close()
 
 
 def test_gather_probe_reads_the_lines_it_names():
