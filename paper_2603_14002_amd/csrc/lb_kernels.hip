@@ -14,6 +14,7 @@
 #include <hip/hip_runtime.h>
 
 #include <mutex>
+#include <type_traits>
 
 #include "lb_device.h"
 #include "lb_launch.h"
@@ -606,7 +607,9 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
   // lane a first pass for the exact range costs less than the bounds
   constexpr bool kOnePass = NC >= 20;
   static_assert(LPB <= 16 && LPB * NC < 64, "a lane's slots stay below symbol 64");
-  static_assert(NC + 2 < 64, "a lane's candidates (its slots, the stay and the repeat) fit the 64-bit sets sel_bits and bnd");
+  static_assert(NC + 2 < 64, "a lane's candidates (its slots, the stay and the repeat) fit the sets sel_bits and bnd");
+  // the candidate sets of a lane: 32 bits where its positions fit
+  using CandSet = typename std::conditional<(NC + 2 <= 32), uint32_t, uint64_t>::type;
   constexpr int NPM = KMAX * kMaxSub;  // (completed word, sub-beam) pairs per frame, at most
   constexpr int NPL = NPM < 256 ? NPM : 256;  // pairs grouped at once
   constexpr int NEB = NPL / kMaxSub;          // completed words per batch
@@ -1119,13 +1122,22 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
     // level 0 decides every candidate outside the boundary bin: above it taken,
     // below it dropped; bnd marks this lane's candidates inside it (bit k: slot
     // k, bit NC: the stay)
-    uint64_t sel_bits = 0;  // bit 0: the stay, bit k+1: slot k
-    uint64_t bnd = 0;
+    CandSet sel_bits = 0;  // bit 0: the stay, bit k+1: slot k
+    CandSet bnd = 0;
+    // lowest set bit and population count of a candidate set
+    auto set_ffs = [](CandSet m) -> int {
+      if constexpr (sizeof(CandSet) == 4) return __ffs(m) - 1;
+      else return __ffsll(static_cast<unsigned long long>(m)) - 1;
+    };
+    auto set_popc = [](CandSet m) -> int {
+      if constexpr (sizeof(CandSet) == 4) return __popc(m);
+      else return __popcll(m);
+    };
     // (branch-free: 0xFFFF, no candidate, is above every bin index; the two
     // sets are updated separately so that they stay in registers)
     auto classify = [&](uint32_t bn, int bit, int bbit) {
-      sel_bits |= static_cast<uint64_t>(static_cast<int>(bn) < beta0) << bit;
-      bnd |= static_cast<uint64_t>(static_cast<int>(bn) == beta0) << bbit;
+      sel_bits |= static_cast<CandSet>(static_cast<int>(bn) < beta0) << bit;
+      bnd |= static_cast<CandSet>(static_cast<int>(bn) == beta0) << bbit;
     };
     classify(bin_stay, 0, NC);
     classify(bin_rep, NC + 1, NC + 1);
@@ -1138,11 +1150,11 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
       // counted first and the bin is refined like any boundary bin.
       const bool small = static_cast<int>(sHisto[bthr]) <= kBoundaryCap;  // (uniform)
 #pragma unroll 1
-      for (uint64_t m = bnd; m; m &= m - 1) {
-        const int k = __ffsll(static_cast<unsigned long long>(m)) - 1;
+      for (CandSet m = bnd; m; m &= m - 1) {
+        const int k = set_ffs(m);
         const double sc = pos_score(k);
         if (!(sc >= thr)) {
-          bnd &= ~(1ull << k);
+          bnd &= ~(CandSet{1} << k);
         } else if (small) {
           const int slot = atomicAdd(&sBCount, 1);
           sBScore[slot] = sc;
@@ -1156,7 +1168,7 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
         all_bin = cntb <= need;  // else: ranked exactly below
       } else {
         int cnt = 0;
-        (void)block_scan<BLOCK>(__popcll(bnd), sScanD, &cnt);
+        (void)block_scan<BLOCK>(set_popc(bnd), sScanD, &cnt);
         cntb = cnt;
         if (cntb <= need)
           all_bin = true;
@@ -1168,8 +1180,8 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
     // boundary bins of levels 1..L-1
     auto for_bnd = [&](int L, auto&& f) {
 #pragma unroll 1
-      for (uint64_t m = bnd; m; m &= m - 1) {
-        const int k = __ffsll(static_cast<unsigned long long>(m)) - 1;
+      for (CandSet m = bnd; m; m &= m - 1) {
+        const int k = set_ffs(m);
         const int v = pos_v(k);
         const double sc = pos_score(k);
         bool in = true;
@@ -1230,8 +1242,8 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
     // the boundary bin's candidates: the deeper levels, then the exact rank on
     // (score desc, key asc)
 #pragma unroll 1
-    for (uint64_t m = bnd; m; m &= m - 1) {
-      const int k = __ffsll(static_cast<unsigned long long>(m)) - 1;
+    for (CandSet m = bnd; m; m &= m - 1) {
+      const int k = set_ffs(m);
       const int v = pos_v(k);
       const double sc = pos_score(k);
       bool take = true;
@@ -1249,17 +1261,17 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
         for (int u = 0; u < nbc; ++u) rank += ranks_before(sBScore[u], sBKey[u], sc, key);
         take = rank < need;
       }
-      if (take) sel_bits |= 1ull << (k == NC ? 0 : (k == NC + 1 ? NC + 1 : k + 1));
+      if (take) sel_bits |= CandSet{1} << (k == NC ? 0 : (k == NC + 1 ? NC + 1 : k + 1));
     }
     int nsel = 0;
-    int wpos = block_scan<BLOCK, false>(__popcll(sel_bits), sScanB, &nsel);
+    int wpos = block_scan<BLOCK, false>(set_popc(sel_bits), sScanB, &nsel);
     if (nsel > P.K) {  // cannot happen when the selection is exact; never write past K entries
       nsel = P.K;
       if (tid == 0) atomicOr(S.flags, kFlagSelect);
     }
 #pragma unroll 1
-    for (uint64_t m = sel_bits; m && wpos < nsel; m &= m - 1) {
-      const int bit = __ffsll(static_cast<unsigned long long>(m)) - 1;
+    for (CandSet m = sel_bits; m && wpos < nsel; m &= m - 1) {
+      const int bit = set_ffs(m);
       const uint32_t v = static_cast<uint32_t>(pos_v(bit == 0 ? NC : (bit == NC + 1 ? NC + 1 : bit - 1)));
       sSelSrc[wpos++] = static_cast<uint32_t>(hi_) | (v << 16);
     }
