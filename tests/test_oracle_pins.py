@@ -83,6 +83,39 @@ def test_brute_force_no_pruning(tiny, seed, omega):
     check_against_brute(res, expect)
 
 
+@pytest.mark.parametrize("seed", range(20))
+def test_brute_force_random_lexicons(seed):
+    """Random small lexicons over phonemes {1, 2, 3} (one to three phonemes a
+    word, so words that are prefixes of others and doubled phonemes occur;
+    distinct spellings plus one homophone pair), random bonuses and LM weight:
+    without pruning, the oracle's complete hypotheses, totals and readings
+    equal the exhaustive enumeration's."""
+    rng = np.random.default_rng(1000 + seed)
+    n = int(rng.integers(4, 8))  # (the tiny LM needs five words or more for its 60 n-grams)
+    words = []
+    while len(words) < n:
+        w = tuple(int(x) for x in rng.integers(1, 4, size=int(rng.integers(1, 4))))
+        if w not in words:
+            words.append(w)
+    words.append(words[int(rng.integers(0, n))])
+    lex = lexicon_from(words)
+    lm = random_small_lm(len(words), 60)
+    orc = oracle.Oracle(lex, lm)
+    try:
+        lg = tiny_logits(6, 50 + seed)
+        omega = float(rng.choice([0.0, 0.5, 1.0]))
+        p = DecodeParams(omega=omega, beta=float(rng.uniform(0.0, 2.0)), gamma=float(rng.uniform(0.0, 2.0)),
+                         fusion_interval=0)
+        res = orc.decode(lg, oracle.params_from(p, **BIG))
+        D = p.alpha * lg.astype(np.float64)
+        expect = bf.complete_hypotheses(D, TINY_CLASSES, words, p.beta, p.gamma,
+                                        ngram_reading_score(orc, lm, omega))
+        assert len(expect) > 1
+        check_against_brute(res, expect)
+    finally:
+        orc.close()
+
+
 @pytest.mark.parametrize("seed", [0, 1, 2])
 @pytest.mark.parametrize("omega", [0.0, 0.5])
 def test_brute_force_max_recombination(tiny, seed, omega):
