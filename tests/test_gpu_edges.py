@@ -11,7 +11,7 @@ import pytest
 import paper_2603_14002_amd as lbm
 from tests import test_oracle_pruning_pins as pins
 from tests.gpu_util import check_parity, gpu_decode, read_outputs, say
-from tests.tinylm import lexicon_from, lm_from_entries, peaked_logits
+from tests.tinylm import lexicon_from, lm_from_entries, peaked_logits, random_small_lm
 from workloads import DecodeParams, load_workload
 from workloads.gen import WorkloadData
 
@@ -344,6 +344,47 @@ def test_two_decoders_on_two_streams():
         for b, (got, want) in enumerate(zip(out, ref)):
             assert got[0] == want[0] and np.array_equal(got[1], want[1]), b
         r["dec"].close()
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_random_small_lexicons_match_oracle(seed):
+    """Random small lexicons over phonemes 1..5 (one to four phonemes a word,
+    so prefix words and doubled phonemes occur, plus two homophones), four
+    utterances spelled from them with blank runs, decoded with pruning (beam
+    8 or 32, two sub-beams, fusion every 4 frames): the oracle's outputs, at
+    the end of the utterance and live."""
+    rng = np.random.default_rng(500 + seed)
+    n = int(rng.integers(6, 12))
+    words = []
+    while len(words) < n:
+        w = tuple(int(x) for x in rng.integers(1, 6, size=int(rng.integers(1, 5))))
+        if w not in words:
+            words.append(w)
+    words += [words[int(rng.integers(0, n))], words[int(rng.integers(0, n))]]
+    lex = lexicon_from(words)
+    lm = random_small_lm(len(words), 80)
+    B, T = 4, 40
+    rows = []
+    for b in range(B):
+        seq = []
+        while len(seq) < T:
+            for ph in words[int(rng.integers(0, len(words)))]:
+                if seq and seq[-1] == ph:
+                    seq.append(0)  # a repeated phoneme needs a blank between
+                seq += [ph] * int(rng.integers(1, 3))
+            seq += [40] + [0] * int(rng.integers(0, 3))
+        rows.append(peaked_logits(seq[:T], strong=3.0, seed=seed * 10 + b, sigma=0.8))
+    lg = np.stack(rows)
+    lengths = np.array([T, T - 7, T, T - 13], np.int32)
+    beam = 8 if seed % 2 == 0 else 32
+    p = DecodeParams(beam=beam, subbeams=2, fusion_interval=4, fusion_top_f=0)
+    wl = load_workload("t-c1k").workload
+    wl = wl.__class__(**{**wl.__dict__, "params": p})
+    d = WorkloadData(wl, lex, lm, lg, lengths, np.zeros((B, T), np.int32), [[] for _ in range(B)], 11 + seed)
+    for fin in (True, False):
+        say(f"[case] random lexicon seed={seed} words={len(words)} K={beam} fin={fin}")
+        out = gpu_decode(d, params=p, finalize=fin)
+        check_parity(d, out, range(B), params=p, name=f"random-lexicon/{seed}", finalize=fin)
 
 
 def test_gather_probe_reads_the_lines_it_names():
