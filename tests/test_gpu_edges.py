@@ -346,13 +346,13 @@ def test_two_decoders_on_two_streams():
         r["dec"].close()
 
 
-@pytest.mark.parametrize("seed", range(6))
+@pytest.mark.parametrize("seed", range(8))
 def test_random_small_lexicons_match_oracle(seed):
     """Random small lexicons over phonemes 1..5 (one to four phonemes a word,
     so prefix words and doubled phonemes occur, plus two homophones), four
     utterances spelled from them with blank runs, decoded with pruning (beam
-    8 or 32, two sub-beams, fusion every 4 frames): the oracle's outputs, at
-    the end of the utterance and live."""
+    8, 32, 64 or 256, two sub-beams, fusion every 4 frames): the oracle's
+    outputs, at the end of the utterance and live."""
     rng = np.random.default_rng(500 + seed)
     n = int(rng.integers(6, 12))
     words = []
@@ -376,7 +376,7 @@ def test_random_small_lexicons_match_oracle(seed):
         rows.append(peaked_logits(seq[:T], strong=3.0, seed=seed * 10 + b, sigma=0.8))
     lg = np.stack(rows)
     lengths = np.array([T, T - 7, T, T - 13], np.int32)
-    beam = 8 if seed % 2 == 0 else 32
+    beam = (8, 32, 64, 256)[seed % 4]
     p = DecodeParams(beam=beam, subbeams=2, fusion_interval=4, fusion_top_f=0)
     wl = load_workload("t-c1k").workload
     wl = wl.__class__(**{**wl.__dict__, "params": p})
