@@ -1910,17 +1910,111 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
       uint64_t* ky = reinterpret_cast<uint64_t*>(sSel + 8 * KMAX);
       uint32_t* ix = reinterpret_cast<uint32_t*>(sSel + 16 * KMAX);
       const int F = (P.fusion_top_f <= 0 || P.fusion_top_f >= n) ? n : P.fusion_top_f;
+      const uint32_t* sel = ix;  // the selected hypotheses (any order: each is fused on its own)
       if (F < n) {
-        if (tid < KMAX) {
-          sc[tid] = tid < n ? N.pt[tid] + N.Lw[tid * kMaxSub] : kNegInf;
-          ky[tid] = tid < n ? N.key[tid] : ~0ull;
-          ix[tid] = tid < n ? static_cast<uint32_t>(tid) : 0u;
+        if constexpr (KMAX >= 128) {
+          // the top F as a set, from a histogram of the totals (a sort of K =
+          // 256 totals takes 36 barrier-separated stages): bins of (hi -
+          // total) over [lo, hi], monotone; the bin holding the F-th found by
+          // one wavefront; the bins above it taken whole, and its members
+          // ranked exactly among themselves by (total desc, key asc; the
+          // index for exact ties, which distinct prefixes do not have)
+          uint32_t* const fH = reinterpret_cast<uint32_t*>(sSel);
+          double* const fT = reinterpret_cast<double*>(sSel + 4 * kBins);
+          uint64_t* const fK = reinterpret_cast<uint64_t*>(sSel + 4 * kBins + 8 * KMAX);
+          uint32_t* const fI = reinterpret_cast<uint32_t*>(sSel + 4 * kBins + 16 * KMAX);
+          uint32_t* const fSel = fI + KMAX;
+          static_assert(4 * kBins + 24 * KMAX <= UNI_BYTES, "top-F scratch");
+          for (int d = tid; d < kBins; d += BLOCK) fH[d] = 0;
+          if (tid == 0) {
+            sBCount = 0;
+            sAthr = 0;
+          }
+          const bool own = tid < n;
+          double tot = kNegInf;
+          uint64_t key = ~0ull;
+          if (own) {
+            tot = N.pt[tid] + N.Lw[tid * kMaxSub];
+            key = N.key[tid];
+          }
+          double hi, lo;
+          block_minmax<BLOCK>(own ? tot : kNegInf, own ? tot : HUGE_VAL, sRed, &hi, &lo);
+          const double inv = hi > lo ? static_cast<double>(kBins) / (hi - lo) : 0.0;
+          int bin = -1;
+          if (own) {
+            const double x = (hi - tot) * inv;
+            bin = x < static_cast<double>(kBins - 1) ? static_cast<int>(x) : kBins - 1;  // NaN: a total of -inf
+            atomicAdd(&fH[bin], 1u);
+          }
+          lds_barrier();
+          if (wave == 0) {
+            constexpr int PERW = kBins / 64;
+            int h[PERW];
+            const uint4* hp = reinterpret_cast<const uint4*>(fH + lane * PERW);
+#pragma unroll
+            for (int q = 0; q < PERW / 4; ++q) {
+              const uint4 x4 = hp[q];
+              h[4 * q] = static_cast<int>(x4.x);
+              h[4 * q + 1] = static_cast<int>(x4.y);
+              h[4 * q + 2] = static_cast<int>(x4.z);
+              h[4 * q + 3] = static_cast<int>(x4.w);
+            }
+            int local = 0;
+#pragma unroll
+            for (int q = 0; q < PERW; ++q) local += h[q];
+            const int incl = wave_scan_incl(local);
+            const int before = incl - local;
+            if (before < F && incl >= F) {
+              int acc = before;
+              bool found = false;
+#pragma unroll
+              for (int q = 0; q < PERW; ++q) {
+                if (!found && acc + h[q] >= F) {
+                  sBucket = lane * PERW + q;
+                  sAbove = acc;
+                  found = true;
+                }
+                acc += h[q];
+              }
+            }
+          }
+          lds_barrier();
+          const int fb = sBucket, fa = sAbove;
+          if (own && bin < fb) fSel[atomicAdd(&sAthr, 1)] = static_cast<uint32_t>(tid);  // positions 0..fa-1
+          if (own && bin == fb) {
+            const int m = atomicAdd(&sBCount, 1);
+            fT[m] = tot;
+            fK[m] = key;
+            fI[m] = static_cast<uint32_t>(tid);
+          }
+          lds_barrier();
+          const int nbm = sBCount;
+          for (int m = tid; m < nbm; m += BLOCK) {
+            const double tm = fT[m];
+            const uint64_t km = fK[m];
+            const uint32_t im = fI[m];
+            int r = 0;
+            for (int u = 0; u < nbm; ++u) {
+              const double tu = fT[u];
+              const uint64_t ku = fK[u];
+              r += (tu > tm || (tu == tm && (ku < km || (ku == km && fI[u] < im)))) ? 1 : 0;
+            }
+            if (r < F - fa) fSel[fa + r] = im;
+          }
+          lds_barrier();
+          sel = fSel;
+        } else {
+          if (tid < KMAX) {
+            sc[tid] = tid < n ? N.pt[tid] + N.Lw[tid * kMaxSub] : kNegInf;
+            ky[tid] = tid < n ? N.key[tid] : ~0ull;
+            ix[tid] = tid < n ? static_cast<uint32_t>(tid) : 0u;
+          }
+          lds_barrier();
+          bitonic_sort<KMAX>(sc, ky, ix);
         }
-        lds_barrier();
-        bitonic_sort<KMAX>(sc, ky, ix);
       }
       if (tid < F) {
-        const int i = F < n ? static_cast<int>(ix[tid]) : tid;
+        const int i = F < n ? static_cast<int>(sel[tid]) : tid;
         const int nsub = (N.meta[i] >> 8) & 0xFF;
         double L[kMaxSub];
         uint32_t h[kMaxSub];

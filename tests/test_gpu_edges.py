@@ -351,7 +351,8 @@ def test_random_small_lexicons_match_oracle(seed):
     """Random small lexicons over phonemes 1..5 (one to four phonemes a word,
     so prefix words and doubled phonemes occur, plus two homophones), four
     utterances spelled from them with blank runs, decoded with pruning (beam
-    8, 32, 64 or 256, two sub-beams, fusion every 4 frames): the oracle's
+    8, 32, 64 or 256, two sub-beams, fusion every 4 frames, of all hypotheses
+    for seeds 0..3 and of the best third for seeds 4..7): the oracle's
     outputs, at the end of the utterance and live."""
     rng = np.random.default_rng(500 + seed)
     n = int(rng.integers(6, 12))
@@ -377,12 +378,12 @@ def test_random_small_lexicons_match_oracle(seed):
     lg = np.stack(rows)
     lengths = np.array([T, T - 7, T, T - 13], np.int32)
     beam = (8, 32, 64, 256)[seed % 4]
-    p = DecodeParams(beam=beam, subbeams=2, fusion_interval=4, fusion_top_f=0)
+    p = DecodeParams(beam=beam, subbeams=2, fusion_interval=4, fusion_top_f=0 if seed < 4 else beam // 3)
     wl = load_workload("t-c1k").workload
     wl = wl.__class__(**{**wl.__dict__, "params": p})
     d = WorkloadData(wl, lex, lm, lg, lengths, np.zeros((B, T), np.int32), [[] for _ in range(B)], 11 + seed)
     for fin in (True, False):
-        say(f"[case] random lexicon seed={seed} words={len(words)} K={beam} fin={fin}")
+        say(f"[case] random lexicon seed={seed} words={len(words)} K={beam} F={p.fusion_top_f} fin={fin}")
         out = gpu_decode(d, params=p, finalize=fin)
         check_parity(d, out, range(B), params=p, name=f"random-lexicon/{seed}", finalize=fin)
 
