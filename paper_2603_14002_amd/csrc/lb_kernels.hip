@@ -644,7 +644,7 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
   __shared__ uint32_t sEvBeam[KMAX], sEvWoff[KMAX], sEvH[KMAX];
   __shared__ int32_t sNG, sHeavy, sNLarge;
   __shared__ int32_t sLarge[KMAX];  // completed words ranked by a whole wavefront
-  __shared__ double sRed[2 * NW], sRedB[2 * NW];
+  __shared__ double sRed[2 * NW], sRedB[3 * NW];
   __shared__ int32_t sScan[NW], sScanB[NW], sScanC[NW], sScanD[NW];
   __shared__ int32_t sBucket, sAbove, sBucketCnt, sBCount, sAthr, sNBinned;
   // counters: probed lines, completed words, LM queries, index lines (summed over
@@ -847,13 +847,16 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
       if constexpr (kOnePass) up = ((C.pt[tid] + sDmax) + fmax(P.beta, P.gamma)) + C.Lw[tid * kMaxSub];
     }
     if constexpr (kOnePass) {
-      // per wavefront: an upper bound of every candidate (sRedB[w]) and the best
-      // stay (sRedB[NW + w]), for the top-K's bin range
+      // per wavefront: an upper bound of every candidate (sRedB[w]), the best
+      // stay (sRedB[NW + w]) and the lowest (sRedB[2 NW + w]), for the top-K's
+      // bin range
       double hi = fmax(st, up), nlo = -st;
       wave_minmax(&hi, &nlo);
+      const double nmin = wave_max(tid < n ? -st : -HUGE_VAL);
       if (lane == 0) {
         sRedB[wave] = hi;
         sRedB[NW + wave] = -nlo;
+        sRedB[2 * NW + wave] = -nmin;
       }
     }
     lds_barrier();
@@ -918,32 +921,39 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
 
     // ---- top-K and the theta cut.  Level 0 bins the candidates at or above L0
     // by (U - score) over [L0, U] into kBins, where U is at least every
-    // candidate's score and L0 at most the cut (best - theta); the map is
-    // monotone, so bins above the one holding the K-th candidate are taken
-    // whole, and the bins above the cut's bin hold only candidates above the
-    // cut.  U and L0 come from the recombination phase's bounds (U: the stays
-    // and each hypothesis' extension bound; L0: the best stay - theta), so one
-    // pass over the slots bins them; the exact best is taken only where the
-    // cut might bind (below), and then the members of the cut's bin are tested
-    // against the cut exactly.  Without a finite stay (and in the instances
-    // without bounds) a first pass finds best and the lowest candidate: U =
-    // best, L0 = max(best - theta, lowest).  The bin holding the K-th candidate is
-    // resolved exactly by rank on (score desc, key asc) when it holds at most
-    // kBoundaryCap candidates; otherwise it is re-binned over its own score
-    // range (deeper levels), and when its scores are all equal, by the bits of
-    // the key (smaller key first).
+    // candidate's score and L0 at most every candidate that can be selected:
+    // at most the cut (best - theta) or at most the K-th candidate (with a
+    // full beam the K stays are candidates, so the K-th candidate scores at
+    // least the lowest stay).  The map is monotone, so bins above the one
+    // holding the K-th candidate are taken whole, and the bins above the
+    // cut's bin hold only candidates above the cut.  U and L0 come from the
+    // recombination phase's bounds (U: the stays and each hypothesis'
+    // extension bound; L0: the best stay - theta, or the lowest stay if the
+    // beam is full and that is higher), so one pass over the slots bins them;
+    // the exact best is taken only where the cut might bind (below), and then
+    // the members of the cut's bin are tested against the cut exactly.
+    // Without a finite stay (and in the instances without bounds) a first
+    // pass finds best and the lowest candidate: U = best, L0 = max(best -
+    // theta, lowest).  The bin holding the
+    // K-th candidate is resolved exactly by rank on (score desc, key asc) when
+    // it holds at most kBoundaryCap candidates; otherwise it is re-binned over
+    // its own score range (deeper levels), and when its scores are all equal,
+    // by the bits of the key (smaller key first).
     const double theta = P.theta;
-    double U = kNegInf, Bst = kNegInf;
+    double U = kNegInf, Bst = kNegInf, Smin = kNegInf;
     if constexpr (kOnePass) {
       U = sRedB[0];
       Bst = sRedB[NW];
+      Smin = sRedB[2 * NW];
 #pragma unroll
       for (int w = 1; w < NW; ++w) {
         U = fmax(U, sRedB[w]);
         Bst = fmax(Bst, sRedB[NW + w]);
+        Smin = fmin(Smin, sRedB[2 * NW + w]);
       }
     }
     double L0 = Bst - theta;
+    if (n >= P.K) L0 = fmax(L0, Smin);  // (a stay of -inf leaves Smin at -inf)
     // with a first pass the best is exact before the binning (and every binned
     // candidate is at or above the cut)
     const bool first_pass = Bst == kNegInf;  // no bounds, or no finite stay (uniform)
