@@ -614,7 +614,7 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
   constexpr int NPL = NPM < 256 ? NPM : 256;  // pairs grouped at once
   constexpr int NEB = NPL / kMaxSub;          // completed words per batch
   constexpr int SEL_BYTES = kBins * 4 + kBoundaryCap * 16;
-  constexpr int LM_BYTES = 56 * NPL + 16;
+  constexpr int LM_BYTES = 64 * NPL + 16;
   constexpr int UNI_BYTES = SEL_BYTES > LM_BYTES ? SEL_BYTES : LM_BYTES;
   static_assert(20 * KMAX <= SEL_BYTES, "fusion sort scratch");
   const int b = blockIdx.x;
@@ -1410,6 +1410,9 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
     Ctx* const sGctx = reinterpret_cast<Ctx*>(sGH + NPL);             // 24 B each
     int32_t* const sGoff = reinterpret_cast<int32_t*>(sGctx + NPL);  // NPL + 1 entries
     uint32_t* const sGcnt = reinterpret_cast<uint32_t*>(sGoff + NPL + 1);  // lookups | kGroupHeavy
+    // heavy groups: bit (h mod 64) set for each homophone h of the explicit list
+    uint64_t* const sGmask = reinterpret_cast<uint64_t*>(sSel + ((4 * (56 * NPL / 4 + 1) + 7) & ~7));
+    static_assert(((4 * (56 * NPL / 4 + 1) + 7) & ~7) + 8 * NPL <= UNI_BYTES, "grouping tables fit the shared scratch");
 #pragma unroll 1
     for (int e0 = 0; e0 < nev; e0 += NEB) {
     const int nb = nev - e0 < NEB ? nev - e0 : NEB;
@@ -1460,9 +1463,10 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
       if (q >= 0) sPairG[pr] = sGId[q];
     }
     // heavy groups (nodes with many homophones): the homophones with an explicit
-    // n-gram for the group's context, from the continuation index; the others
-    // back off to their unigrams and are not looked up.  A group with more than
-    // kMaxExplicit of them is looked up in full.
+    // n-gram for the group's context, from the continuation index (each once: a
+    // homophone can be listed for several context orders); the others back off
+    // to their unigrams and are not looked up.  A group with more than
+    // kMaxExplicit listed is looked up in full.
     const bool heavy_frame = sHeavy != 0;
     for (int g = tid; g < NG; g += BLOCK) {
       const uint32_t Hg = sGH[g];
@@ -1472,17 +1476,31 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
         pres_lookup(S, sGctx[g], sGwoff[g], hit, &plines);
         const uint32_t ne = hit[0].n + hit[1].n + hit[2].n;
         if (ne <= static_cast<uint32_t>(kMaxExplicit)) {
-          uint32_t* E = scrE + static_cast<size_t>(g) * kMaxExplicit;
+          uint32_t* const E = scrE + static_cast<size_t>(g) * kMaxExplicit;
+          uint64_t bm = 0;
+          uint32_t nd = 0;
+          // (the list is read back only when the mask bit is already set)
+          auto add = [&](uint32_t x) {
+            const uint64_t bit = 1ull << (x & 63u);
+            bool seen = false;
+            if (bm & bit)
+              for (uint32_t m = 0; m < nd; ++m) seen |= E[m] == x;
+            if (!seen) {
+              E[nd++] = x;
+              bm |= bit;
+            }
+          };
 #pragma unroll
           for (int o3 = 0; o3 < 3; ++o3) {
             if (hit[o3].n == 1) {
-              *E++ = hit[o3].a;
+              add(hit[o3].a);
             } else {
               const uint32_t* lst = (o3 == 0 ? S.p2.lists : (o3 == 1 ? S.p3.lists : S.p4.lists)) + hit[o3].a;
-              for (uint32_t m = 0; m < hit[o3].n; ++m) *E++ = lst[m];
+              for (uint32_t m = 0; m < hit[o3].n; ++m) add(lst[m]);
             }
           }
-          cnt = ne | kGroupHeavy;
+          cnt = nd | kGroupHeavy;
+          sGmask[g] = bm;
         }
       }
       sGcnt[g] = cnt;
@@ -1518,12 +1536,16 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
     }
     if (tid == 0) sCnt[6] += static_cast<unsigned long long>(U);
     // the results go to LDS when they fit in the grouping keys freed above (the
-    // usual case), else to the stream's scratch in global memory
+    // usual case), else to the stream's scratch in global memory; the log-probs,
+    // read for every candidate (the states only for the kept ones), stay in
+    // LDS up to four times as many lookups, the states then in the scratch
     constexpr int kLdsRes = 12 * NPL / 32;
+    constexpr int kLdsLp = 12 * NPL / 8;
     double* const sResL = reinterpret_cast<double*>(sSel);
-    QState* const sResS = reinterpret_cast<QState*>(sSel + 8 * kLdsRes);
+    QState* const sResS = reinterpret_cast<QState*>(sSel + 8 * kLdsRes);  // (only when U <= kLdsRes)
     const bool res_lds = U <= kLdsRes;
-    auto res_lp = [&](int u) -> double { return res_lds ? sResL[u] : scrL[u]; };
+    const bool lp_lds = U <= kLdsLp;
+    auto res_lp = [&](int u) -> double { return lp_lds ? sResL[u] : scrL[u]; };
     auto res_st = [&](int u) -> QState { return res_lds ? sResS[u] : scrS[u]; };
     lds_barrier();
     mark(kPhGroup);
@@ -1537,13 +1559,14 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
       const uint32_t h = (sGcnt[lo] & kGroupHeavy) ? scrE[static_cast<size_t>(lo) * kMaxExplicit + k] : k;
       const int32_t w = S.trie_words[sGwoff[lo] + h];
       const LmResult res = lm_lookup(S, w, sGctx[lo], &lines);
-      if (res_lds) {
+      if (lp_lds)
         sResL[u] = res.lp;
-        sResS[u] = res.st;
-      } else {
+      else
         scrL[u] = res.lp;
+      if (res_lds)
+        sResS[u] = res.st;
+      else
         scrS[u] = res.st;
-      }
     }
     if (res_lds)
       lds_barrier();
@@ -1662,12 +1685,8 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
               any_heavy = true;
               const uint32_t* E = scrE + static_cast<size_t>(g) * kMaxExplicit;
               const int ne = static_cast<int>(cnt & ~kGroupHeavy);
-              for (int m = 0; m < ne; ++m) {
-                const uint32_t hm = E[m];
-                bool dup = false;
-                for (int m2 = 0; m2 < m; ++m2) dup |= E[m2] == hm;
-                if (!dup) insert(Lw + P.comega * res_lp(off + m), j * H + static_cast<int>(hm), off + m);
-              }
+              for (int m = 0; m < ne; ++m)
+                insert(Lw + P.comega * res_lp(off + m), j * H + static_cast<int>(E[m]), off + m);
             }
           }
         }
@@ -1699,10 +1718,12 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
                   const double L = N.Lw[rr * kMaxSub + j] + P.comega * lp;
                   if (nw[j] < O || !(Lth[j] > L)) {
                     need = true;
-                    const uint32_t* E = scrE + static_cast<size_t>(g) * kMaxExplicit;
-                    const int ne = static_cast<int>(cnt & ~kGroupHeavy);
                     bool member = false;
-                    for (int m = 0; m < ne; ++m) member |= E[m] == wr.h;
+                    if ((sGmask[g] >> (wr.h & 63u)) & 1ull) {
+                      const uint32_t* E = scrE + static_cast<size_t>(g) * kMaxExplicit;
+                      const int ne = static_cast<int>(cnt & ~kGroupHeavy);
+                      for (int m = 0; m < ne; ++m) member |= E[m] == wr.h;
+                    }
                     if (!member) {
                       insert(L, j * H + static_cast<int>(wr.h), -1 - k);
                       nw[j] += 1;
@@ -1792,8 +1813,8 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
         }
       }
       if (any_heavy) {
-        // heavy groups: lane m holds the m-th explicit homophone; its first
-        // occurrence is a candidate with its looked-up score
+        // heavy groups: lane m holds the m-th explicit homophone (the list has
+        // no repeats), a candidate with its looked-up score
         uint32_t eh[kMaxSub];
         int ne[kMaxSub];
 #pragma unroll
@@ -1805,12 +1826,7 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
 #pragma unroll
         for (int j = 0; j < kMaxSub; ++j) {
           if (ne[j] > 0) {
-            bool dup = false;
-            for (int m = 0; m < ne[j]; ++m) {
-              const uint32_t x = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(eh[j]), m));
-              dup |= m < lane && x == eh[j];
-            }
-            if (lane < ne[j] && !dup)
+            if (lane < ne[j])
               insert(Lw[j] + P.comega * res_lp(goff[j] + lane), j * static_cast<int>(H) + static_cast<int>(eh[j]),
                      goff[j] + lane);
           }
