@@ -2415,7 +2415,31 @@ __device__ __forceinline__ void emit_output(const DevParams& P, const DevState& 
   }
   int m = 0;
   (void)block_scan<NT>(ok ? 1 : 0, sScan, &m);
-  bitonic_sort<N>(sc, ky, ix);
+  if constexpr (N <= 64) {
+    // up to 64 entries: each one's position is the number of entries before
+    // it in (score desc, key asc, index asc), counted by one wavefront (two
+    // barriers instead of the sort's stages)
+    double si = kNegInf;
+    uint64_t ki = ~0ull;
+    int rk = 0;
+    if (tid < N) {
+      si = sc[tid];
+      ki = ky[tid];
+      for (int j = 0; j < N; ++j) {
+        const double sj = sc[j];
+        const uint64_t kj = ky[j];
+        rk += (ranks_before(sj, kj, si, ki) || (sj == si && kj == ki && j < tid)) ? 1 : 0;
+      }
+    }
+    __syncthreads();
+    if (tid < N) {
+      sc[rk] = si;
+      ky[rk] = ki;
+      ix[rk] = static_cast<uint32_t>(tid);
+    }
+  } else {
+    bitonic_sort<N>(sc, ky, ix);
+  }
   if (tid == 0) {
     // the stream's frame counter advances by the frames decoded in this call:
     // a length outside 0..Tc is clamped (the decode did the same) and flagged
