@@ -2029,6 +2029,23 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
           }
           lds_barrier();
           sel = fSel;
+        } else if constexpr (WPE == 1) {
+          // the top F as a set by rank counting: the LPB lanes of each
+          // hypothesis count, a share each, the hypotheses ranking before it
+          // (total desc, key asc; the keys are distinct), and one lane places
+          // it; one barrier (in the instances with registers to spare: in the
+          // 128-register ones it costs a spill)
+          const int hf = tid / LPB, lf = tid - hf * LPB;
+          int cnt = 0;
+          if (hf < n) {
+            const double ti = N.pt[hf] + N.Lw[hf * kMaxSub];
+            const uint64_t ki = N.key[hf];
+            for (int j = lf; j < n; j += LPB) cnt += ranks_before(N.pt[j] + N.Lw[j * kMaxSub], N.key[j], ti, ki) ? 1 : 0;
+          }
+#pragma unroll
+          for (int o = 1; o < LPB; o <<= 1) cnt += __shfl_xor(cnt, o, 64);
+          if (hf < n && lf == 0 && cnt < F) ix[cnt] = static_cast<uint32_t>(hf);
+          lds_barrier();
         } else {
           if (tid < KMAX) {
             sc[tid] = tid < n ? N.pt[tid] + N.Lw[tid * kMaxSub] : kNegInf;
