@@ -603,9 +603,9 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
   constexpr int NW = BLOCK / 64;
   constexpr int NC = (kSep + LPB - 1) / LPB;  // extension slots per lane
   // top-K in one pass over the slots, with the bin range from bounds taken in
-  // the recombination phase, where a lane owns 10 or more slots; with fewer
+  // the recombination phase, where a lane owns 5 or more slots; with fewer
   // slots per lane a first pass for the exact range costs less than the bounds
-  constexpr bool kOnePass = NC >= 10;
+  constexpr bool kOnePass = NC >= 5;
   static_assert(LPB <= 16 && LPB * NC < 64, "a lane's slots stay below symbol 64");
   static_assert(NC + 2 < 64, "a lane's candidates (its slots, the stay and the repeat) fit the sets sel_bits and bnd");
   // the candidate sets of a lane: 32 bits where its positions fit
