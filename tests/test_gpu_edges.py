@@ -184,6 +184,58 @@ def test_lengths_outside_range_are_clamped_and_reported():
     np.testing.assert_array_equal(bad[1], ok[1])
 
 
+def test_rejected_decode_calls_leave_the_decoder_usable():
+    """A decode call with no stream (batch 0), more streams than max_batch, a
+    negative frame count, an unknown flag or a null device pointer returns
+    LB_ERR_INVALID_ARG before anything runs; the streams' state is untouched,
+    so a valid call afterwards gives what a fresh decoder gives."""
+    import torch
+    d = load_workload("t-c1k")
+    p = d.workload.params
+    B, T = d.logits.shape[:2]
+    dev = torch.device("cuda:0")
+    logits = torch.from_numpy(d.logits).to(dev)
+    lengths = torch.from_numpy(d.lengths.astype(np.int32)).to(dev)
+    half = T // 2
+
+    def run(bad_calls):
+        lp = lbm.make_params(p, max_batch=B, max_frames=T, fusion_seed=d.fusion_seed)
+        dec = lbm.Decoder(d.lexicon, d.lm, lp)
+        K, W = lp.beam, lp.max_words_out
+        H = torch.empty((B, K, W), dtype=torch.int32, device=dev)
+        S = torch.empty((B, K), dtype=torch.float32, device=dev)
+        first = torch.clamp(lengths, max=half).contiguous()
+        rest = torch.clamp(lengths - half, min=0).contiguous()
+        lbm.lb_decode_batch(dec.handle, logits[:, :half].contiguous(), first, B, half, lbm.LB_BEGIN, None, H, S)
+        for args in bad_calls:
+            with pytest.raises(lbm.LBError) as err:
+                lbm.lb_decode_batch(dec.handle, *args(H, S))
+            assert err.value.status == lbm.LB_ERR_INVALID_ARG, err.value
+        lbm.lb_decode_batch(dec.handle, logits[:, half:].contiguous(), rest, B, T - half, lbm.LB_END, None, H, S)
+        torch.cuda.synchronize()
+        st = dec.status()
+        out = (H.cpu().numpy(), S.cpu().numpy())
+        dec.close()
+        return st, out
+
+    lg2 = logits[:, half:].contiguous()
+    rest = torch.clamp(lengths - half, min=0).contiguous()
+    bad = [
+        lambda H, S: (lg2, rest, 0, T - half, lbm.LB_END, None, H, S),
+        lambda H, S: (lg2, rest, B + 1, T - half, lbm.LB_END, None, H, S),
+        lambda H, S: (lg2, rest, B, -1, lbm.LB_END, None, H, S),
+        lambda H, S: (lg2, rest, B, T - half, lbm.LB_END | 4, None, H, S),
+        lambda H, S: (lg2, None, B, T - half, lbm.LB_END, None, H, S),
+        lambda H, S: (None, rest, B, T - half, lbm.LB_END, None, H, S),
+    ]
+    say("[case] rejected decode calls")
+    st_bad, out_bad = run(bad)
+    st_ok, out_ok = run([])
+    assert st_bad == lbm.LB_OK and st_ok == lbm.LB_OK
+    np.testing.assert_array_equal(out_bad[0], out_ok[0])
+    np.testing.assert_array_equal(out_bad[1], out_ok[1])
+
+
 # ------------------------------------------------------------------ load factor 0.9, wrapping probe chains
 
 @pytest.mark.parametrize("name", ["c1", "t-c20k"])
