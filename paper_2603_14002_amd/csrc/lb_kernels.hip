@@ -934,11 +934,11 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
     // the members of the cut's bin are tested against the cut exactly.
     // Without a finite stay (and in the instances without bounds) a first
     // pass finds best and the lowest candidate: U = best, L0 = max(best -
-    // theta, lowest).  The bin holding the
-    // K-th candidate is resolved exactly by rank on (score desc, key asc) when
-    // it holds at most kBoundaryCap candidates; otherwise it is re-binned over
-    // its own score range (deeper levels), and when its scores are all equal,
-    // by the bits of the key (smaller key first).
+    // theta, lowest).  The bin holding the K-th candidate is resolved exactly
+    // by rank on (score desc, key asc) when it holds at most kBoundaryCap
+    // candidates; otherwise it is re-binned over its own score range (deeper
+    // levels), and when its scores are all equal, by the bits of the key
+    // (smaller key first).
     const double theta = P.theta;
     double U = kNegInf, Bst = kNegInf, Smin = kNegInf;
     if constexpr (kOnePass) {
@@ -1410,9 +1410,12 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
     Ctx* const sGctx = reinterpret_cast<Ctx*>(sGH + NPL);             // 24 B each
     int32_t* const sGoff = reinterpret_cast<int32_t*>(sGctx + NPL);  // NPL + 1 entries
     uint32_t* const sGcnt = reinterpret_cast<uint32_t*>(sGoff + NPL + 1);  // lookups | kGroupHeavy
-    // heavy groups: bit (h mod 64) set for each homophone h of the explicit list
-    uint64_t* const sGmask = reinterpret_cast<uint64_t*>(sSel + ((4 * (56 * NPL / 4 + 1) + 7) & ~7));
-    static_assert(((4 * (56 * NPL / 4 + 1) + 7) & ~7) + 8 * NPL <= UNI_BYTES, "grouping tables fit the shared scratch");
+    // heavy groups: bit (h mod 64) set for each homophone h of the explicit
+    // list; past sGcnt (which ends 56 NPL + 4 bytes in), 8-B aligned
+    constexpr int kGmaskOff = (56 * NPL + 4 + 7) & ~7;
+    uint64_t* const sGmask = reinterpret_cast<uint64_t*>(sSel + kGmaskOff);
+    static_assert(kGmaskOff + 8 * NPL <= UNI_BYTES, "grouping tables fit the shared scratch");
+    static_assert(sizeof(Ctx) == 24, "group contexts are 24 B each");
 #pragma unroll 1
     for (int e0 = 0; e0 < nev; e0 += NEB) {
     const int nb = nev - e0 < NEB ? nev - e0 : NEB;
