@@ -210,33 +210,36 @@ def test_heavy_walk_edges(case):
             assert wa == wb and np.array_equal(sa, sb)
 
 
+@pytest.mark.parametrize("top_f", [0, 100], ids=["fuse-all", "fuse-100"])
 @pytest.mark.parametrize("sigma", [0.0, 1e-3], ids=["exact-ties", "clustered"])
-def test_crowded_boundary_bins(sigma):
+def test_crowded_boundary_bins(sigma, top_f):
     """Uniform (or nearly uniform) log-probs make thousands of candidates share
     the boundary score bin: exact ties are ordered by key bits, clustered
     scores by refined score bins; both must match the oracle, in the beam-256
     kernel for small batches and, for a tiled batch of 300, in the one for
-    batches beyond the CU count."""
+    batches beyond the CU count.  With 100 of the 256 hypotheses fused, the
+    fusion's selection meets the same ties (its boundary bin ranked by total,
+    then key)."""
     base = load_workload("t-k256")
     rng = np.random.default_rng(11)
     B, T = 2, 7
     raw = sigma * rng.standard_normal((B, T, 41))
     lg = (raw - np.log(np.exp(raw).sum(-1, keepdims=True))).astype(np.float32)
-    p = DecodeParams(beam=256, subbeams=3, fusion_interval=3, fusion_top_f=0)
+    p = DecodeParams(beam=256, subbeams=3, fusion_interval=3, fusion_top_f=top_f)
     wl = base.workload.__class__(**{**base.workload.__dict__, "params": p})
     d = WorkloadData(wl, base.lexicon, base.lm, lg, np.full(B, T, np.int32), np.zeros((B, T), np.int32),
                      [[], []], base.fusion_seed)
-    say(f"[case] crowded bins sigma={sigma}")
+    say(f"[case] crowded bins sigma={sigma} F={top_f}")
     big = 300  # more streams than CUs: the other beam-256 kernel
     tile = lambda a: np.concatenate([a] * (big // B))
     db = WorkloadData(wl, base.lexicon, base.lm, tile(lg), np.full(big, T, np.int32), np.zeros((big, T), np.int32),
                       [[]] * big, base.fusion_seed)
     for fin in (False, True):
         out = gpu_decode(d, params=p, finalize=fin)
-        par = check_parity(d, out, range(B), params=p, name=f"crowded/{sigma}", finalize=fin)
+        par = check_parity(d, out, range(B), params=p, name=f"crowded/{sigma}/{top_f}", finalize=fin)
         if not fin:
             assert par.n_hyps == B * 256
-        say(f"[case] crowded bins sigma={sigma} B={big} fin={fin}")
+        say(f"[case] crowded bins sigma={sigma} F={top_f} B={big} fin={fin}")
         outb = gpu_decode(db, params=p, finalize=fin)
         for b in range(big):
             assert outb[b][0] == out[b % B][0] and np.array_equal(outb[b][1], out[b % B][1]), b
