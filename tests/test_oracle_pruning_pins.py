@@ -216,6 +216,46 @@ def test_fusion_top_f_fuses_hypotheses_not_subbeams():
                                   -0.25 + 1.2 * bg(seed, bos, 2)]
 
 
+def test_fused_subbeams_survive_a_merge_with_an_unfused_parent():
+    """Fusion (Sec. 3.4.2) and recombination (App. E.1) over several frames: a
+    hypothesis fused at a fusion frame keeps its fused sub-beams when, a frame
+    later, the extension of an unfused hypothesis (its parent prefix) merges
+    into it: the merged entry takes its word-level state from its own stay,
+    not from the extension."""
+    lex = lexicon_from([(1,), (2,)])
+    W, bos = 2, 2
+    orc = oracle.Oracle(lex, unigram_lm(W, [(-1.0, 0.0)] * W))
+    # seed ^ (<s> << 32 | w0) = 1: Bg(<s>, w0) from splitmix64(1) >> 48 = 0x910A
+    seed = (bos << 32) | 1
+    B0 = bg(seed, bos, 0)
+    assert B0 == -4.6176910400390625
+    # frame 0: (1) = -0.5 + beta 0.5 = 0
+    # frame 1: (1 40) = 0 + 0 + gamma 0.25 = 0.25, word w0 (omega = 0: Lw = 0)
+    # frame 2: Z = (1 40) by its blank, 0.25 - 1 = -0.75; X = (1 40 2) = 0.25 -
+    #          0.5 + 0.5 = 0.25.  Fusion (t = 2, I = 2) on the top F = 1: X
+    #          alone, Lw(X) = 1.2 B0; Z keeps Lw = 0.
+    # frame 3: X: blank-ending 0.25 - 1 = -0.75; non-blank-ending LSE(its repeat
+    #          0.25 - 0.5 = -0.25, Z's extension by 2: -0.75 - 0.5 + 0.5 =
+    #          -0.75), with X's own (fused) sub-beam; Z: -0.75 - 1 = -1.75.
+    lg = frames({1: -0.5}, {40: 0.0}, {0: -1.0, 2: -0.5}, {0: -1.0, 2: -0.5})
+
+    def lse(a, b):
+        return max(a, b) + math.log1p(math.exp(-abs(a - b)))
+
+    ax = lse(-0.75, lse(-0.25, -0.75))
+    res = run(orc, lg, fusion_interval=2, fusion_top_f=1, fusion_seed=seed)
+    # Z (-1.75) now ranks before X (ax + 1.2 B0 = -4.999); with the extension's
+    # sub-beam X would lead at ax = 0.543
+    assert labels(res) == [(1, 40), (1, 40, 2)]
+    np.testing.assert_allclose(res.total, [-1.75, ax + 1.2 * B0], rtol=0, atol=1e-12)
+    assert res.subs[0] == [(0.0, [0])]
+    assert res.subs[1] == [(1.2 * B0, [0])]
+    # after frame 2: X, which led before the fusion, is the fused one
+    r2 = run(orc, lg[:3], fusion_interval=2, fusion_top_f=1, fusion_seed=seed)
+    assert labels(r2) == [(1, 40), (1, 40, 2)]
+    assert r2.total.tolist() == [-0.75, 0.25 + 1.2 * B0]
+
+
 # ------------------------------------------------------------------ top-o and lambda
 
 def test_lambda_cut_from_the_best_survivor():
