@@ -440,6 +440,51 @@ def test_random_small_lexicons_match_oracle(seed):
         check_parity(d, out, range(B), params=p, name=f"random-lexicon/{seed}", finalize=fin)
 
 
+@pytest.mark.parametrize("seed", range(10))
+def test_random_parameters_match_oracle(seed):
+    """Every decode parameter drawn at random (beam 1..256, sub-beams 1..4,
+    alpha, beta, gamma, omega, phi, theta, lambda, fusion interval and top F,
+    log-sum-exp or max recombination) over the 1k-, 20k- and 125k-word test
+    workloads (the last with ~300-word homophone sets), the first 60 frames:
+    the oracle's outputs, at the end of the utterance and live.  Odd seeds
+    also decode 300 copies of the batch, which takes the kernels for batches
+    beyond the CU count; every copy must equal the small batch's output."""
+    rng = np.random.default_rng(900 + seed)
+    name = ("t-c1k", "t-c20k", "t-c125k")[seed % 3]
+    base = load_workload(name, batch=4)
+    beam = int(rng.choice([1, 2, 5, 16, 33, 64, 100, 128, 200, 256]))
+    p = DecodeParams(
+        beam=beam, subbeams=int(rng.integers(1, 5)),
+        alpha=float(rng.choice([0.5, 0.6, 1.0])), beta=float(rng.choice([0.0, 0.75, 1.5])),
+        gamma=float(rng.choice([0.0, 1.0, 2.0])), omega=float(rng.choice([0.0, 0.5, 1.25])),
+        phi=float(rng.choice([0.5, 1.2])), theta=float(rng.choice([2.0, 8.0, 22.0, 1e30])),
+        lam=float(rng.choice([0.5, 4.0, 1e30])), fusion_interval=int(rng.choice([0, 1, 4, 9])),
+        fusion_top_f=int(rng.choice([0, 1, max(1, beam // 3)])))
+    merge_max = bool(rng.random() < 0.25)
+    T = min(60, base.logits.shape[1])
+    B = base.logits.shape[0]
+    lengths = np.minimum(base.lengths, T).astype(np.int32)
+    wl = base.workload.__class__(**{**base.workload.__dict__, "params": p})
+    d = WorkloadData(wl, base.lexicon, base.lm, np.ascontiguousarray(base.logits[:, :T]), lengths,
+                     base.targets[:, :T], base.words, base.fusion_seed)
+    lb_over = dict(merge=lbm.LB_MERGE_MAX) if merge_max else None
+    orc_over = dict(merge_max=1) if merge_max else None
+    for fin in (True, False):
+        say(f"[case] random parameters seed={seed} {name} {p} merge_max={merge_max} fin={fin}")
+        out = gpu_decode(d, params=p, finalize=fin, lb_overrides=lb_over)
+        check_parity(d, out, range(B), params=p, name=f"random-params/{seed}", finalize=fin,
+                     oracle_overrides=orc_over, min_hyps=0 if fin else 1)
+        if seed % 2:
+            big = 300
+            tile = lambda a: np.concatenate([a] * (big // B))
+            db = WorkloadData(wl, base.lexicon, base.lm, tile(d.logits), tile(lengths), tile(d.targets),
+                              d.words * (big // B), base.fusion_seed)
+            say(f"[case] random parameters seed={seed} B={big} fin={fin}")
+            outb = gpu_decode(db, params=p, finalize=fin, lb_overrides=lb_over)
+            for b in range(big):
+                assert outb[b][0] == out[b % B][0] and np.array_equal(outb[b][1], out[b % B][1]), b
+
+
 def test_gather_probe_reads_the_lines_it_names():
     """lb_measure_gather reads line mulhi(splitmix64(seed + i), lines) for
     gather i, 8 per thread, and writes each thread's XOR of the 16 words it
