@@ -448,7 +448,9 @@ def test_random_parameters_match_oracle(seed):
     workloads (the last with ~300-word homophone sets), the first 60 frames:
     the oracle's outputs, at the end of the utterance and live.  Odd seeds
     also decode 300 copies of the batch, which takes the kernels for batches
-    beyond the CU count; every copy must equal the small batch's output."""
+    beyond the CU count; every copy must equal the small batch's output.
+    Decoded in calls of a random number of frames (1..16, the streams' state
+    carried from call to call), the output equals the one-shot decode's."""
     rng = np.random.default_rng(900 + seed)
     name = ("t-c1k", "t-c20k", "t-c125k")[seed % 3]
     base = load_workload(name, batch=4)
@@ -461,6 +463,7 @@ def test_random_parameters_match_oracle(seed):
         lam=float(rng.choice([0.5, 4.0, 1e30])), fusion_interval=int(rng.choice([0, 1, 4, 9])),
         fusion_top_f=int(rng.choice([0, 1, max(1, beam // 3)])))
     merge_max = bool(rng.random() < 0.25)
+    chunk = int(rng.integers(1, 17))
     T = min(60, base.logits.shape[1])
     B = base.logits.shape[0]
     lengths = np.minimum(base.lengths, T).astype(np.int32)
@@ -474,6 +477,10 @@ def test_random_parameters_match_oracle(seed):
         out = gpu_decode(d, params=p, finalize=fin, lb_overrides=lb_over)
         check_parity(d, out, range(B), params=p, name=f"random-params/{seed}", finalize=fin,
                      oracle_overrides=orc_over, min_hyps=0 if fin else 1)
+        say(f"[case] random parameters seed={seed} in calls of {chunk} frames fin={fin}")
+        outc = gpu_decode(d, params=p, finalize=fin, chunk=chunk, lb_overrides=lb_over)
+        for b in range(B):
+            assert outc[b][0] == out[b][0] and np.array_equal(outc[b][1], out[b][1]), (b, chunk)
         if seed % 2:
             big = 300
             tile = lambda a: np.concatenate([a] * (big // B))
