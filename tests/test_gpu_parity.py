@@ -245,7 +245,7 @@ def test_crowded_boundary_bins(sigma, top_f):
             assert outb[b][0] == out[b % B][0] and np.array_equal(outb[b][1], out[b % B][1]), b
 
 
-@pytest.mark.parametrize("name", ["t-c20k", "t-c125k"])
+@pytest.mark.parametrize("name", ["t-c20k", "t-c125k", "t-k256"])
 def test_external_fusion_round_trip(name):
     """LB_FUSION_EXTERNAL: the decoder stops at every fusion event, exports the
     word sequences of the fused sub-beams, and applies the caller's scores.
