@@ -407,7 +407,7 @@ def test_max_recombination(name):
     assert any(len(a[1]) and len(b[1]) and abs(float(a[1][0]) - float(b[1][0])) > 1e-3 for a, b in zip(lse, mx))
 
 
-@pytest.mark.parametrize("name", ["t-c1k", "t-c125k"])
+@pytest.mark.parametrize("name", ["t-c1k", "t-c125k", "t-k256"])
 def test_raw_logits_log_softmax(name):
     """input = raw scores: each frame is log-softmax-normalised in the kernel.
     The raw rows are the log-probs plus a seeded per-frame shift."""
@@ -436,7 +436,7 @@ def test_pronunciation_variants():
         check_parity(d, out, range(B), name=f"variants/{'end' if fin else 'live'}", finalize=fin)
 
 
-@pytest.mark.parametrize("name", ["t-c1k", "t-c20k"])
+@pytest.mark.parametrize("name", ["t-c1k", "t-c20k", "t-k256"])
 def test_end_of_sentence_marks(name):
     """At LB_END every sub-beam takes its best end-of-sentence mark under the
     synthetic scorer; the mark is appended to the output words."""
