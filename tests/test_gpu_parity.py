@@ -425,15 +425,22 @@ def test_raw_logits_log_softmax(name):
 # ---------------------------------------------------------------- pronunciation variants, end-of-sentence marks
 
 
-def test_pronunciation_variants():
-    """A lexicon where a fifth of the words have a second spelling (App. I)."""
+@pytest.mark.parametrize("beam", [32, 256])
+def test_pronunciation_variants(beam):
+    """A lexicon where a fifth of the words have a second spelling (App. I),
+    at the workload's beam and at 256 with the top third fused."""
     d = load_workload("t-variants")
     B = d.logits.shape[0]
     assert d.lexicon.entry_word is not None and d.lexicon.n_words > d.lm.vocab_size - 3
-    say(f"[case] variants: B={B} entries={d.lexicon.n_words}")
+    p = d.workload.params
+    if beam != p.beam:
+        p = p.__class__(**{**p.__dict__, "beam": beam, "fusion_top_f": beam // 3})
+        d = WorkloadData(d.workload.__class__(**{**d.workload.__dict__, "params": p}), d.lexicon, d.lm,
+                         d.logits, d.lengths, d.targets, d.words, d.fusion_seed)
+    say(f"[case] variants: B={B} entries={d.lexicon.n_words} K={beam}")
     for fin in (True, False):
         out = gpu_decode(d, finalize=fin)
-        check_parity(d, out, range(B), name=f"variants/{'end' if fin else 'live'}", finalize=fin)
+        check_parity(d, out, range(B), name=f"variants/{beam}/{'end' if fin else 'live'}", finalize=fin)
 
 
 @pytest.mark.parametrize("name", ["t-c1k", "t-c20k", "t-k256"])
