@@ -24,7 +24,6 @@ namespace lb {
 namespace {
 
 constexpr double kNegInf = -HUGE_VAL;
-constexpr int kBins = 1024;         // score bins of the top-K selection
 constexpr int kBoundaryCap = 256;   // candidates resolved exactly inside the boundary bin
 constexpr int kMaxLevels = 16;      // refinement levels of the top-K selection
 constexpr uint32_t kGroupHeavy = 0x80000000u;  // query group scored through its explicit homophones
@@ -613,6 +612,11 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
   constexpr int NPM = KMAX * kMaxSub;  // (completed word, sub-beam) pairs per frame, at most
   constexpr int NPL = NPM < 256 ? NPM : 256;  // pairs grouped at once
   constexpr int NEB = NPL / kMaxSub;          // completed words per batch
+  // score bins of the top-K selection: 1024 at K = 256; 512 for the smaller
+  // beams' fewer candidates (c5: 25.69 against 25.83 ms with 1024; c4 9.91
+  // against 9.80 with 512)
+  constexpr int kBinBits = KMAX >= 256 ? 10 : 9;
+  constexpr int kBins = 1 << kBinBits;
   constexpr int SEL_BYTES = kBins * 4 + kBoundaryCap * 16;
   constexpr int LM_BYTES = 64 * NPL + 16;
   constexpr int UNI_BYTES = SEL_BYTES > LM_BYTES ? SEL_BYTES : LM_BYTES;
@@ -973,7 +977,7 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
       L0 = fmax(best - theta, lowest);
     }
     const double inv0 = U > L0 ? static_cast<double>(kBins) / (U - L0) : 0.0;
-    const int shift0 = U > L0 ? -1 : 64 - 10;
+    const int shift0 = U > L0 ? -1 : 64 - kBinBits;
     auto bin_score = [&](double hi, double inv, double s) -> int {
       const double x = (hi - s) * inv;
       return x >= static_cast<double>(kBins - 1) ? kBins - 1 : static_cast<int>(x);
@@ -997,7 +1001,7 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
     // finds the bin holding the need-th candidate of sHisto (sBucket, sAbove,
     // sBucketCnt) and, for bthr < kBins, the number of candidates in the bins
     // above bin bthr (sAthr); returns the number of binned candidates.  The
-    // first wavefront scans the bins, 16 per lane, so one barrier ends it.
+    // first wavefront scans the bins, kBins / 64 per lane, so one barrier ends it.
     auto find_bin = [&](int need_in, int bthr) -> int {
       constexpr int PERW = kBins / 64;
       static_assert(PERW % 4 == 0, "bins per lane in 16-B loads");
@@ -1200,7 +1204,7 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
       }
     };
     if (resolve) {
-      int key_shift = shift0 >= 0 ? shift0 - 10 : 64 - 10;
+      int key_shift = shift0 >= 0 ? shift0 - kBinBits : 64 - kBinBits;
       bool key_level = shift0 >= 0;
       int last_shift = shift0;  // shift of the deepest level (-1: score bins)
       while (cntb != need && cntb > kBoundaryCap && !(key_level && last_shift == 0) && nlev < kMaxLevels) {
@@ -1222,7 +1226,7 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
         lds_barrier();
         last_shift = sLvShift[L];
         key_level = last_shift >= 0;
-        if (key_level) key_shift -= 10;
+        if (key_level) key_shift -= kBinBits;
         for_bnd(L, [&](int, int v, double sc) { atomicAdd(&sHisto[bin_at(L, v, sc)], 1u); });
         lds_barrier();
         (void)find_bin(need, kBins);
