@@ -131,7 +131,7 @@ typedef struct lb_params {
                               appended to the output words (first of equals wins) */
   int32_t eos_ids[3];      /* the marks' LM word ids                              */
   int32_t heavy_homophones; /* trie nodes with at least this many words are scored
-                              through the explicit-continuation index (0 = 16,
+                              through the explicit-continuation index (0 = 3,
                               < 0 = never): per (context, node) only the homophones
                               that have an n-gram entry are looked up, the others
                               back off to their unigrams and are ranked by a walk

@@ -45,7 +45,7 @@ constexpr uint32_t kRootHist = 0;                      // empty word history
 constexpr double kLn10 = 2.302585092994045684017991454684364208;
 constexpr int kWordCountShift = 48;  // TrieNode::mask bits 48..63: words ending at the node
 constexpr int kMaxExplicit = 16;     // a heavy group with more explicit homophones takes the full path
-constexpr int kHeavyDefault = 16;    // default homophone count from which a node is heavy
+constexpr int kHeavyDefault = 3;     // default homophone count from which a node is heavy
 
 // overflow / error flag bits (DevState::flags)
 constexpr uint32_t kFlagArena = 1u;
