@@ -898,11 +898,16 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
       c_key = C.key[hi_];
       if (ln == 0) c_stay = sStay[hi_];
     }
-    // the slot of the separator on this lane (-1: none)
-    const int c_sep = ((kSep - 1 - ln) % LPB) == 0 ? (kSep - 1 - ln) / LPB : -1;
+    // the separator (symbol kSep = 1 + ln + LPB*k) can only be slot
+    // (kSep - 1) / LPB of lane (kSep - 1) % LPB: with k known at compile time
+    // (the unrolled slot loops) the bonus of every other slot is beta without
+    // a select
+    constexpr int kSepSlot = (kSep - 1) / LPB;
+    const bool sep_lane = ln == (kSep - 1) % LPB;
     // (the bonuses are read once here: inside the slot loops a constant-memory
     // load per slot would wait together with the LDS loads)
     const double bon_ph = P.beta, bon_sep = P.gamma;
+    auto bonus_at = [&](int k) -> double { return (k == kSepSlot && sep_lane) ? bon_sep : bon_ph; };
     // the repeat extension (the hypothesis' last symbol again, from its
     // blank-ending part) is a candidate of its own, position NC + 1, and its
     // slot is left out of the slot loops, whose extensions all start from pt
@@ -910,12 +915,12 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
     double c_rps = kNegInf;   // its score
     if (c_rep >= 0 && c_rep % LPB == 0 && ((c_rel >> c_rep) & 1ull)) {
       c_rk = c_rep / LPB;
-      c_rps = ((c_ab + sD[1 + ln + c_rep]) + (c_rk == c_sep ? bon_sep : bon_ph)) + c_L;
+      c_rps = ((c_ab + sD[1 + ln + c_rep]) + bonus_at(c_rk)) + c_L;
       c_rel &= ~(1ull << c_rep);
     }
     auto score_now = [&](int k) -> double {
       const bool valid = (c_rel >> (LPB * k)) & 1ull;
-      const double sc = ((c_p + sD[1 + ln + LPB * k]) + (k == c_sep ? bon_sep : bon_ph)) + c_L;
+      const double sc = ((c_p + sD[1 + ln + LPB * k]) + bonus_at(k)) + c_L;
       return valid ? sc : kNegInf;
     };
     auto key_of = [&](int v) -> uint64_t { return v == 0 ? c_key : prefix_step(c_key, v); };
@@ -1066,7 +1071,7 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
         // branch-free: the score and bin of the slot, valid or not (a bin in
         // range either way), then a select
         const bool valid = (c_rel >> (LPB * k)) & 1ull;
-        const double sc = ((c_p + sD[1 + ln + LPB * k]) + (k == c_sep ? bon_sep : bon_ph)) + c_L;
+        const double sc = ((c_p + sD[1 + ln + LPB * k]) + bonus_at(k)) + c_L;
         const bool in = valid && sc >= L0;
         const uint32_t bn = in ? static_cast<uint32_t>(bin_lv0(sc)) : 0xFFFFu;
         if (k & 1)
