@@ -257,7 +257,7 @@ __host__ __device__ inline uint64_t bucket_of(uint64_t key, uint64_t nbuckets) {
 // rounded in 99 % of them, never off by more than 0.7 ulp; about half the
 // instructions of the general routine, which a two-input log-sum-exp in
 // every hypothesis of every frame makes worth it.
-__device__ inline double log1p_unit(double e) {
+__host__ __device__ inline double log1p_unit(double e) {
   const double den = 2.0 + e;
   const double err = e - (den - 2.0);  // 2 + e == den + err exactly
   const double r = 1.0 / den;

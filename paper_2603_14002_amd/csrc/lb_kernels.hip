@@ -853,14 +853,22 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
     if constexpr (kOnePass) {
       // per wavefront: an upper bound of every candidate (sRedB[w]), the best
       // stay (sRedB[NW + w]) and the lowest (sRedB[2 NW + w]), for the top-K's
-      // bin range
-      double hi = fmax(st, up), nlo = -st;
-      wave_minmax(&hi, &nlo);
-      const double nmin = wave_max(tid < n ? -st : -HUGE_VAL);
-      if (lane == 0) {
-        sRedB[wave] = hi;
-        sRedB[NW + wave] = -nlo;
-        sRedB[2 * NW + wave] = -nmin;
+      // bin range (a wavefront past the last hypothesis, e.g. the upper half
+      // of the block when there is one thread per hypothesis here but two
+      // lanes per hypothesis later, has the neutral values without reducing)
+      if (wave * 64 < n) {
+        double hi = fmax(st, up), nlo = -st;
+        wave_minmax(&hi, &nlo);
+        const double nmin = wave_max(tid < n ? -st : -HUGE_VAL);
+        if (lane == 0) {
+          sRedB[wave] = hi;
+          sRedB[NW + wave] = -nlo;
+          sRedB[2 * NW + wave] = -nmin;
+        }
+      } else if (lane == 0) {
+        sRedB[wave] = kNegInf;
+        sRedB[NW + wave] = kNegInf;
+        sRedB[2 * NW + wave] = HUGE_VAL;
       }
     }
     lds_barrier();
