@@ -257,23 +257,36 @@ __host__ __device__ inline uint64_t bucket_of(uint64_t key, uint64_t nbuckets) {
 // rounded in 99 % of them, never off by more than 0.7 ulp; about half the
 // instructions of the general routine, which a two-input log-sum-exp in
 // every hypothesis of every frame makes worth it.
-__host__ __device__ inline double log1p_unit(double e) {
+// The series' coefficient of s^(2n+3) is 1/(2n+3), n = 0..kAtanhTerms-1;
+// coef(n) returns it (a compile-time constant, or a table the caller keeps:
+// the decode kernel reads them from LDS, which loads them into vector
+// registers without a vector move per constant half).
+constexpr int kAtanhTerms = 16;
+template <class Coef>
+__host__ __device__ inline double log1p_unit(double e, Coef coef) {
   const double den = 2.0 + e;
   const double err = e - (den - 2.0);  // 2 + e == den + err exactly
   const double r = 1.0 / den;
   const double q = e * r;
   const double lo = fma(-q, err, fma(-q, den, e)) * r;
   const double u = q * q;
-  double p = 1.0 / 33.0;
+  double p = coef(kAtanhTerms - 1);
 #pragma unroll
-  for (int n = 14; n >= 0; --n) p = fma(p, u, 1.0 / (2 * n + 3));
+  for (int n = kAtanhTerms - 2; n >= 0; --n) p = fma(p, u, coef(n));
   return 2.0 * q + 2.0 * (lo + (q * u) * p);
 }
+__host__ __device__ inline double log1p_unit(double e) {
+  return log1p_unit(e, [](int n) { return 1.0 / (2 * n + 3); });
+}
 
-__device__ inline double lse2(double x, double y) {
+template <class Coef>
+__device__ inline double lse2(double x, double y, Coef coef) {
   if (x == -HUGE_VAL && y == -HUGE_VAL) return -HUGE_VAL;
   const double m = x > y ? x : y;
-  return m + log1p_unit(exp(-fabs(x - y)));
+  return m + log1p_unit(exp(-fabs(x - y)), coef);
+}
+__device__ inline double lse2(double x, double y) {
+  return lse2(x, y, [](int n) { return 1.0 / (2 * n + 3); });
 }
 
 // Synthetic word-bigram fusion score Bg(a, b), natural log.

@@ -657,6 +657,8 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
   __shared__ unsigned long long sCnt[7];
   // phase cycles of thread 0 (kPh*), and the last timestamp
   __shared__ unsigned long long sPhase[kPhases + 1];
+  // the log-sum-exp's series coefficients (log1p_unit), read from LDS
+  __shared__ double sAtanh[kAtanhTerms];
   const bool timing = (opts & kOptPhaseTimers) != 0;
   // closes the current phase as phase k (taken after the barrier that ends it)
   auto mark = [&](int k) {
@@ -718,6 +720,7 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
     B0.woff[tid] = tn.word_off;
   }
   if (tid < 7) sCnt[tid] = 0;
+  if (tid < kAtanhTerms) sAtanh[tid] = 1.0 / (2 * tid + 3);
   if (timing && tid == 0) {
     for (int k = 0; k < kPhases; ++k) sPhase[k] = 0;
     sPhase[kPhases] = __builtin_amdgcn_s_memtime();
@@ -831,7 +834,7 @@ __global__ __launch_bounds__(KMAX * LPB) __attribute__((amdgpu_waves_per_eu(WPE)
       double x = rep, y = ext, anb2 = 0.0;
 #pragma unroll 1
       for (int pass = 0; pass < 2; ++pass) {
-        const double l = P.merge_max ? fmax(x, y) : lse2(x, y);
+        const double l = P.merge_max ? fmax(x, y) : lse2(x, y, [&](int k) { return sAtanh[k]; });
         if (pass == 0) {
           anb2 = l;
           x = ab2;
